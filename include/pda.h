@@ -1,0 +1,167 @@
+/*
+ * pda.h -- C interface of the MI355X (gfx950) paged-KV decode-attention library.
+ *
+ * What it computes. Rollout decoding -- one new token per live sequence per
+ * step over a long-tailed mix of sequence lengths -- is the phase of RLVR
+ * training whose throughput collapses in the tail (paper Sec. 2.2; decode
+ * throughput per GPU in Sec. 6.2, Fig. e2e-conv(c)). Each decode step of the
+ * Transformer models it serves (Sec. 1) attends the new token's query to the
+ * keys and values cached for its sequence, read through a block table as in
+ * the paged KV-cache memory management the paper cites in Sec. 8 (vLLM):
+ *
+ *     out[b, h, :] = softmax(softmax_scale * K_b q[b, h]) V_b
+ *
+ * where K_b and V_b hold tokens 0 .. seq_lens[b]-1 of KV head h / G,
+ * G = num_q_heads / num_kv_heads (query heads g*G .. g*G+G-1 share KV head g).
+ *
+ * All entry points are plain C; every pointer argument of
+ * pda_paged_decode_attention is a device pointer (HBM) owned by the caller.
+ */
+#ifndef PDA_H
+#define PDA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PDA_VERSION 1
+
+/* Element types. PDA_DTYPE_FP8_E4M3 is the OCP 8-bit E4M3 format without
+ * infinities ("e4m3fn": bias 7, max 448, NaN = S.1111.111). */
+typedef enum pda_dtype {
+  PDA_DTYPE_F32 = 0,
+  PDA_DTYPE_BF16 = 1,
+  PDA_DTYPE_FP8_E4M3 = 2
+} pda_dtype;
+
+/* Return codes. Negative values are errors; pda_last_error() has the text. */
+typedef enum pda_status {
+  PDA_OK = 0,
+  PDA_EINVAL = -1,        /* null pointer, bad size, bad dtype combination      */
+  PDA_EUNSUPPORTED = -2,  /* valid but not implemented (head_dim, block size...) */
+  PDA_EHIP = -3,          /* a HIP runtime call or a kernel launch failed        */
+  PDA_ENOMEM = -4         /* the library's workspace could not be allocated      */
+} pda_status;
+
+/* Kernel family. AUTO picks MFMA for bf16/fp8 caches with a GQA group of at
+ * least 4 query heads and the vector kernel otherwise. */
+typedef enum pda_variant {
+  PDA_VARIANT_AUTO = 0,
+  PDA_VARIANT_VECTOR = 1, /* VALU dot products with wavefront (DPP) reductions */
+  PDA_VARIANT_MFMA = 2    /* bf16 matrix-core QK^T and PV per GQA group        */
+} pda_variant;
+
+/* Sizes and element types of one decode step.
+ *
+ *   q            [num_seqs, num_q_heads, head_dim]            q_dtype, contiguous
+ *   k_cache      [num_blocks, num_kv_heads, block_size, head_dim] kv_dtype, contiguous
+ *                (token-major tile per (block, KV head))
+ *   v_cache      [num_blocks, num_kv_heads, head_dim, block_size] kv_dtype, contiguous
+ *                (dim-major tile per (block, KV head))
+ *   block_table  [num_seqs, max_blocks_per_seq] int32 physical block ids; entry j
+ *                of row b holds tokens 16j .. 16j+15 of sequence b; entries at or
+ *                past ceil(seq_lens[b] / 16) are never read
+ *   seq_lens     [num_seqs] int32, 0 <= seq_lens[b] <= max_seq_len
+ *   kv_scales    [2, num_blocks, num_kv_heads] fp32 dequantisation scales, index 0
+ *                for K and 1 for V; required for fp8 caches, ignored otherwise
+ *   out          [num_seqs, num_q_heads, head_dim] out_dtype, contiguous
+ *
+ * max_seq_len is a host-side upper bound on every seq_lens[b] (0 means
+ * max_blocks_per_seq * block_size). Lengths above it, above
+ * max_blocks_per_seq * block_size, or below 0 are clamped into range on the
+ * device and reported by pda_read_device_status(); so are block-table entries
+ * outside [0, num_blocks), whose blocks are then skipped.
+ */
+typedef struct pda_problem {
+  int32_t num_seqs;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;            /* 64 or 128 */
+  int32_t block_size;          /* tokens per KV block: 16 */
+  int32_t max_blocks_per_seq;  /* row length (and stride) of block_table */
+  int64_t num_blocks;          /* physical blocks in k_cache / v_cache */
+  int32_t max_seq_len;
+  int32_t q_dtype;             /* pda_dtype: F32 or BF16 */
+  int32_t kv_dtype;            /* pda_dtype: F32 (needs F32 q), BF16 or FP8_E4M3 (need BF16 q) */
+  int32_t out_dtype;           /* pda_dtype of out: q_dtype or F32 (accumulation stays fp32) */
+} pda_problem;
+
+/* Optional tuning knobs; pass NULL for the defaults (all zero). */
+typedef struct pda_options {
+  int32_t variant;             /* pda_variant */
+  int32_t waves_per_cu;        /* persistent waves launched per compute unit; 0 = auto */
+  int32_t min_blocks_per_wave; /* smallest share of KV blocks one wave takes; 0 = auto */
+} pda_options;
+
+/* Host-side plan of one call: what pda_paged_decode_attention would launch. */
+typedef struct pda_plan_info {
+  int32_t variant;             /* the kernel family that runs (never AUTO) */
+  int32_t waves;               /* persistent waves (one per workgroup) */
+  int32_t group_size;          /* G = num_q_heads / num_kv_heads */
+  int64_t workspace_bytes;     /* library-owned device workspace this call needs */
+} pda_plan_info;
+
+/*
+ * One batched decode-attention step, enqueued on `stream` (a hipStream_t; NULL
+ * is the null stream). Asynchronous: results are valid once the stream has
+ * reached this point. Work is split so every persistent wave reads an equal
+ * share of the step's KV blocks; a sequence split between waves is finished by
+ * a log-sum-exp combine kernel on the same stream.
+ *
+ * Ownership: the caller owns every buffer; the library keeps no pointer to
+ * them after returning. It owns one device workspace per (device, stream),
+ * grown on demand (growth synchronises that stream) and released by
+ * pda_release_workspaces().
+ *
+ * Errors: all argument checks run on the host before any HIP call, so invalid
+ * arguments return PDA_EINVAL / PDA_EUNSUPPORTED without touching a device.
+ * Returns PDA_OK once the kernels are enqueued.
+ *
+ * Thread safety: calls on different streams may run concurrently; calls on
+ * one stream from several threads are serialised by an internal lock.
+ */
+int pda_paged_decode_attention(const void* q,
+                               const void* k_cache,
+                               const void* v_cache,
+                               const int32_t* block_table,
+                               const int32_t* seq_lens,
+                               const float* kv_scales,
+                               void* out,
+                               float softmax_scale,
+                               const pda_problem* problem,
+                               const pda_options* options,
+                               hipStream_t stream);
+
+/* Validate `problem` / `options` and describe the launch, on the host only
+ * (no HIP call). `num_compute_units` sizes the persistent grid (MI355X: 256).
+ * Returns the same error codes as pda_paged_decode_attention. */
+int pda_query_plan(const pda_problem* problem,
+                   const pda_options* options,
+                   float softmax_scale,
+                   int32_t num_compute_units,
+                   pda_plan_info* info);
+
+/* Wait for `stream`, then return (and clear) the device-side status bits that
+ * calls on it recorded: 1 = a sequence length was clamped, 2 = a block-table
+ * entry outside [0, num_blocks) was skipped. 0 when clean; negative on error. */
+int pda_read_device_status(hipStream_t stream);
+
+/* Free every workspace the library holds (waits for the owning streams). */
+int pda_release_workspaces(void);
+
+/* Text of the last error on the calling thread ("" if none). */
+const char* pda_last_error(void);
+
+/* PDA_VERSION of the built library. */
+int pda_version(void);
+
+#ifdef __cplusplus
+}  /* extern "C" */
+#endif
+
+#endif  /* PDA_H */

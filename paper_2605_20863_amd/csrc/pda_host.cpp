@@ -1,0 +1,354 @@
+// Host side of the C interface in include/pda.h: argument validation (pure
+// host code, no HIP call), the launch plan, the per-(device, stream)
+// workspace and the two kernel launches of one decode step.
+
+#include "pda.h"
+#include "pda_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <utility>
+
+namespace {
+
+thread_local std::string g_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return code;
+}
+
+int fail_hip(hipError_t e, const char* what) {
+  return fail(PDA_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kDefaultWavesPerCu = 8;   // upper bound used by pda_query_plan
+constexpr int kDefaultMinShare = 8;     // blocks: below this a wave's fixed costs dominate
+constexpr int64_t kAlign = 256;
+
+int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Plan {
+  pda::Variant variant;
+  pda::KvType kv;
+  int G;
+  int len_cap;
+  int waves_per_cu;  // 0 = decide from occupancy at launch
+  int min_share;
+};
+
+// Validate everything that does not need a device. Returns PDA_OK or an error.
+int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, Plan* plan) {
+  if (!pr) return fail(PDA_EINVAL, "problem is NULL");
+  if (pr->num_seqs < 0) return fail(PDA_EINVAL, "num_seqs = %d < 0", pr->num_seqs);
+  if (pr->num_q_heads < 1 || pr->num_kv_heads < 1)
+    return fail(PDA_EINVAL, "num_q_heads = %d and num_kv_heads = %d must be >= 1", pr->num_q_heads,
+                pr->num_kv_heads);
+  if (pr->num_q_heads % pr->num_kv_heads)
+    return fail(PDA_EINVAL, "num_q_heads = %d is not a multiple of num_kv_heads = %d", pr->num_q_heads,
+                pr->num_kv_heads);
+  const int G = pr->num_q_heads / pr->num_kv_heads;
+  if (G > pda::kMaxGroup)
+    return fail(PDA_EUNSUPPORTED, "GQA group of %d query heads per KV head (max %d)", G, pda::kMaxGroup);
+  if (pr->head_dim != 64 && pr->head_dim != 128)
+    return fail(PDA_EUNSUPPORTED, "head_dim = %d (supported: 64, 128)", pr->head_dim);
+  if (pr->block_size != pda::kBlockSize)
+    return fail(PDA_EUNSUPPORTED, "block_size = %d (supported: 16)", pr->block_size);
+  if (pr->max_blocks_per_seq < 1) return fail(PDA_EINVAL, "max_blocks_per_seq = %d < 1", pr->max_blocks_per_seq);
+  if (pr->num_blocks < 1) return fail(PDA_EINVAL, "num_blocks = %lld < 1", (long long)pr->num_blocks);
+  const int64_t table_tokens = (int64_t)pr->max_blocks_per_seq * pda::kBlockSize;
+  if (table_tokens > INT32_MAX) return fail(PDA_EINVAL, "max_blocks_per_seq * 16 overflows int32");
+  if ((int64_t)pr->num_seqs * pr->max_blocks_per_seq * pr->num_kv_heads > INT32_MAX)
+    return fail(PDA_EINVAL, "num_seqs * max_blocks_per_seq * num_kv_heads overflows int32");
+  if ((int64_t)pr->num_seqs * pr->num_q_heads > INT32_MAX) return fail(PDA_EINVAL, "num_seqs * num_q_heads too large");
+  if (pr->max_seq_len < 0) return fail(PDA_EINVAL, "max_seq_len = %d < 0", pr->max_seq_len);
+  if (pr->max_seq_len > table_tokens)
+    return fail(PDA_EINVAL, "max_seq_len = %d exceeds max_blocks_per_seq * 16 = %lld", pr->max_seq_len,
+                (long long)table_tokens);
+  // every cache byte offset must fit int64 (and the tile index p * Hkv + kvh)
+  const int64_t tile = (int64_t)pda::kBlockSize * pr->head_dim * 4;
+  if (pr->num_blocks > INT64_MAX / pr->num_kv_heads / tile) return fail(PDA_EINVAL, "num_blocks too large");
+
+  const int qd = pr->q_dtype, kd = pr->kv_dtype;
+  if (qd != PDA_DTYPE_F32 && qd != PDA_DTYPE_BF16)
+    return fail(qd == PDA_DTYPE_FP8_E4M3 ? PDA_EUNSUPPORTED : PDA_EINVAL, "q_dtype = %d (supported: F32, BF16)", qd);
+  if (kd != PDA_DTYPE_F32 && kd != PDA_DTYPE_BF16 && kd != PDA_DTYPE_FP8_E4M3)
+    return fail(PDA_EINVAL, "kv_dtype = %d is not a pda_dtype", kd);
+  if (kd == PDA_DTYPE_F32 && qd != PDA_DTYPE_F32)
+    return fail(PDA_EUNSUPPORTED, "an f32 KV cache needs f32 q");
+  if (kd != PDA_DTYPE_F32 && qd != PDA_DTYPE_BF16)
+    return fail(PDA_EUNSUPPORTED, "a bf16 or fp8 KV cache needs bf16 q");
+  if (pr->out_dtype != qd && pr->out_dtype != PDA_DTYPE_F32)
+    return fail(PDA_EINVAL, "out_dtype = %d (must be q_dtype or F32)", pr->out_dtype);
+  if (!std::isfinite(softmax_scale)) return fail(PDA_EINVAL, "softmax_scale is not finite");
+
+  int variant = op ? op->variant : PDA_VARIANT_AUTO;
+  if (variant != PDA_VARIANT_AUTO && variant != PDA_VARIANT_VECTOR && variant != PDA_VARIANT_MFMA)
+    return fail(PDA_EINVAL, "options.variant = %d is not a pda_variant", variant);
+  if (variant == PDA_VARIANT_AUTO)
+    variant = (kd != PDA_DTYPE_F32 && G >= 4) ? PDA_VARIANT_MFMA : PDA_VARIANT_VECTOR;
+  if (variant == PDA_VARIANT_MFMA && kd == PDA_DTYPE_F32)
+    return fail(PDA_EUNSUPPORTED, "the MFMA kernel needs a bf16 or fp8 KV cache");
+  if (variant == PDA_VARIANT_VECTOR && G > pda::kMaxGroupVector)
+    return fail(PDA_EUNSUPPORTED, "the vector kernel handles at most %d query heads per KV head (got %d)",
+                pda::kMaxGroupVector, G);
+  if (op && (op->waves_per_cu < 0 || op->waves_per_cu > 64))
+    return fail(PDA_EINVAL, "options.waves_per_cu = %d (0..64)", op->waves_per_cu);
+  if (op && op->min_blocks_per_wave < 0)
+    return fail(PDA_EINVAL, "options.min_blocks_per_wave = %d < 0", op->min_blocks_per_wave);
+
+  plan->variant = variant == PDA_VARIANT_MFMA ? pda::Variant::Mfma : pda::Variant::Vector;
+  plan->kv = kd == PDA_DTYPE_F32 ? pda::KvType::F32 : (kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8);
+  plan->G = G;
+  plan->len_cap = pr->max_seq_len > 0 ? pr->max_seq_len : (int)table_tokens;
+  plan->waves_per_cu = op ? op->waves_per_cu : 0;
+  plan->min_share = (op && op->min_blocks_per_wave > 0) ? op->min_blocks_per_wave : kDefaultMinShare;
+  return PDA_OK;
+}
+
+struct Layout {
+  int64_t hdr, cum, m, l, acc, total;
+};
+
+Layout workspace_layout(const pda_problem* pr, int G, int waves) {
+  Layout w;
+  const int64_t slots = pda::partial_slots(pr->num_seqs, pr->num_kv_heads, waves);
+  w.hdr = 0;
+  w.cum = align_up(pda::kHdrWords * 4);
+  w.m = w.cum + align_up((int64_t)pr->num_seqs * 4);
+  w.l = w.m + align_up(slots * G * 4);
+  w.acc = w.l + align_up(slots * G * 4);
+  w.total = w.acc + align_up(slots * G * pr->head_dim * 4);
+  return w;
+}
+
+// ------------------------------------------------------------- device state
+
+struct DeviceInfo {
+  bool ok = false;
+  int cus = 0;
+  std::string arch;
+};
+
+struct Workspace {
+  std::mutex mu;
+  void* ptr = nullptr;
+  int64_t bytes = 0;
+};
+
+std::mutex g_mu;
+std::map<int, DeviceInfo> g_devices;
+std::map<std::pair<int, hipStream_t>, std::unique_ptr<Workspace>> g_workspaces;
+std::map<std::tuple<int, int, int, int, int>, int> g_occupancy;
+
+int device_info(int dev, DeviceInfo* out) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_devices.find(dev);
+  if (it != g_devices.end()) {
+    *out = it->second;
+    return PDA_OK;
+  }
+  DeviceInfo d;
+  hipDeviceProp_t prop;
+  hipError_t e = hipGetDeviceProperties(&prop, dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDeviceProperties");
+  d.cus = prop.multiProcessorCount;
+  d.arch = prop.gcnArchName;
+  d.ok = d.arch.rfind("gfx950", 0) == 0;
+  g_devices[dev] = d;
+  *out = d;
+  return PDA_OK;
+}
+
+int occupancy(int dev, pda::Variant v, pda::KvType kv, int D, int G, int* wgs) {
+  const int gb = v == pda::Variant::Mfma ? 16 : (G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8);
+  auto key = std::make_tuple(dev, (int)v, (int)kv, D, gb);
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_occupancy.find(key);
+    if (it != g_occupancy.end()) {
+      *wgs = it->second;
+      return PDA_OK;
+    }
+  }
+  int n = 0;
+  hipError_t e = pda::decode_occupancy(v, kv, D, G, &n);
+  if (e != hipSuccess) return fail_hip(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+  if (n < 1) n = 1;
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_occupancy[key] = n;
+  *wgs = n;
+  return PDA_OK;
+}
+
+Workspace* workspace_for(int dev, hipStream_t s) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto& slot = g_workspaces[std::make_pair(dev, s)];
+  if (!slot) slot.reset(new Workspace);
+  return slot.get();
+}
+
+// Grow ws (caller holds ws->mu) to at least `bytes`; growth waits for `s`.
+int ensure_workspace(Workspace* ws, int64_t bytes, hipStream_t s) {
+  if (ws->bytes >= bytes) return PDA_OK;
+  hipError_t e;
+  if (ws->ptr) {
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+    if ((e = hipFree(ws->ptr)) != hipSuccess) return fail_hip(e, "hipFree");
+    ws->ptr = nullptr;
+    ws->bytes = 0;
+  }
+  const int64_t want = bytes + bytes / 4;  // headroom so small growth does not reallocate
+  if ((e = hipMalloc(&ws->ptr, (size_t)want)) != hipSuccess) {
+    ws->ptr = nullptr;
+    return fail(PDA_ENOMEM, "hipMalloc(%lld) of the workspace: %s", (long long)want, hipGetErrorString(e));
+  }
+  ws->bytes = want;
+  if ((e = hipMemsetAsync(ws->ptr, 0, pda::kHdrWords * 4, s)) != hipSuccess) return fail_hip(e, "hipMemsetAsync");
+  return PDA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int pda_version(void) { return PDA_VERSION; }
+
+const char* pda_last_error(void) { return g_error.c_str(); }
+
+int pda_query_plan(const pda_problem* problem, const pda_options* options, float softmax_scale,
+                   int32_t num_compute_units, pda_plan_info* info) {
+  g_error.clear();
+  if (!info) return fail(PDA_EINVAL, "info is NULL");
+  if (num_compute_units < 1) return fail(PDA_EINVAL, "num_compute_units = %d < 1", num_compute_units);
+  Plan plan;
+  int rc = validate(problem, options, softmax_scale, &plan);
+  if (rc != PDA_OK) return rc;
+  const int wpc = plan.waves_per_cu > 0 ? plan.waves_per_cu : kDefaultWavesPerCu;
+  info->variant = plan.variant == pda::Variant::Mfma ? PDA_VARIANT_MFMA : PDA_VARIANT_VECTOR;
+  info->waves = num_compute_units * wpc;
+  info->group_size = plan.G;
+  info->workspace_bytes = workspace_layout(problem, plan.G, info->waves).total;
+  return PDA_OK;
+}
+
+int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                               const int32_t* block_table, const int32_t* seq_lens, const float* kv_scales,
+                               void* out, float softmax_scale, const pda_problem* problem,
+                               const pda_options* options, hipStream_t stream) {
+  g_error.clear();
+  Plan plan;
+  int rc = validate(problem, options, softmax_scale, &plan);
+  if (rc != PDA_OK) return rc;
+  if (problem->num_seqs == 0) return PDA_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
+    return fail(PDA_EINVAL, "a required pointer (q, k_cache, v_cache, block_table, seq_lens, out) is NULL");
+  if (problem->kv_dtype == PDA_DTYPE_FP8_E4M3 && !kv_scales)
+    return fail(PDA_EINVAL, "an fp8 KV cache needs kv_scales");
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  DeviceInfo di;
+  if ((rc = device_info(dev, &di)) != PDA_OK) return rc;
+  if (!di.ok) return fail(PDA_EUNSUPPORTED, "device %d is %s; this library is built for gfx950", dev, di.arch.c_str());
+
+  int wpc = plan.waves_per_cu;
+  if (wpc == 0) {
+    if ((rc = occupancy(dev, plan.variant, plan.kv, problem->head_dim, plan.G, &wpc)) != PDA_OK) return rc;
+    if (wpc > kDefaultWavesPerCu) wpc = kDefaultWavesPerCu;
+  }
+  const int waves = di.cus * wpc;
+  const Layout lay = workspace_layout(problem, plan.G, waves);
+
+  Workspace* ws = workspace_for(dev, stream);
+  std::lock_guard<std::mutex> lk(ws->mu);
+  if ((rc = ensure_workspace(ws, lay.total, stream)) != PDA_OK) return rc;
+  char* base = static_cast<char*>(ws->ptr);
+
+  pda::DecodeArgs a;
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.block_table = block_table;
+  a.seq_lens = seq_lens;
+  a.kv_scales = kv_scales;
+  a.out = out;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.B = problem->num_seqs;
+  a.Hq = problem->num_q_heads;
+  a.Hkv = problem->num_kv_heads;
+  a.G = plan.G;
+  a.D = problem->head_dim;
+  a.max_blocks = problem->max_blocks_per_seq;
+  a.num_blocks = problem->num_blocks;
+  a.len_cap = plan.len_cap;
+  a.min_share = plan.min_share;
+  a.waves = waves;
+  a.out_bf16 = problem->out_dtype == PDA_DTYPE_BF16;
+  a.hdr = reinterpret_cast<int32_t*>(base + lay.hdr);
+  a.share = a.hdr + 1;
+  a.cum = reinterpret_cast<int32_t*>(base + lay.cum);
+  a.ws_m = reinterpret_cast<float*>(base + lay.m);
+  a.ws_l = reinterpret_cast<float*>(base + lay.l);
+  a.ws_acc = reinterpret_cast<float*>(base + lay.acc);
+
+  if ((e = pda::launch_decode(a, plan.variant, plan.kv, stream)) != hipSuccess)
+    return fail_hip(e, "decode kernel launch");
+  if ((e = pda::launch_combine(a, stream)) != hipSuccess) return fail_hip(e, "combine kernel launch");
+  return PDA_OK;
+}
+
+int pda_read_device_status(hipStream_t stream) {
+  g_error.clear();
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  Workspace* ws = workspace_for(dev, stream);
+  std::lock_guard<std::mutex> lk(ws->mu);
+  if ((e = hipStreamSynchronize(stream)) != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+  if (!ws->ptr) return 0;
+  int32_t word = 0;
+  int32_t* hdr = static_cast<int32_t*>(ws->ptr) + pda::kHdrStatus;
+  if ((e = hipMemcpy(&word, hdr, 4, hipMemcpyDeviceToHost)) != hipSuccess) return fail_hip(e, "hipMemcpy");
+  if (word && (e = hipMemset(hdr, 0, 4)) != hipSuccess) return fail_hip(e, "hipMemset");
+  return word;
+}
+
+int pda_release_workspaces(void) {
+  g_error.clear();
+  std::lock_guard<std::mutex> lk(g_mu);
+  int rc = PDA_OK;
+  int cur = 0;
+  const bool have_dev = hipGetDevice(&cur) == hipSuccess;
+  for (auto& kv : g_workspaces) {
+    Workspace* ws = kv.second.get();
+    std::lock_guard<std::mutex> wl(ws->mu);
+    if (!ws->ptr) continue;
+    hipError_t e = hipSetDevice(kv.first.first);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipFree(ws->ptr);
+    if (e != hipSuccess) rc = fail_hip(e, "releasing a workspace");
+    ws->ptr = nullptr;
+    ws->bytes = 0;
+  }
+  g_workspaces.clear();
+  if (have_dev) (void)hipSetDevice(cur);
+  return rc;
+}
+
+}  // extern "C"

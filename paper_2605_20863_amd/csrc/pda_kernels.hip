@@ -1,0 +1,867 @@
+// HIP kernels for batched paged-KV decode attention on MI355X (gfx950, CDNA4).
+//
+// One decode step computes, for every sequence b and query head h,
+//     out[b, h] = softmax(scale * K_b q[b, h]) V_b
+// over the sequence's cached tokens, read through its block table (the paged
+// KV cache of the vLLM work cited in the paper's Sec. 8). Rollout decoding has
+// a long-tailed length mix (Sec. 2.2), so the work split must not depend on
+// how lengths are distributed:
+//
+// * Stream-K split. The (sequence, KV head) units are laid end to end as one
+//   stream of 16-token block-heads (sequence-major, KV head minor). Wave w of a
+//   persistent grid takes the contiguous range [w*Q, (w+1)*Q) of that stream,
+//   Q = ceil(total / waves). Every wave reads the same number of KV bytes, no
+//   matter how lengths are distributed. A wave whose range covers a whole unit
+//   writes the normalised output; otherwise it writes the unit's partial
+//   softmax state (m, l, acc) to slot (unit + wave), and the combine kernel
+//   merges a unit's partials with log-sum-exp rescaling. Every wave plans its
+//   own range from seq_lens (a prefix sum over sequences), so one call is two
+//   launches and needs neither atomics nor a planning kernel.
+//
+// * Two wave kernels share that driver:
+//   - MFMA (bf16 or fp8 cache, bf16 q): per pair of 16-token blocks,
+//     S^T[16 tok x 16 heads] = K[16 x D] . Q^T[D x 16] on v_mfma_f32_16x16x32_bf16
+//     (the GQA group's G <= 16 heads padded to 16 columns), online softmax on
+//     the accumulator registers, then O^T[D x 16] += V^T[D x 32 tok] . P^T[32 x 16].
+//     The accumulator layout of S^T already holds, per lane, the 4+4 token
+//     weights that the P^T operand needs, so P never moves between lanes. The
+//     price is the dim-major V tile [D][16] in the cache layout. P is split
+//     into two bf16 terms (hi + lo) so that rounding P costs ~2^-17, not 2^-9.
+//   - Vector (any cache dtype, G <= 8): each 16-lane row owns 4 tokens; QK dot
+//     products are lane-partial FMAs reduced across the row with DPP row
+//     rotations; PV uses the same 4 tokens per row, so no LDS is needed.
+//
+// * fp8 (OCP e4m3) caches are dequantised in registers: codes convert exactly
+//   to f32 / bf16; the per-(block, KV head) K scale multiplies that block's
+//   logits and the V scale multiplies its softmax weights.
+//
+// * Masking selects, never multiplies: tokens at or past seq_len get logit
+//   -inf and their V elements are replaced by 0, so NaN poison in unused cache
+//   slots cannot leak (0 * NaN = NaN).
+
+#include "pda_internal.h"
+
+#include <stdint.h>
+
+namespace pda {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kNegInf = -__builtin_inff();
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ------------------------------------------------------------- conversions
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xFFFF0000u); }
+
+// Two e4m3 codes of w (bytes 0,1 or 2,3) -> two f32, exactly.
+template <bool HI>
+__device__ __forceinline__ f32x2 fp8_pair(uint32_t w) {
+  return __builtin_amdgcn_cvt_pk_f32_fp8((int)w, HI);
+}
+
+// Four e4m3 codes -> four bf16 (two words), exactly (every e4m3 value is a
+// bf16 value); one v_cvt_scalef32_pk_bf16_fp8 per pair, scale 1.
+__device__ __forceinline__ u32x2 fp8x4_to_bf16x4(uint32_t w) {
+  u32x2 r;
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, false));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, true));
+  return r;
+}
+
+// f32 -> bf16 bits, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+template <typename T>
+__device__ __forceinline__ T ld(const void* p) {
+  return *reinterpret_cast<const T*>(p);
+}
+
+// Inclusive prefix sum over the 64 lanes of the wave.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (l >= o) x += y;
+  }
+  return x;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
+                                                               0xF, 0xF, false));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane of the row gets the total.
+__device__ __forceinline__ float row_sum16(float x) {
+  x += dpp<0x128>(x);  // row_ror:8
+  x += dpp<0x124>(x);  // row_ror:4
+  x += dpp<0x122>(x);  // row_ror:2
+  x += dpp<0x121>(x);  // row_ror:1
+  return x;
+}
+
+// ------------------------------------------------------------- planning
+
+__device__ __forceinline__ int clamp_len(const DecodeArgs& a, int L) {
+  return L < 0 ? 0 : (L > a.len_cap ? a.len_cap : L);
+}
+
+// Total block count over all sequences (wave-uniform). With write_cum, also
+// stores the exclusive prefix sum of per-sequence block counts and flags
+// clamped lengths.
+__device__ int plan_total_blocks(const DecodeArgs& a, bool write_cum) {
+  const int l = lane_id();
+  int carry = 0;
+  int bad = 0;
+  for (int b0 = 0; b0 < a.B; b0 += 64) {
+    const int b = b0 + l;
+    int n = 0;
+    if (b < a.B) {
+      const int raw = a.seq_lens[b];
+      const int L = clamp_len(a, raw);
+      bad |= (raw != L);
+      n = (L + kBlockSize - 1) / kBlockSize;
+    }
+    const int incl = wave_incl_scan(n);
+    if (write_cum && b < a.B) a.cum[b] = carry + incl - n;
+    carry += __shfl(incl, 63, 64);
+  }
+  if (write_cum && __any(bad) && l == 0) atomicOr(a.hdr + kHdrStatus, kStatusLenClamped);
+  return uni(carry);
+}
+
+// First sequence whose block-head range contains stream position pos, and its
+// exclusive block prefix. pos must be < Hkv * total.
+__device__ void plan_locate(const DecodeArgs& a, int64_t pos, int& b_out, int& cum_out) {
+  const int l = lane_id();
+  int carry = 0;
+  for (int b0 = 0; b0 < a.B; b0 += 64) {
+    const int b = b0 + l;
+    int n = 0;
+    if (b < a.B) n = (clamp_len(a, a.seq_lens[b]) + kBlockSize - 1) / kBlockSize;
+    const int incl = wave_incl_scan(n);
+    const int total = __shfl(incl, 63, 64);
+    if ((int64_t)(carry + total) * a.Hkv > pos) {
+      const int excl = carry + incl - n;
+      const uint64_t m = __ballot(b < a.B && (int64_t)excl * a.Hkv <= pos);
+      const int idx = __popcll(m) - 1;
+      b_out = uni(b0 + idx);
+      cum_out = uni(__shfl(excl, idx, 64));
+      return;
+    }
+    carry += total;
+  }
+  b_out = a.B;
+  cum_out = carry;
+}
+
+// Block-table cache: lane i holds entry chunk + i of the row, so block ids
+// come from v_readlane instead of a scalar load in front of every tile load.
+struct BlockIds {
+  const int32_t* row;
+  int base;
+  int end;
+  int ids;
+  __device__ void load(int j) {
+    base = j;
+    const int i = j + lane_id();
+    ids = i < end ? row[i] : 0;
+  }
+  __device__ int get(int j) {
+    if (j >= base + 64) load(j);
+    return __builtin_amdgcn_readlane(ids, j - base);
+  }
+};
+
+// Physical block of logical block j, or block 0 with lim = 0 when the table
+// entry is out of range (flagged). lim = valid tokens in the block (0..16).
+struct Blk {
+  int64_t tile;  // (p * Hkv + kvh): tile index into either cache
+  int p;
+  int lim;
+};
+
+__device__ __forceinline__ Blk block_at(const DecodeArgs& a, BlockIds& ids, int j, int L, int kvh,
+                                        int& status) {
+  Blk r;
+  int p = ids.get(j);
+  int lim = L - j * kBlockSize;
+  lim = lim > kBlockSize ? kBlockSize : lim;
+  if ((unsigned)p >= (uint64_t)a.num_blocks) {
+    status |= kStatusBadBlock;
+    p = 0;
+    lim = 0;
+  }
+  r.p = p;
+  r.lim = lim;
+  r.tile = (int64_t)p * a.Hkv + kvh;
+  return r;
+}
+
+// ------------------------------------------------------------- MFMA wave kernel
+
+template <KvType KV, int D>
+struct MfmaCfg {
+  static constexpr int ESZ = KV == KvType::FP8 ? 1 : 2;
+  static constexpr int KSTEPS = D / 32;       // 16x16x32 k-steps over head_dim
+  static constexpr int DL = D / 4;            // head-dim elements per lane per token row
+  static constexpr int NK4 = DL * ESZ / 16;   // 16-byte K loads per lane per block
+  static constexpr int MT = D / 16;           // 16-row output tiles of O^T
+};
+
+template <KvType KV, int D>
+struct MfmaPair {
+  using C = MfmaCfg<KV, D>;
+  u32x4 k[2][C::NK4];
+  // V^T: 4 tokens of one dim row per M-tile: bf16 -> 2 words, fp8 -> 1 word
+  u32x2 v[2][C::MT];
+  float ks[2], vs[2];
+  int lim[2];
+};
+
+// K A-operand of k-step j (8 bf16: dims c*DL + 8j .. +8 of token row r).
+template <KvType KV, int D>
+__device__ __forceinline__ bf16x8 k_operand(const u32x4 (&k)[MfmaCfg<KV, D>::NK4], int j) {
+  if constexpr (KV == KvType::BF16) {
+    return __builtin_bit_cast(bf16x8, k[j]);
+  } else {
+    const u32x4 w = k[j >> 1];
+    const uint32_t w0 = (j & 1) ? w.z : w.x;
+    const uint32_t w1 = (j & 1) ? w.w : w.y;
+    const u32x2 a = fp8x4_to_bf16x4(w0);
+    const u32x2 b = fp8x4_to_bf16x4(w1);
+    u32x4 r = {a.x, a.y, b.x, b.y};
+    return __builtin_bit_cast(bf16x8, r);
+  }
+}
+
+template <KvType KV, int D>
+__device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs& a, BlockIds& ids,
+                                           int j0, int j_hi, int L, int kvh, int& status) {
+  using C = MfmaCfg<KV, D>;
+  const int l = lane_id();
+  const int r = l & 15, c = l >> 4;
+  const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
+  const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
+  constexpr int64_t TILE = (int64_t)kBlockSize * D * C::ESZ;  // bytes per (block, head) tile
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int j = j0 + s;
+    if (s == 0 || j < j_hi) {
+      const Blk blk = block_at(a, ids, j, L, kvh, status);
+      bf.lim[s] = blk.lim;
+      const uint8_t* kt = kc + blk.tile * TILE + (r * D + c * C::DL) * C::ESZ;
+#pragma unroll
+      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = ld<u32x4>(kt + 16 * i);
+      const uint8_t* vt = vc + blk.tile * TILE + (r * kBlockSize + 4 * c) * C::ESZ;
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) {
+        const uint8_t* pv = vt + m * 16 * kBlockSize * C::ESZ;
+        if constexpr (KV == KvType::BF16) {
+          bf.v[s][m] = ld<u32x2>(pv);
+        } else {
+          bf.v[s][m].x = ld<uint32_t>(pv);
+          bf.v[s][m].y = 0;
+        }
+      }
+      if constexpr (KV == KvType::FP8) {
+        bf.ks[s] = a.kv_scales[blk.tile];
+        bf.vs[s] = a.kv_scales[a.num_blocks * a.Hkv + blk.tile];
+      } else {
+        bf.ks[s] = 1.f;
+        bf.vs[s] = 1.f;
+      }
+    } else {
+      bf.lim[s] = 0;
+#pragma unroll
+      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) bf.v[s][m] = u32x2{0, 0};
+      bf.ks[s] = 0.f;
+      bf.vs[s] = 0.f;
+    }
+  }
+}
+
+template <KvType KV, int D>
+__device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[MfmaCfg<KV, D>::KSTEPS],
+                                             float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT],
+                                             float& m_run, float& l_run) {
+  using C = MfmaCfg<KV, D>;
+  const int l = lane_id();
+  const int c = l >> 4;
+
+  // S^T = K . Q^T for both blocks: lane holds tokens 4c..4c+3 of head (lane & 15).
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < C::KSTEPS; ++j) {
+    s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[0], j), qb[j], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[1], j), qb[j], s1, 0, 0, 0);
+  }
+  const float c0 = scale_log2 * bf.ks[0];
+  const float c1 = scale_log2 * bf.ks[1];
+  float x[8];
+  bool valid[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    valid[i] = 4 * c + i < bf.lim[0];
+    valid[4 + i] = 4 * c + i < bf.lim[1];
+    x[i] = valid[i] ? s0[i] * c0 : kNegInf;
+    x[4 + i] = valid[4 + i] ? s1[i] * c1 : kNegInf;
+  }
+  float mx = x[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) mx = fmaxf(mx, x[i]);
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(m_run, mx);
+  const float m_safe = m_new == kNegInf ? 0.f : m_new;
+  const float alpha = fast_exp2(m_run - m_safe);
+  m_run = m_new;
+  l_run *= alpha;
+#pragma unroll
+  for (int m = 0; m < C::MT; ++m) acc[m] *= alpha;
+
+  float p[8];
+  float psum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    p[i] = fast_exp2(x[i] - m_safe);
+    psum += p[i];
+  }
+  l_run += psum;
+  if constexpr (KV == KvType::FP8) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      p[i] *= bf.vs[0];
+      p[4 + i] *= bf.vs[1];
+    }
+  }
+  // P^T operand in two bf16 terms: p = hi + lo + O(2^-17 p).
+  bf16x8 phi, plo;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const __bf16 h = (__bf16)p[i];
+    phi[i] = h;
+    plo[i] = (__bf16)(p[i] - (float)h);
+  }
+  // Token masks for V (select, so NaN poison in dead slots cannot leak).
+  const uint32_t m0a = (valid[0] ? 0xFFFFu : 0u) | (valid[1] ? 0xFFFF0000u : 0u);
+  const uint32_t m0b = (valid[2] ? 0xFFFFu : 0u) | (valid[3] ? 0xFFFF0000u : 0u);
+  const uint32_t m1a = (valid[4] ? 0xFFFFu : 0u) | (valid[5] ? 0xFFFF0000u : 0u);
+  const uint32_t m1b = (valid[6] ? 0xFFFFu : 0u) | (valid[7] ? 0xFFFF0000u : 0u);
+#pragma unroll
+  for (int m = 0; m < C::MT; ++m) {
+    u32x2 v0, v1;
+    if constexpr (KV == KvType::BF16) {
+      v0 = bf.v[0][m];
+      v1 = bf.v[1][m];
+    } else {
+      v0 = fp8x4_to_bf16x4(bf.v[0][m].x);
+      v1 = fp8x4_to_bf16x4(bf.v[1][m].x);
+    }
+    const u32x4 w = {v0.x & m0a, v0.y & m0b, v1.x & m1a, v1.y & m1b};
+    const bf16x8 va = __builtin_bit_cast(bf16x8, w);
+    acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[m], 0, 0, 0);
+    acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[m], 0, 0, 0);
+  }
+}
+
+template <KvType KV, int D>
+__device__ void mfma_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo, int j_hi, bool final,
+                             int64_t slot, int& status) {
+  using C = MfmaCfg<KV, D>;
+  const int l = lane_id();
+  const int r = l & 15, c = l >> 4;
+
+  // Q^T B-operand: head r of the group, dims c*DL + 8j .. +8 for k-step j.
+  bf16x8 qb[C::KSTEPS];
+  {
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.Hq + kvh * a.G + r) * D + c * C::DL;
+#pragma unroll
+    for (int j = 0; j < C::KSTEPS; ++j) {
+      u32x4 w = {0, 0, 0, 0};
+      if (r < a.G) w = ld<u32x4>(qrow + 8 * j);
+      qb[j] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
+
+  BlockIds ids;
+  ids.row = a.block_table + (int64_t)b * a.max_blocks;
+  ids.end = j_hi;
+  ids.load(j_lo);
+
+  f32x4 acc[C::MT];
+#pragma unroll
+  for (int m = 0; m < C::MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = kNegInf, l_run = 0.f;
+
+  const int npairs = (j_hi - j_lo + 1) >> 1;
+  MfmaPair<KV, D> b0, b1;
+  if (npairs > 0) mfma_issue<KV, D>(b0, a, ids, j_lo, j_hi, L, kvh, status);
+  if (npairs > 1) mfma_issue<KV, D>(b1, a, ids, j_lo + 2, j_hi, L, kvh, status);
+  int i = 0;
+  for (; i + 3 < npairs; i += 2) {
+    mfma_compute<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
+    mfma_compute<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_issue<KV, D>(b1, a, ids, j_lo + 2 * (i + 3), j_hi, L, kvh, status);
+  }
+  if (i < npairs) {
+    mfma_compute<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+    if (i + 2 < npairs) mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
+  }
+  if (i + 1 < npairs) mfma_compute<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
+  if (i + 2 < npairs) mfma_compute<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+
+  // Lanes c = 0..3 hold disjoint token subsets of head r: total the denominator.
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+
+  if (r >= a.G) return;
+  const int h = kvh * a.G + r;
+  if (final) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    const int64_t orow = ((int64_t)b * a.Hq + h) * D;
+    if (a.out_bf16) {
+      uint16_t* o = static_cast<uint16_t*>(a.out) + orow;
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) {
+        u32x2 w;
+        w.x = f32_to_bf16_bits(acc[m][0] * inv) | (f32_to_bf16_bits(acc[m][1] * inv) << 16);
+        w.y = f32_to_bf16_bits(acc[m][2] * inv) | (f32_to_bf16_bits(acc[m][3] * inv) << 16);
+        *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) = w;
+      }
+    } else {
+      float* o = static_cast<float*>(a.out) + orow;
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m] * inv;
+    }
+  } else {
+    float* arow = a.ws_acc + (slot * a.G + r) * D;
+#pragma unroll
+    for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(arow + 16 * m + 4 * c) = acc[m];
+    if (c == 0) {
+      a.ws_m[slot * a.G + r] = m_run;
+      a.ws_l[slot * a.G + r] = l_run;
+    }
+  }
+}
+
+// ------------------------------------------------------------- vector wave kernel
+
+template <KvType KV, int D>
+struct VecCfg {
+  static constexpr int ESZ = KV == KvType::F32 ? 4 : (KV == KvType::BF16 ? 2 : 1);
+  static constexpr int ED = D / 16;          // dims per lane (K side) / dim rows per lane (V side)
+  static constexpr int KW = ED * ESZ / 4;    // words per lane per token (K)
+  static constexpr int VW = ESZ;             // words per lane per dim row (4 tokens)
+};
+
+template <KvType KV, int D>
+struct VecBlock {
+  using C = VecCfg<KV, D>;
+  uint32_t k[4][C::KW];
+  uint32_t v[C::ED][C::VW];
+  float ks, vs;
+  int lim;
+};
+
+template <int N>
+__device__ __forceinline__ void ld_words(uint32_t (&dst)[N], const uint8_t* p) {
+  if constexpr (N % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < N; i += 4) {
+      const u32x4 w = ld<u32x4>(p + 4 * i);
+      dst[i] = w.x; dst[i + 1] = w.y; dst[i + 2] = w.z; dst[i + 3] = w.w;
+    }
+  } else if constexpr (N == 2) {
+    const u32x2 w = ld<u32x2>(p);
+    dst[0] = w.x; dst[1] = w.y;
+  } else {
+    dst[0] = ld<uint32_t>(p);
+  }
+}
+
+// Decode N stored elements (packed in words) to f32.
+template <KvType KV, int N, int W>
+__device__ __forceinline__ void decode_elems(float (&f)[N], const uint32_t (&w)[W]) {
+  if constexpr (KV == KvType::F32) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) f[i] = __builtin_bit_cast(float, w[i]);
+  } else if constexpr (KV == KvType::BF16) {
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) {
+      f[2 * i] = bf16_lo(w[i]);
+      f[2 * i + 1] = bf16_hi(w[i]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N / 4; ++i) {
+      const f32x2 lo = fp8_pair<false>(w[i]);
+      const f32x2 hi = fp8_pair<true>(w[i]);
+      f[4 * i] = lo.x; f[4 * i + 1] = lo.y; f[4 * i + 2] = hi.x; f[4 * i + 3] = hi.y;
+    }
+  }
+}
+
+template <KvType KV, int D>
+__device__ __forceinline__ void vec_issue(VecBlock<KV, D>& bk, const DecodeArgs& a, BlockIds& ids, int j,
+                                          int L, int kvh, int& status) {
+  using C = VecCfg<KV, D>;
+  const int l = lane_id();
+  const int r4 = l >> 4, c16 = l & 15;
+  const Blk blk = block_at(a, ids, j, L, kvh, status);
+  bk.lim = blk.lim;
+  constexpr int64_t TILE = (int64_t)kBlockSize * D * C::ESZ;
+  const uint8_t* kt = static_cast<const uint8_t*>(a.k_cache) + blk.tile * TILE;
+  const uint8_t* vt = static_cast<const uint8_t*>(a.v_cache) + blk.tile * TILE;
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj)
+    ld_words<C::KW>(bk.k[jj], kt + ((4 * r4 + jj) * D + c16 * C::ED) * C::ESZ);
+#pragma unroll
+  for (int e = 0; e < C::ED; ++e)
+    ld_words<C::VW>(bk.v[e], vt + ((c16 + 16 * e) * kBlockSize + 4 * r4) * C::ESZ);
+  if constexpr (KV == KvType::FP8) {
+    bk.ks = a.kv_scales[blk.tile];
+    bk.vs = a.kv_scales[a.num_blocks * a.Hkv + blk.tile];
+  } else {
+    bk.ks = 1.f;
+    bk.vs = 1.f;
+  }
+}
+
+template <KvType KV, int D, int GV>
+__device__ __forceinline__ void vec_compute(const VecBlock<KV, D>& bk, const float (&qf)[GV][VecCfg<KV, D>::ED],
+                                            float scale_log2, float (&acc)[GV][VecCfg<KV, D>::ED],
+                                            float (&m_run)[GV], float (&l_run)[GV]) {
+  using C = VecCfg<KV, D>;
+  const int r4 = lane_id() >> 4;
+  float s[4][GV];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) {
+    float kf[C::ED];
+    decode_elems<KV, C::ED, C::KW>(kf, bk.k[jj]);
+#pragma unroll
+    for (int h = 0; h < GV; ++h) {
+      float part = 0.f;
+#pragma unroll
+      for (int e = 0; e < C::ED; ++e) part = fmaf(qf[h][e], kf[e], part);
+      s[jj][h] = row_sum16(part);
+    }
+  }
+  bool valid[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) valid[jj] = 4 * r4 + jj < bk.lim;
+  // V rows (c16 + 16e) x this row's 4 tokens, masked by select.
+  float vf[C::ED][4];
+#pragma unroll
+  for (int e = 0; e < C::ED; ++e) {
+    float t4[4];
+    decode_elems<KV, 4, C::VW>(t4, bk.v[e]);
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) vf[e][jj] = valid[jj] ? t4[jj] : 0.f;
+  }
+  const float coef = scale_log2 * bk.ks;
+#pragma unroll
+  for (int h = 0; h < GV; ++h) {
+    float x[4];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) x[jj] = valid[jj] ? s[jj][h] * coef : kNegInf;
+    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run[h], mx);
+    const float m_safe = m_new == kNegInf ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run[h] - m_safe);
+    m_run[h] = m_new;
+    float p[4];
+    float psum = 0.f;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      p[jj] = fast_exp2(x[jj] - m_safe);
+      psum += p[jj];
+    }
+    l_run[h] = l_run[h] * alpha + psum;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) p[jj] *= bk.vs;
+#pragma unroll
+    for (int e = 0; e < C::ED; ++e) {
+      float t = acc[h][e] * alpha;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) t = fmaf(p[jj], vf[e][jj], t);
+      acc[h][e] = t;
+    }
+  }
+}
+
+template <KvType KV, int D, int GV>
+__device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo, int j_hi, bool final,
+                            int64_t slot, int& status) {
+  using C = VecCfg<KV, D>;
+  const int l = lane_id();
+  const int r4 = l >> 4, c16 = l & 15;
+
+  float qf[GV][C::ED];
+#pragma unroll
+  for (int h = 0; h < GV; ++h) {
+    const int64_t row = ((int64_t)b * a.Hq + kvh * a.G + h) * D + c16 * C::ED;
+#pragma unroll
+    for (int e = 0; e < C::ED; ++e) {
+      float v = 0.f;
+      if (h < a.G) {
+        if constexpr (KV == KvType::F32) {
+          v = static_cast<const float*>(a.q)[row + e];
+        } else {
+          v = __builtin_bit_cast(float, (uint32_t) static_cast<const uint16_t*>(a.q)[row + e] << 16);
+        }
+      }
+      qf[h][e] = v;
+    }
+  }
+
+  BlockIds ids;
+  ids.row = a.block_table + (int64_t)b * a.max_blocks;
+  ids.end = j_hi;
+  ids.load(j_lo);
+
+  float acc[GV][C::ED];
+  float m_run[GV], l_run[GV];
+#pragma unroll
+  for (int h = 0; h < GV; ++h) {
+    m_run[h] = kNegInf;
+    l_run[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < C::ED; ++e) acc[h][e] = 0.f;
+  }
+
+  const int n = j_hi - j_lo;
+  VecBlock<KV, D> b0, b1;
+  if (n > 0) vec_issue<KV, D>(b0, a, ids, j_lo, L, kvh, status);
+  if (n > 1) vec_issue<KV, D>(b1, a, ids, j_lo + 1, L, kvh, status);
+  int i = 0;
+  for (; i + 3 < n; i += 2) {
+    vec_compute<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
+    vec_issue<KV, D>(b0, a, ids, j_lo + i + 2, L, kvh, status);
+    vec_compute<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
+    vec_issue<KV, D>(b1, a, ids, j_lo + i + 3, L, kvh, status);
+  }
+  if (i < n) {
+    vec_compute<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
+    if (i + 2 < n) vec_issue<KV, D>(b0, a, ids, j_lo + i + 2, L, kvh, status);
+  }
+  if (i + 1 < n) vec_compute<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
+  if (i + 2 < n) vec_compute<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
+
+  // Each 16-lane row holds its own 4-token subsets: total over the 4 rows.
+#pragma unroll
+  for (int h = 0; h < GV; ++h) {
+    l_run[h] += __shfl_xor(l_run[h], 16, 64);
+    l_run[h] += __shfl_xor(l_run[h], 32, 64);
+#pragma unroll
+    for (int e = 0; e < C::ED; ++e) {
+      acc[h][e] += __shfl_xor(acc[h][e], 16, 64);
+      acc[h][e] += __shfl_xor(acc[h][e], 32, 64);
+    }
+  }
+  if (r4 != 0) return;
+#pragma unroll
+  for (int h = 0; h < GV; ++h) {
+    if (h >= a.G) break;
+    const int hq = kvh * a.G + h;
+    if (final) {
+      const float inv = l_run[h] > 0.f ? 1.f / l_run[h] : 0.f;
+      const int64_t orow = ((int64_t)b * a.Hq + hq) * D;
+#pragma unroll
+      for (int e = 0; e < C::ED; ++e) {
+        const float o = acc[h][e] * inv;
+        if (a.out_bf16) {
+          static_cast<uint16_t*>(a.out)[orow + c16 + 16 * e] = (uint16_t)f32_to_bf16_bits(o);
+        } else {
+          static_cast<float*>(a.out)[orow + c16 + 16 * e] = o;
+        }
+      }
+    } else {
+      float* arow = a.ws_acc + (slot * a.G + h) * D;
+#pragma unroll
+      for (int e = 0; e < C::ED; ++e) arow[c16 + 16 * e] = acc[h][e];
+      if (c16 == 0) {
+        a.ws_m[slot * a.G + h] = m_run[h];
+        a.ws_l[slot * a.G + h] = l_run[h];
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------- persistent driver
+
+template <Variant V, KvType KV, int D, int GV>
+__global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
+  const int wave = blockIdx.x;
+  const int64_t total = (int64_t)plan_total_blocks(a, wave == 0) * a.Hkv;
+  int64_t share = (total + a.waves - 1) / a.waves;
+  if (share < a.min_share) share = a.min_share;
+  if (wave == 0 && lane_id() == 0) a.share[0] = (int32_t)share;
+  int64_t pos = (int64_t)wave * share;
+  const int64_t end = pos + share < total ? pos + share : total;
+  if (pos >= end) return;
+
+  int b, cum_b;
+  plan_locate(a, pos, b, cum_b);
+  int status = 0;
+  while (pos < end && b < a.B) {
+    const int L = clamp_len(a, a.seq_lens[b]);
+    const int nb = (L + kBlockSize - 1) / kBlockSize;
+    const int64_t base = (int64_t)cum_b * a.Hkv;
+    if (pos >= base + (int64_t)nb * a.Hkv) {
+      cum_b += nb;
+      ++b;
+      continue;
+    }
+    const int64_t rel = pos - base;
+    const int kvh = (int)(rel / nb);
+    const int j_lo = (int)(rel - (int64_t)kvh * nb);
+    const int64_t room = end - pos;
+    const int j_hi = (int64_t)(nb - j_lo) <= room ? nb : j_lo + (int)room;
+    const bool final = j_lo == 0 && j_hi == nb;
+    const int64_t slot = (int64_t)b * a.Hkv + kvh + wave;
+    if constexpr (V == Variant::Mfma) {
+      mfma_segment<KV, D>(a, b, kvh, L, j_lo, j_hi, final, slot, status);
+    } else {
+      vec_segment<KV, D, GV>(a, b, kvh, L, j_lo, j_hi, final, slot, status);
+    }
+    pos += j_hi - j_lo;
+  }
+  if (__any(status) && lane_id() == 0) atomicOr(a.hdr + kHdrStatus, status);
+}
+
+// ------------------------------------------------------------- LSE combine
+
+// One workgroup per (sequence, KV head) unit: merges the partial softmax states
+// of the waves that shared the unit, out = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w,
+// and writes zeros for empty sequences.
+template <bool OUT_BF16, int D>
+__global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
+  const int u = blockIdx.x;
+  const int b = u / a.Hkv;
+  const int kvh = u - b * a.Hkv;
+  const int L = clamp_len(a, a.seq_lens[b]);
+  const int nb = (L + kBlockSize - 1) / kBlockSize;
+  const int G = a.G;
+  const int64_t obase = ((int64_t)b * a.Hq + (int64_t)kvh * G) * D;
+  if (nb == 0) {
+    for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
+      if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = 0;
+      else static_cast<float*>(a.out)[obase + i] = 0.f;
+    }
+    return;
+  }
+  const int64_t share = a.share[0];
+  const int64_t start = (int64_t)a.cum[b] * a.Hkv + (int64_t)kvh * nb;
+  const int64_t w0 = start / share;
+  const int64_t w1 = (start + nb - 1) / share;
+  if (w0 == w1) return;  // one wave covered the unit and wrote the output
+  for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
+    const int h = i / D;
+    const int d = i - h * D;
+    float M = kNegInf;
+    for (int64_t w = w0; w <= w1; ++w) M = fmaxf(M, a.ws_m[((int64_t)u + w) * G + h]);
+    const float M_safe = M == kNegInf ? 0.f : M;
+    float num = 0.f, den = 0.f;
+    for (int64_t w = w0; w <= w1; ++w) {
+      const int64_t s = ((int64_t)u + w) * G + h;
+      const float e = fast_exp2(a.ws_m[s] - M_safe);
+      num = fmaf(e, a.ws_acc[s * D + d], num);
+      den = fmaf(e, a.ws_l[s], den);
+    }
+    const float o = den > 0.f ? num / den : 0.f;
+    if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = (uint16_t)f32_to_bf16_bits(o);
+    else static_cast<float*>(a.out)[obase + i] = o;
+  }
+}
+
+// ------------------------------------------------------------- dispatch
+
+template <Variant V, KvType KV, int D, int GV>
+void* kernel_ptr() {
+  return reinterpret_cast<void*>(&decode_kernel<V, KV, D, GV>);
+}
+
+template <Variant V, KvType KV, int D>
+void* pick_g(int G) {
+  if constexpr (V == Variant::Mfma) {
+    return kernel_ptr<V, KV, D, 16>();
+  } else {
+    if (G <= 1) return kernel_ptr<V, KV, D, 1>();
+    if (G <= 2) return kernel_ptr<V, KV, D, 2>();
+    if (G <= 4) return kernel_ptr<V, KV, D, 4>();
+    return kernel_ptr<V, KV, D, 8>();
+  }
+}
+
+template <Variant V, KvType KV>
+void* pick_d(int D, int G) {
+  return D == 64 ? pick_g<V, KV, 64>(G) : pick_g<V, KV, 128>(G);
+}
+
+void* pick(Variant v, KvType kv, int D, int G) {
+  if (v == Variant::Mfma) {
+    if (kv == KvType::BF16) return pick_d<Variant::Mfma, KvType::BF16>(D, G);
+    if (kv == KvType::FP8) return pick_d<Variant::Mfma, KvType::FP8>(D, G);
+    return nullptr;
+  }
+  if (kv == KvType::F32) return pick_d<Variant::Vector, KvType::F32>(D, G);
+  if (kv == KvType::BF16) return pick_d<Variant::Vector, KvType::BF16>(D, G);
+  return pick_d<Variant::Vector, KvType::FP8>(D, G);
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t s) {
+  void* fn = pick(v, kv, a.D, a.G);
+  if (!fn) return hipErrorInvalidValue;
+  DecodeArgs args = a;
+  void* params[] = {&args};
+  return hipLaunchKernel(fn, dim3(a.waves), dim3(64), params, 0, s);
+}
+
+hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
+  void* fn;
+  if (a.out_bf16)
+    fn = a.D == 64 ? reinterpret_cast<void*>(&combine_kernel<true, 64>)
+                   : reinterpret_cast<void*>(&combine_kernel<true, 128>);
+  else
+    fn = a.D == 64 ? reinterpret_cast<void*>(&combine_kernel<false, 64>)
+                   : reinterpret_cast<void*>(&combine_kernel<false, 128>);
+  const unsigned units = (unsigned)a.B * (unsigned)a.Hkv;
+  if (units == 0) return hipSuccess;
+  DecodeArgs args = a;
+  void* params[] = {&args};
+  return hipLaunchKernel(fn, dim3(units), dim3(256), params, 0, s);
+}
+
+hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* wgs_per_cu) {
+  void* fn = pick(v, kv, D, G);
+  if (!fn) return hipErrorInvalidValue;
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(wgs_per_cu, fn, 64, 0);
+}
+
+}  // namespace pda

@@ -1,0 +1,163 @@
+"""The C interface on the host: the library loads, exports what include/pda.h
+declares, and rejects bad arguments with the documented codes before any HIP
+call (these tests run without a GPU)."""
+
+import ctypes
+import math
+import subprocess
+
+import pytest
+
+from paper_2605_20863_amd import _lib as L
+
+
+def prob(**kw):
+    base = dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, head_dim=128, block_size=16,
+                max_blocks_per_seq=32, num_blocks=200, max_seq_len=0, q_dtype=L.BF16, kv_dtype=L.BF16,
+                out_dtype=None)
+    base.update(kw)
+    if base["out_dtype"] is None:
+        base["out_dtype"] = base["q_dtype"]
+    return L.Problem(**base)
+
+
+def test_exports_every_declared_symbol():
+    declared = L.header_symbols()
+    assert set(declared) == {"pda_paged_decode_attention", "pda_query_plan", "pda_read_device_status",
+                             "pda_release_workspaces", "pda_last_error", "pda_version"}
+    for name in declared:
+        assert hasattr(L._lib, name), name
+    nm = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True).stdout
+    exported = {line.split()[-1] for line in nm.splitlines() if " T " in line}
+    assert set(declared) <= exported
+    # nothing else with the public prefix leaks out
+    assert {s for s in exported if s.startswith("pda_")} == set(declared)
+
+
+def test_version():
+    assert L.version() == 1
+
+
+def test_struct_layout_matches_header(tmp_path):
+    """ctypes mirrors of the structs agree with the C compiler's layout of pda.h."""
+    src = tmp_path / "layout.c"
+    src.write_text(r"""
+#include <stddef.h>
+#include <stdio.h>
+#include "pda.h"
+#define F(T, m) printf(#T "." #m " %zu\n", offsetof(T, m))
+int main(void) {
+  printf("pda_problem %zu\npda_options %zu\npda_plan_info %zu\n",
+         sizeof(pda_problem), sizeof(pda_options), sizeof(pda_plan_info));
+  F(pda_problem, num_blocks); F(pda_problem, max_seq_len); F(pda_problem, out_dtype);
+  F(pda_options, min_blocks_per_wave); F(pda_plan_info, workspace_bytes);
+  return 0;
+}
+""")
+    exe = tmp_path / "layout"
+    import os
+    inc = os.path.dirname(L.HEADER_PATH)
+    subprocess.run(["gcc", "-std=c11", "-D__HIP_PLATFORM_AMD__", "-I", inc, "-I", "/opt/rocm/include",
+                    str(src), "-o", str(exe)], check=True)
+    got = dict(line.rsplit(" ", 1) for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                               check=True).stdout.splitlines())
+    assert int(got["pda_problem"]) == ctypes.sizeof(L.Problem)
+    assert int(got["pda_options"]) == ctypes.sizeof(L.Options)
+    assert int(got["pda_plan_info"]) == ctypes.sizeof(L.PlanInfo)
+    assert int(got["pda_problem.num_blocks"]) == L.Problem.num_blocks.offset
+    assert int(got["pda_problem.max_seq_len"]) == L.Problem.max_seq_len.offset
+    assert int(got["pda_problem.out_dtype"]) == L.Problem.out_dtype.offset
+    assert int(got["pda_options.min_blocks_per_wave"]) == L.Options.min_blocks_per_wave.offset
+    assert int(got["pda_plan_info.workspace_bytes"]) == L.PlanInfo.workspace_bytes.offset
+
+
+BAD = [
+    (dict(num_seqs=-1), L.EINVAL),
+    (dict(num_q_heads=0), L.EINVAL),
+    (dict(num_q_heads=7, num_kv_heads=2), L.EINVAL),
+    (dict(num_q_heads=34, num_kv_heads=2), L.EUNSUPPORTED),
+    (dict(head_dim=96), L.EUNSUPPORTED),
+    (dict(head_dim=256), L.EUNSUPPORTED),
+    (dict(block_size=32), L.EUNSUPPORTED),
+    (dict(max_blocks_per_seq=0), L.EINVAL),
+    (dict(num_blocks=0), L.EINVAL),
+    (dict(max_seq_len=-5), L.EINVAL),
+    (dict(max_seq_len=32 * 16 + 1), L.EINVAL),
+    (dict(q_dtype=7), L.EINVAL),
+    (dict(kv_dtype=9), L.EINVAL),
+    (dict(q_dtype=L.FP8_E4M3), L.EUNSUPPORTED),
+    (dict(q_dtype=L.BF16, kv_dtype=L.F32), L.EUNSUPPORTED),
+    (dict(q_dtype=L.F32, kv_dtype=L.BF16), L.EUNSUPPORTED),
+    (dict(q_dtype=L.F32, kv_dtype=L.FP8_E4M3), L.EUNSUPPORTED),
+    (dict(num_seqs=1 << 20, max_blocks_per_seq=1 << 12), L.EINVAL),
+    (dict(out_dtype=L.FP8_E4M3), L.EINVAL),
+    (dict(q_dtype=L.F32, kv_dtype=L.F32, out_dtype=L.BF16), L.EINVAL),
+]
+
+
+@pytest.mark.parametrize("kw,code", BAD, ids=[str(k) for k, _ in BAD])
+def test_bad_problem_rejected_on_host(kw, code):
+    p = prob(**kw)
+    # dummy non-null pointers: validation must reject before dereferencing anything
+    rc = L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, p)
+    assert rc == code, L.last_error()
+    assert L.last_error()
+    with pytest.raises(L.PdaError):
+        L.query_plan(p)
+
+
+def test_bad_scale_and_options_rejected():
+    for s in (math.nan, math.inf, -math.inf):
+        assert L.raw_call(16, 16, 16, 16, 16, 16, 16, s, prob()) == L.EINVAL
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(5, 0, 0)) == L.EINVAL
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(0, -1, 0)) == L.EINVAL
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(0, 0, -3)) == L.EINVAL
+    # vector kernel: at most 8 query heads per KV head
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(num_q_heads=32, num_kv_heads=2),
+                      L.Options(L.VARIANT_VECTOR, 0, 0)) == L.EUNSUPPORTED
+    # MFMA kernel: not for f32 caches
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_dtype=L.F32, kv_dtype=L.F32),
+                      L.Options(L.VARIANT_MFMA, 0, 0)) == L.EUNSUPPORTED
+
+
+def test_null_pointers_rejected():
+    p = prob()
+    for i in range(7):
+        if i == 5:
+            continue  # kv_scales may be NULL for bf16
+        ptrs = [16] * 7
+        ptrs[i] = None
+        assert L.raw_call(*ptrs, 0.1, p) == L.EINVAL, i
+    assert L.raw_call(16, 16, 16, 16, 16, None, 16, 0.1, prob(kv_dtype=L.FP8_E4M3)) == L.EINVAL
+
+
+def test_empty_batch_is_a_no_op():
+    assert L.raw_call(None, None, None, None, None, None, None, 0.1, prob(num_seqs=0)) == L.OK
+
+
+def test_query_plan_variants_and_workspace():
+    # AUTO: MFMA for bf16/fp8 with G >= 4, vector otherwise
+    assert L.query_plan(prob(num_q_heads=8, num_kv_heads=2)).variant == L.VARIANT_MFMA
+    assert L.query_plan(prob(num_q_heads=4, num_kv_heads=2)).variant == L.VARIANT_VECTOR
+    assert L.query_plan(prob(kv_dtype=L.FP8_E4M3, num_q_heads=64, num_kv_heads=8)).variant == L.VARIANT_MFMA
+    assert L.query_plan(prob(q_dtype=L.F32, kv_dtype=L.F32, num_q_heads=4, num_kv_heads=4)).variant == L.VARIANT_VECTOR
+    info = L.query_plan(prob(num_seqs=64, num_q_heads=28, num_kv_heads=4), num_compute_units=256)
+    assert info.group_size == 7 and info.waves == 256 * 8
+    slots = 64 * 4 + info.waves
+    # header + cum + (m, l) + acc, each rounded up to 256 bytes
+    up = lambda x: (x + 255) // 256 * 256
+    assert info.workspace_bytes == up(64) + up(64 * 4) + 2 * up(slots * 7 * 4) + up(slots * 7 * 128 * 4)
+    info = L.query_plan(prob(), L.make_options("vector", waves_per_cu=3), num_compute_units=10)
+    assert info.waves == 30 and info.variant == L.VARIANT_VECTOR
+
+
+def test_one_hip_runtime_in_process():
+    # the binding maps torch's HIP runtime before libpda.so, so both use one runtime
+    import os
+
+    import torch  # noqa: F401
+
+    maps = open("/proc/self/maps").read()
+    hip = {os.path.realpath(l.split()[-1]) for l in maps.splitlines() if "libamdhip64" in l}
+    hsa = {os.path.realpath(l.split()[-1]) for l in maps.splitlines() if "libhsa-runtime64" in l}
+    assert len(hip) == 1 and len(hsa) == 1, (hip, hsa)
