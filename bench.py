@@ -1,0 +1,302 @@
+#!/usr/bin/env python3
+"""Benchmark one batched paged-KV decode-attention step on one MI355X.
+
+A "step" is one call of the library's decode attention (the stream-K decode
+kernel plus the log-sum-exp combine kernel) over one synthetic decode batch
+whose inputs are already resident in HBM. Default workload: the 7B-class GQA
+step (64 sequences, 28 query / 4 KV heads, head_dim 128, bf16, lognormal
+lengths with median 2048). The KV cache is rotated over enough copies that
+consecutive steps never find their cache in the 256 MB last-level cache.
+
+Prints one JSON line. `value` is achieved GB/s of algorithmic bytes (K/V
+tiles of every token, fp8 scales, q, out, block-table entries, lengths) over
+the wall-clock step time; `roofline.achieved` is the same bytes over the
+average per-call GPU time measured with HIP events on the launch stream.
+`cpu_baseline` times the CPU fp64 oracle on a bounded sample of the same step.
+"""
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+LLC_BYTES = 256 << 20
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2605_20863_amd", "csrc", "pda_kernels.hip")
+
+
+def algorithmic_bytes(workload, seq_lens):
+    """Bytes one step must move at least: each token's K and V once, plus
+    fp8 scales, q, out, block-table entries and lengths."""
+    e_kv = {"f32": 4, "bf16": 2, "fp8_e4m3": 1}[workload.kv_dtype]
+    e_q = 4 if workload.q_dtype == "f32" else 2
+    tokens = int(seq_lens.sum())
+    blocks = int(((seq_lens.astype("int64") + 15) // 16).sum())
+    B, hq, hkv, d = len(seq_lens), workload.num_q_heads, workload.num_kv_heads, workload.head_dim
+    kv = tokens * hkv * 2 * d * e_kv
+    scales = blocks * hkv * 2 * 4 if workload.kv_dtype == "fp8_e4m3" else 0
+    return kv + scales + 2 * B * hq * d * e_q + 4 * blocks + 4 * B, tokens
+
+
+# ----------------------------------------------------------------- CPU baseline
+
+def _worker_init():
+    # one BLAS thread per oracle process (the pool already uses every core)
+    for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ[k] = "1"
+
+
+def _oracle_one(args):
+    import oracle  # the CPU fp64 reference; test infrastructure
+
+    (q, kc, vc, table, lens, scale, q_dtype, kv_dtype, ks) = args
+    t0 = time.perf_counter()
+    oracle.paged_decode_attention(q=q, k_cache=kc, v_cache=vc, block_table=table, seq_lens=lens,
+                                  softmax_scale=scale, q_dtype=q_dtype, kv_dtype=kv_dtype, kv_scales=ks)
+    return time.perf_counter() - t0
+
+
+def _sequence_problem(inp, b, raw):
+    """Host copy of sequence b's blocks as a one-sequence problem (data movement only)."""
+    import numpy as np
+    import torch
+
+    lay = inp.layout
+    n = (int(lay.seq_lens[b]) + 15) // 16
+    phys = lay.block_table[b, :max(n, 1)].astype(np.int64)
+    if n == 0:
+        phys = np.zeros(1, dtype=np.int64)
+    idx = torch.from_numpy(phys).to(inp.device)
+    kc = raw(inp.k_cache.index_select(0, idx))
+    vc = raw(inp.v_cache.index_select(0, idx))
+    ks = raw(inp.kv_scales.index_select(1, idx)) if inp.kv_scales is not None else None
+    table = np.arange(max(n, 1), dtype=np.int32)[None, :]
+    w = inp.workload
+    return (raw(inp.q[b:b + 1]), kc, vc, table, lay.seq_lens[b:b + 1].copy(), inp.softmax_scale,
+            w.q_dtype, w.kv_dtype, ks)
+
+
+def cpu_baseline(inp, budget_s):
+    """Time the oracle over a seeded sample of sequences, all host cores (<= 16)."""
+    import multiprocessing as mp
+
+    import numpy as np
+    import torch
+
+    def raw(t):
+        t = t.detach().cpu().contiguous()
+        if t.dtype == torch.bfloat16:
+            return t.view(torch.int16).numpy().view(np.uint16)
+        return t.numpy()
+
+    cores = min(len(os.sched_getaffinity(0)), 16)
+    lay = inp.layout
+    order = np.random.default_rng(0).permutation(len(lay.seq_lens))
+    ctx = mp.get_context("spawn")
+    done, t_cpu = [], 0.0
+    with ctx.Pool(cores, initializer=_worker_init) as pool:
+        t0 = time.perf_counter()
+        pending = []
+        # keep the pool fed, pass after pass over the step's sequences, until the
+        # wall budget is spent; every submitted sequence is finished and counted
+        stop = False
+        while not stop:
+            for b in order:
+                pending.append((int(b), pool.apply_async(_oracle_one, (_sequence_problem(inp, int(b), raw),))))
+                if len(pending) >= 2 * cores:
+                    bb, r = pending.pop(0)
+                    t_cpu += r.get()
+                    done.append(bb)
+                    if time.perf_counter() - t0 > budget_s:
+                        stop = True
+                        break
+            if time.perf_counter() - t0 > budget_s:
+                stop = True
+        for bb, r in pending:
+            t_cpu += r.get()
+            done.append(bb)
+        wall = time.perf_counter() - t0
+    lens = lay.seq_lens[done]
+    nbytes, tokens = algorithmic_bytes(inp.workload, lens)
+    return {
+        "value": round(nbytes / wall / 1e9, 4),
+        "unit": "GB/s",
+        "cores": cores,
+        "kind": "oracle",
+        "kv_tokens_per_s": round(tokens / wall, 1),
+        "seconds": round(wall, 2),
+        "cpu_seconds": round(t_cpu, 2),
+        "sample": f"{len(done)} sequence evaluations ({tokens} tokens; passes over the step's "
+                  f"{len(lay.seq_lens)} sequences in a seeded order) of the same step, fp64 numpy "
+                  f"oracle, one process per core",
+    }
+
+
+# ----------------------------------------------------------------- traffic
+
+def measured_traffic(workload_name, per_launch_bytes):
+    """HBM bytes per call from committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs,
+    or None when absent or taken on a different kernel source."""
+    path = os.path.join(PROFILES, f"traffic_{workload_name}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    if rec.get("kernel_source_sha256") != src:
+        return None
+    return rec.get("hbm_bytes_per_call")
+
+
+# ----------------------------------------------------------------- main
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gqa7b_bf16")
+    ap.add_argument("--variant", default="auto", choices=["auto", "vector", "mfma"])
+    ap.add_argument("--waves-per-cu", type=int, default=0)
+    ap.add_argument("--min-blocks-per-wave", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle wall time")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build is a single-GPU kernel library "
+              "(sharding across GPUs is described in DESIGN.md, not implemented); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2605_20863_amd import _lib
+    from paper_2605_20863_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    if args.calibrate_copy:
+        # a copy kernel of known size: reads and writes 2^30 bytes per dispatch
+        src = torch.randn(1 << 28, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read_per_dispatch": 1 << 30,
+                          "bytes_written_per_dispatch": 1 << 30, "dispatches": args.warmup + args.steps}))
+        return
+
+    w = W.WORKLOADS[args.workload]
+    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    inp = W.generate(w, dev)
+    lens = inp.layout.seq_lens
+    nbytes, tokens = algorithmic_bytes(w, lens)
+    kv_bytes = inp.k_cache.numel() * inp.k_cache.element_size() * 2
+    # rotate over >= 4 GB of cache copies (16x the last-level cache) between steps
+    ncopies = max(1, min(16, math.ceil(16 * LLC_BYTES / kv_bytes)))
+    caches = [(inp.k_cache, inp.v_cache, inp.kv_scales)]
+    for _ in range(ncopies - 1):
+        caches.append((inp.k_cache.clone(), inp.v_cache.clone(),
+                       inp.kv_scales.clone() if inp.kv_scales is not None else None))
+    out = torch.empty_like(inp.q)
+
+    stream = torch.cuda.current_stream(dev)
+    prob = _lib.problem_for(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
+                            inp.layout.max_seq_len, out)
+    opts = _lib.make_options(args.variant, args.waves_per_cu, args.min_blocks_per_wave)
+    ptrs = [(k.data_ptr(), v.data_ptr(), s.data_ptr() if s is not None else None) for k, v, s in caches]
+    sh = stream.cuda_stream
+    qp, bp, lp, op = inp.q.data_ptr(), inp.block_table.data_ptr(), inp.seq_lens.data_ptr(), out.data_ptr()
+
+    def step(i):
+        kp, vp, sp = ptrs[i % ncopies]
+        rc = _lib.raw_call(qp, kp, vp, bp, lp, sp, op, inp.softmax_scale, prob, opts, sh)
+        if rc != 0:
+            raise RuntimeError(f"pda error {rc}: {_lib.last_error()}")
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all(), "non-finite output"
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step(i)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_call_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    call_ms = float(np.mean(per_call_ms))
+    ms_per_step = wall * 1e3 / args.steps
+    status = _lib.read_device_status()
+    print(f"[bench] {w.name}: {ms_per_step * 1e3:.1f} us/step wall, {call_ms * 1e3:.1f} us/call GPU "
+          f"(median {np.median(per_call_ms) * 1e3:.1f}, min {min(per_call_ms) * 1e3:.1f}), "
+          f"{ncopies} cache copies, status {status}", file=sys.stderr, flush=True)
+
+    achieved = nbytes / (call_ms * 1e-3) / 1e9
+    value = nbytes / (ms_per_step * 1e-3) / 1e9
+    traffic = measured_traffic(w.name, nbytes)
+    dtype = {"f32": "f32", "bf16": "bf16", "fp8_e4m3": "fp8e4m3-kv/bf16-q"}[w.kv_dtype]
+    res = {
+        "metric": "paged decode attention achieved HBM GB/s (% of peak) + KV tokens/s read",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "kv_tokens_per_s": round(tokens / (ms_per_step * 1e-3), 1),
+        "config": {
+            "workload": w.name,
+            "num_seqs": len(lens),
+            "q_heads": w.num_q_heads,
+            "kv_heads": w.num_kv_heads,
+            "head_dim": w.head_dim,
+            "kv_dtype": w.kv_dtype,
+            "block_size": w.block_size,
+            "total_tokens": tokens,
+            "max_seq_len": int(lens.max()),
+            "variant": args.variant,
+            "cache_copies": ncopies,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "decode step (stream-K decode + LSE combine, one call)",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_call": nbytes,
+            "call_us": round(call_ms * 1e3, 2),
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
