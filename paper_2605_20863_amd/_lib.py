@@ -15,7 +15,8 @@ import os
 import re
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libpda.so")
+# PDA_LIBRARY may point at another build of the same library (same C interface)
+LIB_PATH = os.environ.get("PDA_LIBRARY") or os.path.join(_PKG, "libpda.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "pda.h")
 
 if not os.path.exists(LIB_PATH):

@@ -173,21 +173,27 @@ __device__ void plan_locate(const DecodeArgs& a, int64_t pos, int& b_out, int& c
   cum_out = carry;
 }
 
-// Block-table cache: lane i holds entry chunk + i of the row, so block ids
-// come from v_readlane instead of a scalar load in front of every tile load.
+// A segment's block ids, staged through a per-wave LDS chunk. Tile addresses
+// depend on the ids, so an id read must not wait on the vector-memory counter:
+// an id held in a VGPR that a conditional reload may still be filling makes
+// the compiler wait for every tile load in flight at each issue. LDS reads are
+// counted separately (lgkmcnt); the chunk refill, which does wait for its own
+// global load, runs once per kIdChunk blocks.
+constexpr int kIdChunk = 128;
+
 struct BlockIds {
   const int32_t* row;
-  int base;
-  int end;
-  int ids;
-  __device__ void load(int j) {
+  int end;   // one past the last block of the segment
+  int base;  // logical block of lds[0]
+  int32_t* lds;
+  __device__ void fill(int j) {
     base = j;
-    const int i = j + lane_id();
-    ids = i < end ? row[i] : 0;
+    for (int i = lane_id(); i < kIdChunk; i += 64) lds[i] = j + i < end ? row[j + i] : 0;
+    __syncthreads();  // one-wave workgroup: orders the LDS writes before the reads
   }
   __device__ int get(int j) {
-    if (j >= base + 64) load(j);
-    return __builtin_amdgcn_readlane(ids, j - base);
+    if (j >= base + kIdChunk) fill(j);
+    return uni(lds[j - base]);
   }
 };
 
@@ -218,13 +224,20 @@ __device__ __forceinline__ Blk block_at(const DecodeArgs& a, BlockIds& ids, int 
 
 // ------------------------------------------------------------- MFMA wave kernel
 
+// K-tile loads are line-friendly: 16-byte load i of lane group c reads bytes
+// [64 i + 16 c, +16) of its token row, so one instruction covers 64
+// contiguous bytes of each of the 16 rows. MFMA contracts over head_dim in any
+// order, so q's operand follows the same head-dim permutation (qdim below).
 template <KvType KV, int D>
 struct MfmaCfg {
   static constexpr int ESZ = KV == KvType::FP8 ? 1 : 2;
   static constexpr int KSTEPS = D / 32;       // 16x16x32 k-steps over head_dim
-  static constexpr int DL = D / 4;            // head-dim elements per lane per token row
-  static constexpr int NK4 = DL * ESZ / 16;   // 16-byte K loads per lane per block
+  static constexpr int NK4 = D * ESZ / 64;    // 16-byte K loads per lane per block
   static constexpr int MT = D / 16;           // 16-row output tiles of O^T
+  // first head-dim index of the 8 that lane group c feeds to k-step j
+  static __device__ __forceinline__ int qdim(int j, int c) {
+    return KV == KvType::BF16 ? 8 * (4 * j + c) : 64 * (j >> 1) + 16 * c + 8 * (j & 1);
+  }
 };
 
 template <KvType KV, int D>
@@ -237,7 +250,7 @@ struct MfmaPair {
   int lim[2];
 };
 
-// K A-operand of k-step j (8 bf16: dims c*DL + 8j .. +8 of token row r).
+// K A-operand of k-step j (8 bf16: dims qdim(j, c) .. +8 of token row r).
 template <KvType KV, int D>
 __device__ __forceinline__ bf16x8 k_operand(const u32x4 (&k)[MfmaCfg<KV, D>::NK4], int j) {
   if constexpr (KV == KvType::BF16) {
@@ -268,9 +281,9 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
     if (s == 0 || j < j_hi) {
       const Blk blk = block_at(a, ids, j, L, kvh, status);
       bf.lim[s] = blk.lim;
-      const uint8_t* kt = kc + blk.tile * TILE + (r * D + c * C::DL) * C::ESZ;
+      const uint8_t* kt = kc + blk.tile * TILE + r * D * C::ESZ + 16 * c;
 #pragma unroll
-      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = ld<u32x4>(kt + 16 * i);
+      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = ld<u32x4>(kt + 64 * i);
       const uint8_t* vt = vc + blk.tile * TILE + (r * kBlockSize + 4 * c) * C::ESZ;
 #pragma unroll
       for (int m = 0; m < C::MT; ++m) {
@@ -301,7 +314,17 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
   }
 }
 
-template <KvType KV, int D>
+// Running-max slack (log2 units). The accumulators are rescaled only when a
+// head's block maximum exceeds its reference max m_run by more than this, so
+// unnormalised weights stay below 2^8 (harmless in fp32) and the rescale --
+// a multiply of every accumulator -- almost never runs once a segment is under
+// way. Every partial carries its own m_run, so the log-sum-exp combine is exact
+// for any reference max.
+constexpr float kMaxSlack = 8.f;
+
+// One pair of 16-token blocks. MASKED handles pairs with slots at or past the
+// sequence end (or a skipped block): those tokens get logit -inf and zero V.
+template <KvType KV, int D, bool MASKED>
 __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[MfmaCfg<KV, D>::KSTEPS],
                                              float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT],
                                              float& m_run, float& l_run) {
@@ -322,29 +345,33 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
   bool valid[8];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    valid[i] = 4 * c + i < bf.lim[0];
-    valid[4 + i] = 4 * c + i < bf.lim[1];
-    x[i] = valid[i] ? s0[i] * c0 : kNegInf;
-    x[4 + i] = valid[4 + i] ? s1[i] * c1 : kNegInf;
+    x[i] = s0[i] * c0;
+    x[4 + i] = s1[i] * c1;
+    if constexpr (MASKED) {
+      valid[i] = 4 * c + i < bf.lim[0];
+      valid[4 + i] = 4 * c + i < bf.lim[1];
+      x[i] = valid[i] ? x[i] : kNegInf;
+      x[4 + i] = valid[4 + i] ? x[4 + i] : kNegInf;
+    }
   }
-  float mx = x[0];
-#pragma unroll
-  for (int i = 1; i < 8; ++i) mx = fmaxf(mx, x[i]);
+  float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
   mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-  const float m_new = fmaxf(m_run, mx);
-  const float m_safe = m_new == kNegInf ? 0.f : m_new;
-  const float alpha = fast_exp2(m_run - m_safe);
-  m_run = m_new;
-  l_run *= alpha;
+  if (__any(mx > m_run + kMaxSlack)) {  // wave-uniform; -inf + slack = -inf starts a segment
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
 #pragma unroll
-  for (int m = 0; m < C::MT; ++m) acc[m] *= alpha;
+    for (int m = 0; m < C::MT; ++m) acc[m] *= alpha;
+  }
+  const float m_ref = m_run == kNegInf ? 0.f : m_run;
 
   float p[8];
   float psum = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    p[i] = fast_exp2(x[i] - m_safe);
+    p[i] = fast_exp2(x[i] - m_ref);
     psum += p[i];
   }
   l_run += psum;
@@ -363,11 +390,14 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
     phi[i] = h;
     plo[i] = (__bf16)(p[i] - (float)h);
   }
-  // Token masks for V (select, so NaN poison in dead slots cannot leak).
-  const uint32_t m0a = (valid[0] ? 0xFFFFu : 0u) | (valid[1] ? 0xFFFF0000u : 0u);
-  const uint32_t m0b = (valid[2] ? 0xFFFFu : 0u) | (valid[3] ? 0xFFFF0000u : 0u);
-  const uint32_t m1a = (valid[4] ? 0xFFFFu : 0u) | (valid[5] ? 0xFFFF0000u : 0u);
-  const uint32_t m1b = (valid[6] ? 0xFFFFu : 0u) | (valid[7] ? 0xFFFF0000u : 0u);
+  uint32_t m0a = ~0u, m0b = ~0u, m1a = ~0u, m1b = ~0u;
+  if constexpr (MASKED) {
+    // select, so NaN poison in dead slots cannot leak through 0 * NaN
+    m0a = (valid[0] ? 0xFFFFu : 0u) | (valid[1] ? 0xFFFF0000u : 0u);
+    m0b = (valid[2] ? 0xFFFFu : 0u) | (valid[3] ? 0xFFFF0000u : 0u);
+    m1a = (valid[4] ? 0xFFFFu : 0u) | (valid[5] ? 0xFFFF0000u : 0u);
+    m1b = (valid[6] ? 0xFFFFu : 0u) | (valid[7] ? 0xFFFF0000u : 0u);
+  }
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
     u32x2 v0, v1;
@@ -378,7 +408,8 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
       v0 = fp8x4_to_bf16x4(bf.v[0][m].x);
       v1 = fp8x4_to_bf16x4(bf.v[1][m].x);
     }
-    const u32x4 w = {v0.x & m0a, v0.y & m0b, v1.x & m1a, v1.y & m1b};
+    u32x4 w = {v0.x, v0.y, v1.x, v1.y};
+    if constexpr (MASKED) w = u32x4{v0.x & m0a, v0.y & m0b, v1.x & m1a, v1.y & m1b};
     const bf16x8 va = __builtin_bit_cast(bf16x8, w);
     acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[m], 0, 0, 0);
     acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[m], 0, 0, 0);
@@ -386,28 +417,36 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
 }
 
 template <KvType KV, int D>
+__device__ __forceinline__ void mfma_step(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[MfmaCfg<KV, D>::KSTEPS],
+                                          float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT], float& m_run,
+                                          float& l_run) {
+  if ((bf.lim[0] & bf.lim[1]) == kBlockSize)  // both blocks full (lim <= 16)
+    mfma_compute<KV, D, false>(bf, qb, scale_log2, acc, m_run, l_run);
+  else
+    mfma_compute<KV, D, true>(bf, qb, scale_log2, acc, m_run, l_run);
+}
+
+template <KvType KV, int D>
 __device__ void mfma_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo, int j_hi, bool final,
-                             int64_t slot, int& status) {
+                             int64_t slot, int& status, int32_t* id_lds) {
   using C = MfmaCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
 
-  // Q^T B-operand: head r of the group, dims c*DL + 8j .. +8 for k-step j.
+  // Q^T B-operand: head r of the group, dims qdim(j, c) .. +8 for k-step j.
   bf16x8 qb[C::KSTEPS];
   {
-    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.Hq + kvh * a.G + r) * D + c * C::DL;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.Hq + kvh * a.G + r) * D;
 #pragma unroll
     for (int j = 0; j < C::KSTEPS; ++j) {
       u32x4 w = {0, 0, 0, 0};
-      if (r < a.G) w = ld<u32x4>(qrow + 8 * j);
+      if (r < a.G) w = ld<u32x4>(qrow + C::qdim(j, c));
       qb[j] = __builtin_bit_cast(bf16x8, w);
     }
   }
 
-  BlockIds ids;
-  ids.row = a.block_table + (int64_t)b * a.max_blocks;
-  ids.end = j_hi;
-  ids.load(j_lo);
+  BlockIds ids{a.block_table + (int64_t)b * a.max_blocks, j_hi, 0, id_lds};
+  ids.fill(j_lo);
 
   f32x4 acc[C::MT];
 #pragma unroll
@@ -420,17 +459,17 @@ __device__ void mfma_segment(const DecodeArgs& a, int b, int kvh, int L, int j_l
   if (npairs > 1) mfma_issue<KV, D>(b1, a, ids, j_lo + 2, j_hi, L, kvh, status);
   int i = 0;
   for (; i + 3 < npairs; i += 2) {
-    mfma_compute<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
     mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
-    mfma_compute<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
     mfma_issue<KV, D>(b1, a, ids, j_lo + 2 * (i + 3), j_hi, L, kvh, status);
   }
   if (i < npairs) {
-    mfma_compute<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
     if (i + 2 < npairs) mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
   }
-  if (i + 1 < npairs) mfma_compute<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
-  if (i + 2 < npairs) mfma_compute<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+  if (i + 1 < npairs) mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
+  if (i + 2 < npairs) mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
 
   // Lanes c = 0..3 hold disjoint token subsets of head r: total the denominator.
   l_run += __shfl_xor(l_run, 16, 64);
@@ -549,13 +588,19 @@ __device__ __forceinline__ void vec_issue(VecBlock<KV, D>& bk, const DecodeArgs&
   }
 }
 
-template <KvType KV, int D, int GV>
+template <KvType KV, int D, int GV, bool MASKED>
 __device__ __forceinline__ void vec_compute(const VecBlock<KV, D>& bk, const float (&qf)[GV][VecCfg<KV, D>::ED],
                                             float scale_log2, float (&acc)[GV][VecCfg<KV, D>::ED],
                                             float (&m_run)[GV], float (&l_run)[GV]) {
   using C = VecCfg<KV, D>;
   const int r4 = lane_id() >> 4;
-  float s[4][GV];
+  const float coef = scale_log2 * bk.ks;
+  bool valid[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) valid[jj] = !MASKED || 4 * r4 + jj < bk.lim;
+  // logits of this row's 4 tokens for every head: lane-partial dot products
+  // over D/16 dims, reduced across the 16-lane row
+  float x[4][GV];
 #pragma unroll
   for (int jj = 0; jj < 4; ++jj) {
     float kf[C::ED];
@@ -565,13 +610,11 @@ __device__ __forceinline__ void vec_compute(const VecBlock<KV, D>& bk, const flo
       float part = 0.f;
 #pragma unroll
       for (int e = 0; e < C::ED; ++e) part = fmaf(qf[h][e], kf[e], part);
-      s[jj][h] = row_sum16(part);
+      const float sx = row_sum16(part) * coef;
+      x[jj][h] = valid[jj] ? sx : kNegInf;
     }
   }
-  bool valid[4];
-#pragma unroll
-  for (int jj = 0; jj < 4; ++jj) valid[jj] = 4 * r4 + jj < bk.lim;
-  // V rows (c16 + 16e) x this row's 4 tokens, masked by select.
+  // V rows (c16 + 16e) x this row's 4 tokens; dead slots selected to 0
   float vf[C::ED][4];
 #pragma unroll
   for (int e = 0; e < C::ED; ++e) {
@@ -580,32 +623,45 @@ __device__ __forceinline__ void vec_compute(const VecBlock<KV, D>& bk, const flo
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) vf[e][jj] = valid[jj] ? t4[jj] : 0.f;
   }
-  const float coef = scale_log2 * bk.ks;
+  float mx[GV];
+  bool grow = false;
 #pragma unroll
   for (int h = 0; h < GV; ++h) {
-    float x[4];
+    float m = fmaxf(fmaxf(x[0][h], x[1][h]), fmaxf(x[2][h], x[3][h]));
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    mx[h] = m;
+    grow |= m > m_run[h] + kMaxSlack;
+  }
+  if (__any(grow)) {  // wave-uniform lazy rescale, as in the MFMA kernel
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) x[jj] = valid[jj] ? s[jj][h] * coef : kNegInf;
-    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run[h], mx);
-    const float m_safe = m_new == kNegInf ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run[h] - m_safe);
-    m_run[h] = m_new;
+    for (int h = 0; h < GV; ++h) {
+      const float m_new = fmaxf(m_run[h], mx[h]);
+      const float alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run[h] - m_new);
+      m_run[h] = m_new;
+      l_run[h] *= alpha;
+#pragma unroll
+      for (int e = 0; e < C::ED; ++e) acc[h][e] *= alpha;
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < GV; ++h) {
+    const float m_ref = m_run[h] == kNegInf ? 0.f : m_run[h];
     float p[4];
     float psum = 0.f;
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      p[jj] = fast_exp2(x[jj] - m_safe);
+      p[jj] = fast_exp2(x[jj][h] - m_ref);
       psum += p[jj];
     }
-    l_run[h] = l_run[h] * alpha + psum;
+    l_run[h] += psum;
+    if constexpr (KV == KvType::FP8) {
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) p[jj] *= bk.vs;
+      for (int jj = 0; jj < 4; ++jj) p[jj] *= bk.vs;
+    }
 #pragma unroll
     for (int e = 0; e < C::ED; ++e) {
-      float t = acc[h][e] * alpha;
+      float t = acc[h][e];
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) t = fmaf(p[jj], vf[e][jj], t);
       acc[h][e] = t;
@@ -614,8 +670,18 @@ __device__ __forceinline__ void vec_compute(const VecBlock<KV, D>& bk, const flo
 }
 
 template <KvType KV, int D, int GV>
+__device__ __forceinline__ void vec_step(const VecBlock<KV, D>& bk, const float (&qf)[GV][VecCfg<KV, D>::ED],
+                                         float scale_log2, float (&acc)[GV][VecCfg<KV, D>::ED],
+                                         float (&m_run)[GV], float (&l_run)[GV]) {
+  if (bk.lim == kBlockSize)
+    vec_compute<KV, D, GV, false>(bk, qf, scale_log2, acc, m_run, l_run);
+  else
+    vec_compute<KV, D, GV, true>(bk, qf, scale_log2, acc, m_run, l_run);
+}
+
+template <KvType KV, int D, int GV>
 __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo, int j_hi, bool final,
-                            int64_t slot, int& status) {
+                            int64_t slot, int& status, int32_t* id_lds) {
   using C = VecCfg<KV, D>;
   const int l = lane_id();
   const int r4 = l >> 4, c16 = l & 15;
@@ -638,10 +704,8 @@ __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo
     }
   }
 
-  BlockIds ids;
-  ids.row = a.block_table + (int64_t)b * a.max_blocks;
-  ids.end = j_hi;
-  ids.load(j_lo);
+  BlockIds ids{a.block_table + (int64_t)b * a.max_blocks, j_hi, 0, id_lds};
+  ids.fill(j_lo);
 
   float acc[GV][C::ED];
   float m_run[GV], l_run[GV];
@@ -659,17 +723,17 @@ __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo
   if (n > 1) vec_issue<KV, D>(b1, a, ids, j_lo + 1, L, kvh, status);
   int i = 0;
   for (; i + 3 < n; i += 2) {
-    vec_compute<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
+    vec_step<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
     vec_issue<KV, D>(b0, a, ids, j_lo + i + 2, L, kvh, status);
-    vec_compute<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
+    vec_step<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
     vec_issue<KV, D>(b1, a, ids, j_lo + i + 3, L, kvh, status);
   }
   if (i < n) {
-    vec_compute<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
+    vec_step<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
     if (i + 2 < n) vec_issue<KV, D>(b0, a, ids, j_lo + i + 2, L, kvh, status);
   }
-  if (i + 1 < n) vec_compute<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
-  if (i + 2 < n) vec_compute<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
+  if (i + 1 < n) vec_step<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
+  if (i + 2 < n) vec_step<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
 
   // Each 16-lane row holds its own 4-token subsets: total over the 4 rows.
 #pragma unroll
@@ -714,7 +778,8 @@ __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo
 // ------------------------------------------------------------- persistent driver
 
 template <Variant V, KvType KV, int D, int GV>
-__global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
+__device__ __forceinline__ void decode_body(const DecodeArgs& a) {
+  __shared__ int32_t id_lds[kIdChunk];
   const int wave = blockIdx.x;
   const int64_t total = (int64_t)plan_total_blocks(a, wave == 0) * a.Hkv;
   int64_t share = (total + a.waves - 1) / a.waves;
@@ -744,31 +809,73 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     const bool final = j_lo == 0 && j_hi == nb;
     const int64_t slot = (int64_t)b * a.Hkv + kvh + wave;
     if constexpr (V == Variant::Mfma) {
-      mfma_segment<KV, D>(a, b, kvh, L, j_lo, j_hi, final, slot, status);
+      mfma_segment<KV, D>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
     } else {
-      vec_segment<KV, D, GV>(a, b, kvh, L, j_lo, j_hi, final, slot, status);
+      vec_segment<KV, D, GV>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
     }
     pos += j_hi - j_lo;
   }
   if (__any(status) && lane_id() == 0) atomicOr(a.hdr + kHdrStatus, status);
 }
 
+// The read-only inputs also arrive as __restrict__ kernel parameters: with
+// them marked noalias the compiler may read block ids and fp8 scales through
+// the scalar cache (the kernel's own stores to the workspace cannot clobber
+// them), which keeps id lookups off the vector-memory counter.
+__device__ __forceinline__ DecodeArgs with_inputs(DecodeArgs a, const void* __restrict__ q,
+                                                  const void* __restrict__ kc, const void* __restrict__ vc,
+                                                  const int32_t* __restrict__ bt,
+                                                  const int32_t* __restrict__ lens,
+                                                  const float* __restrict__ scales) {
+  a.q = q;
+  a.k_cache = kc;
+  a.v_cache = vc;
+  a.block_table = bt;
+  a.seq_lens = lens;
+  a.kv_scales = scales;
+  return a;
+}
+
+template <Variant V, KvType KV, int D, int GV>
+__global__ __launch_bounds__(64) void decode_kernel(
+    DecodeArgs a, const void* __restrict__ q, const void* __restrict__ kc, const void* __restrict__ vc,
+    const int32_t* __restrict__ bt, const int32_t* __restrict__ lens, const float* __restrict__ scales) {
+  decode_body<V, KV, D, GV>(with_inputs(a, q, kc, vc, bt, lens, scales));
+}
+
+template <Variant V, KvType KV, int D, int GV>
+__global__ __launch_bounds__(64) void decode_kernel_vec(
+    DecodeArgs a, const void* __restrict__ q, const void* __restrict__ kc, const void* __restrict__ vc,
+    const int32_t* __restrict__ bt, const int32_t* __restrict__ lens, const float* __restrict__ scales) {
+  decode_body<V, KV, D, GV>(with_inputs(a, q, kc, vc, bt, lens, scales));
+}
+
 // ------------------------------------------------------------- LSE combine
 
+constexpr int kCombineThreads = 256;
+constexpr int kCombineSegs = 64;  // segments staged in LDS per pass
+
 // One workgroup per (sequence, KV head) unit: merges the partial softmax states
-// of the waves that shared the unit, out = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w,
-// and writes zeros for empty sequences.
+// (m_w, l_w, acc_w) of the waves w that shared the unit,
+//     out = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w,   M = max_w m_w,
+// and writes zeros for empty sequences. Every (segment, head) state is read
+// by its own thread into LDS; the weights are formed there once; the
+// accumulator rows are then streamed with independent, batched loads.
 template <bool OUT_BF16, int D>
-__global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) {
+  __shared__ float s_m[kCombineSegs][kMaxGroup];
+  __shared__ float s_l[kCombineSegs][kMaxGroup];
+  __shared__ float s_M[kMaxGroup], s_den[kMaxGroup], s_scale[kMaxGroup];
   const int u = blockIdx.x;
   const int b = u / a.Hkv;
   const int kvh = u - b * a.Hkv;
   const int L = clamp_len(a, a.seq_lens[b]);
   const int nb = (L + kBlockSize - 1) / kBlockSize;
   const int G = a.G;
+  const int tid = threadIdx.x;
   const int64_t obase = ((int64_t)b * a.Hq + (int64_t)kvh * G) * D;
   if (nb == 0) {
-    for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
+    for (int i = tid; i < G * D; i += kCombineThreads) {
       if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = 0;
       else static_cast<float*>(a.out)[obase + i] = 0.f;
     }
@@ -777,24 +884,89 @@ __global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
   const int64_t share = a.share[0];
   const int64_t start = (int64_t)a.cum[b] * a.Hkv + (int64_t)kvh * nb;
   const int64_t w0 = start / share;
-  const int64_t w1 = (start + nb - 1) / share;
-  if (w0 == w1) return;  // one wave covered the unit and wrote the output
-  for (int i = threadIdx.x; i < G * D; i += blockDim.x) {
-    const int h = i / D;
-    const int d = i - h * D;
-    float M = kNegInf;
-    for (int64_t w = w0; w <= w1; ++w) M = fmaxf(M, a.ws_m[((int64_t)u + w) * G + h]);
-    const float M_safe = M == kNegInf ? 0.f : M;
-    float num = 0.f, den = 0.f;
-    for (int64_t w = w0; w <= w1; ++w) {
-      const int64_t s = ((int64_t)u + w) * G + h;
-      const float e = fast_exp2(a.ws_m[s] - M_safe);
-      num = fmaf(e, a.ws_acc[s * D + d], num);
-      den = fmaf(e, a.ws_l[s], den);
+  const int nseg = (int)((start + nb - 1) / share - w0) + 1;
+  if (nseg == 1) return;  // one wave covered the unit and wrote the output
+  const int64_t slot0 = (int64_t)u + w0;
+
+  constexpr int kPer = (kMaxGroup * D + kCombineThreads - 1) / kCombineThreads;
+  float acc[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) acc[k] = 0.f;
+  if (tid < kMaxGroup) {
+    s_M[tid] = kNegInf;
+    s_den[tid] = 0.f;
+  }
+  for (int s0 = 0; s0 < nseg; s0 += kCombineSegs) {
+    const int ns = nseg - s0 < kCombineSegs ? nseg - s0 : kCombineSegs;
+    for (int i = tid; i < ns * G; i += kCombineThreads) {
+      const int sg = i / G, h = i - sg * G;
+      const int64_t at = (slot0 + s0 + sg) * G + h;
+      s_m[sg][h] = a.ws_m[at];
+      s_l[sg][h] = a.ws_l[at];
     }
-    const float o = den > 0.f ? num / den : 0.f;
-    if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = (uint16_t)f32_to_bf16_bits(o);
-    else static_cast<float*>(a.out)[obase + i] = o;
+    __syncthreads();
+    // running max / denominator per head across passes; s_scale rescales the
+    // accumulators of earlier passes when the max moves
+    if (tid < G) {
+      float M = s_M[tid];
+      for (int sg = 0; sg < ns; ++sg) M = fmaxf(M, s_m[sg][tid]);
+      const float Ms = M == kNegInf ? 0.f : M;
+      const float Mold = s_M[tid] == kNegInf ? Ms : s_M[tid];
+      const float rescale = fast_exp2(Mold - Ms);
+      float den = s_den[tid] * rescale;
+      for (int sg = 0; sg < ns; ++sg) {
+        const float e = fast_exp2(s_m[sg][tid] - Ms);
+        s_m[sg][tid] = e;  // now the segment's weight
+        den = fmaf(e, s_l[sg][tid], den);
+      }
+      s_M[tid] = M;
+      s_den[tid] = den;
+      s_scale[tid] = rescale;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int i = tid + k * kCombineThreads;
+      if (i < G * D) acc[k] *= s_scale[i / D];
+    }
+    // four segments per batch: 4 x kPer independent loads in flight per thread
+    const float* base = a.ws_acc + (slot0 + s0) * G * D;
+    int sg = 0;
+    for (; sg + 4 <= ns; sg += 4) {
+      float v[4][kPer];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+          const int i = tid + k * kCombineThreads;
+          v[q][k] = i < G * D ? base[(int64_t)(sg + q) * G * D + i] : 0.f;
+        }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+          const int i = tid + k * kCombineThreads;
+          if (i < G * D) acc[k] = fmaf(s_m[sg + q][i / D], v[q][k], acc[k]);
+        }
+    }
+    for (; sg < ns; ++sg) {
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int i = tid + k * kCombineThreads;
+        if (i < G * D) acc[k] = fmaf(s_m[sg][i / D], base[(int64_t)sg * G * D + i], acc[k]);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = tid + k * kCombineThreads;
+    if (i < G * D) {
+      const float den = s_den[i / D];
+      const float o = den > 0.f ? acc[k] / den : 0.f;
+      if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = (uint16_t)f32_to_bf16_bits(o);
+      else static_cast<float*>(a.out)[obase + i] = o;
+    }
   }
 }
 
@@ -802,7 +974,8 @@ __global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
 
 template <Variant V, KvType KV, int D, int GV>
 void* kernel_ptr() {
-  return reinterpret_cast<void*>(&decode_kernel<V, KV, D, GV>);
+  if constexpr (V == Variant::Mfma) return reinterpret_cast<void*>(&decode_kernel<V, KV, D, GV>);
+  else return reinterpret_cast<void*>(&decode_kernel_vec<V, KV, D, GV>);
 }
 
 template <Variant V, KvType KV, int D>
@@ -839,7 +1012,13 @@ hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t 
   void* fn = pick(v, kv, a.D, a.G);
   if (!fn) return hipErrorInvalidValue;
   DecodeArgs args = a;
-  void* params[] = {&args};
+  const void* q = a.q;
+  const void* kc = a.k_cache;
+  const void* vc = a.v_cache;
+  const int32_t* bt = a.block_table;
+  const int32_t* lens = a.seq_lens;
+  const float* scales = a.kv_scales;
+  void* params[] = {&args, &q, &kc, &vc, &bt, &lens, &scales};
   return hipLaunchKernel(fn, dim3(a.waves), dim3(64), params, 0, s);
 }
 
@@ -855,7 +1034,7 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   if (units == 0) return hipSuccess;
   DecodeArgs args = a;
   void* params[] = {&args};
-  return hipLaunchKernel(fn, dim3(units), dim3(256), params, 0, s);
+  return hipLaunchKernel(fn, dim3(units), dim3(kCombineThreads), params, 0, s);
 }
 
 hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* wgs_per_cu) {
