@@ -862,19 +862,18 @@ __global__ __launch_bounds__(64) void decode_kernel_vec(
 // ------------------------------------------------------------- LSE combine
 
 constexpr int kCombineThreads = 256;
-constexpr int kCombineSegs = 64;  // segments staged in LDS per pass
+constexpr int kCombineChunk = 8;  // segments whose loads are in flight together
 
 // One workgroup per (sequence, KV head) unit: merges the partial softmax states
 // (m_w, l_w, acc_w) of the waves w that shared the unit,
 //     out = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w,   M = max_w m_w,
-// and writes zeros for empty sequences. Every (segment, head) state is read
-// by its own thread into LDS; the weights are formed there once; the
-// accumulator rows are then streamed with independent, batched loads.
+// and writes zeros for empty sequences. The kernel is latency-bound (a few KB
+// per unit), so it is organised around round trips: one for the unit's
+// segment range, then one per chunk of segments in which every thread loads
+// the (m, l) of its heads and its accumulator elements together and folds them
+// in with a running maximum.
 template <bool OUT_BF16, int D>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) {
-  __shared__ float s_m[kCombineSegs][kMaxGroup];
-  __shared__ float s_l[kCombineSegs][kMaxGroup];
-  __shared__ float s_M[kMaxGroup], s_den[kMaxGroup], s_scale[kMaxGroup];
   const int u = blockIdx.x;
   const int b = u / a.Hkv;
   const int kvh = u - b * a.Hkv;
@@ -897,85 +896,57 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   if (nseg == 1) return;  // one wave covered the unit and wrote the output
   const int64_t slot0 = (int64_t)u + w0;
 
-  constexpr int kPer = (kMaxGroup * D + kCombineThreads - 1) / kCombineThreads;
-  float acc[kPer];
+  // thread t owns head h = t / 16 (if < G) and dims [ (t % 16) * D/16, +D/16 )
+  constexpr int DE = D / 16;
+  const int h = tid >> 4;
+  const int d0 = (tid & 15) * DE;
+  if (h >= G) return;
+  float acc[DE];
 #pragma unroll
-  for (int k = 0; k < kPer; ++k) acc[k] = 0.f;
-  if (tid < kMaxGroup) {
-    s_M[tid] = kNegInf;
-    s_den[tid] = 0.f;
-  }
-  for (int s0 = 0; s0 < nseg; s0 += kCombineSegs) {
-    const int ns = nseg - s0 < kCombineSegs ? nseg - s0 : kCombineSegs;
-    for (int i = tid; i < ns * G; i += kCombineThreads) {
-      const int sg = i / G, h = i - sg * G;
-      const int64_t at = (slot0 + s0 + sg) * G + h;
-      s_m[sg][h] = a.ws_m[at];
-      s_l[sg][h] = a.ws_l[at];
+  for (int e = 0; e < DE; ++e) acc[e] = 0.f;
+  float M = kNegInf, den = 0.f;
+  for (int s0 = 0; s0 < nseg; s0 += kCombineChunk) {
+    const int ns = nseg - s0 < kCombineChunk ? nseg - s0 : kCombineChunk;
+    float vm[kCombineChunk], vl[kCombineChunk];
+    f32x4 va[kCombineChunk][DE / 4];
+#pragma unroll
+    for (int q = 0; q < kCombineChunk; ++q) {
+      const bool live = q < ns;
+      const int64_t at = (slot0 + s0 + (live ? q : 0)) * G + h;
+      vm[q] = live ? a.ws_m[at] : kNegInf;
+      vl[q] = live ? a.ws_l[at] : 0.f;
+      const f32x4* row = reinterpret_cast<const f32x4*>(a.ws_acc + at * D + d0);
+#pragma unroll
+      for (int e = 0; e < DE / 4; ++e) va[q][e] = live ? row[e] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    __syncthreads();
-    // running max / denominator per head across passes; s_scale rescales the
-    // accumulators of earlier passes when the max moves
-    if (tid < G) {
-      float M = s_M[tid];
-      for (int sg = 0; sg < ns; ++sg) M = fmaxf(M, s_m[sg][tid]);
-      const float Ms = M == kNegInf ? 0.f : M;
-      const float Mold = s_M[tid] == kNegInf ? Ms : s_M[tid];
-      const float rescale = fast_exp2(Mold - Ms);
-      float den = s_den[tid] * rescale;
-      for (int sg = 0; sg < ns; ++sg) {
-        const float e = fast_exp2(s_m[sg][tid] - Ms);
-        s_m[sg][tid] = e;  // now the segment's weight
-        den = fmaf(e, s_l[sg][tid], den);
-      }
-      s_M[tid] = M;
-      s_den[tid] = den;
-      s_scale[tid] = rescale;
-    }
-    __syncthreads();
+    float mc = M;
 #pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      const int i = tid + k * kCombineThreads;
-      if (i < G * D) acc[k] *= s_scale[i / D];
-    }
-    // four segments per batch: 4 x kPer independent loads in flight per thread
-    const float* base = a.ws_acc + (slot0 + s0) * G * D;
-    int sg = 0;
-    for (; sg + 4 <= ns; sg += 4) {
-      float v[4][kPer];
+    for (int q = 0; q < kCombineChunk; ++q) mc = fmaxf(mc, vm[q]);
+    const float ms = mc == kNegInf ? 0.f : mc;
+    const float r = fast_exp2((M == kNegInf ? ms : M) - ms);
+    den *= r;
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+    for (int e = 0; e < DE; ++e) acc[e] *= r;
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-          const int i = tid + k * kCombineThreads;
-          v[q][k] = i < G * D ? base[(int64_t)(sg + q) * G * D + i] : 0.f;
-        }
+    for (int q = 0; q < kCombineChunk; ++q) {
+      const float w = fast_exp2(vm[q] - ms);  // 0 for padded segments (m = -inf)
+      den = fmaf(w, vl[q], den);
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-          const int i = tid + k * kCombineThreads;
-          if (i < G * D) acc[k] = fmaf(s_m[sg + q][i / D], v[q][k], acc[k]);
-        }
-    }
-    for (; sg < ns; ++sg) {
-#pragma unroll
-      for (int k = 0; k < kPer; ++k) {
-        const int i = tid + k * kCombineThreads;
-        if (i < G * D) acc[k] = fmaf(s_m[sg][i / D], base[(int64_t)sg * G * D + i], acc[k]);
+      for (int e = 0; e < DE / 4; ++e) {
+        acc[4 * e] = fmaf(w, va[q][e][0], acc[4 * e]);
+        acc[4 * e + 1] = fmaf(w, va[q][e][1], acc[4 * e + 1]);
+        acc[4 * e + 2] = fmaf(w, va[q][e][2], acc[4 * e + 2]);
+        acc[4 * e + 3] = fmaf(w, va[q][e][3], acc[4 * e + 3]);
       }
     }
-    __syncthreads();
+    M = mc;
   }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  const int64_t o = obase + (int64_t)h * D + d0;
 #pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int i = tid + k * kCombineThreads;
-    if (i < G * D) {
-      const float den = s_den[i / D];
-      const float o = den > 0.f ? acc[k] / den : 0.f;
-      if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = (uint16_t)f32_to_bf16_bits(o);
-      else static_cast<float*>(a.out)[obase + i] = o;
-    }
+  for (int e = 0; e < DE; ++e) {
+    if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[o + e] = (uint16_t)f32_to_bf16_bits(acc[e] * inv);
+    else static_cast<float*>(a.out)[o + e] = acc[e] * inv;
   }
 }
 
