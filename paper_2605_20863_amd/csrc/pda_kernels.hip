@@ -43,6 +43,8 @@
 
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace pda {
 namespace {
 
@@ -249,12 +251,15 @@ struct MfmaCfg {
   }
 };
 
+// V^T slice of one M-tile: 4 tokens of one head-dim row (bf16: 2 words, fp8: 1)
+template <KvType KV>
+using VSlice = typename std::conditional<KV == KvType::BF16, u32x2, uint32_t>::type;
+
 template <KvType KV, int D>
 struct MfmaPair {
   using C = MfmaCfg<KV, D>;
   u32x4 k[2][C::NK4];
-  // V^T: 4 tokens of one dim row per M-tile: bf16 -> 2 words, fp8 -> 1 word
-  u32x2 v[2][C::MT];
+  VSlice<KV> v[2][C::MT];
   float ks[2], vs[2];
   int lim[2];
 };
@@ -297,12 +302,7 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
 #pragma unroll
       for (int m = 0; m < C::MT; ++m) {
         const uint8_t* pv = vt + m * 16 * kBlockSize * C::ESZ;
-        if constexpr (KV == KvType::BF16) {
-          bf.v[s][m] = ld_stream<u32x2>(pv);
-        } else {
-          bf.v[s][m].x = ld_stream<uint32_t>(pv);
-          bf.v[s][m].y = 0;
-        }
+        bf.v[s][m] = ld_stream<VSlice<KV>>(pv);
       }
       if constexpr (KV == KvType::FP8) {
         bf.ks[s] = a.kv_scales[blk.tile];
@@ -316,7 +316,7 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
 #pragma unroll
       for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = u32x4{0, 0, 0, 0};
 #pragma unroll
-      for (int m = 0; m < C::MT; ++m) bf.v[s][m] = u32x2{0, 0};
+      for (int m = 0; m < C::MT; ++m) bf.v[s][m] = VSlice<KV>{};
       bf.ks[s] = 0.f;
       bf.vs[s] = 0.f;
     }
@@ -414,8 +414,8 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
       v0 = bf.v[0][m];
       v1 = bf.v[1][m];
     } else {
-      v0 = fp8x4_to_bf16x4(bf.v[0][m].x);
-      v1 = fp8x4_to_bf16x4(bf.v[1][m].x);
+      v0 = fp8x4_to_bf16x4(bf.v[0][m]);
+      v1 = fp8x4_to_bf16x4(bf.v[1][m]);
     }
     u32x4 w = {v0.x, v0.y, v1.x, v1.y};
     if constexpr (MASKED) w = u32x4{v0.x & m0a, v0.y & m0b, v1.x & m1a, v1.y & m1b};
@@ -852,6 +852,15 @@ __global__ __launch_bounds__(64) void decode_kernel(
   decode_body<V, KV, D, GV>(with_inputs(a, q, kc, vc, bt, lens, scales));
 }
 
+// fp8 MFMA waves are held to two per SIMD (<= 256 VGPR + AGPR): the fp8 body
+// spends more VALU time per byte, and a second wave per SIMD covers it.
+template <Variant V, KvType KV, int D, int GV>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel_occ2(
+    DecodeArgs a, const void* __restrict__ q, const void* __restrict__ kc, const void* __restrict__ vc,
+    const int32_t* __restrict__ bt, const int32_t* __restrict__ lens, const float* __restrict__ scales) {
+  decode_body<V, KV, D, GV>(with_inputs(a, q, kc, vc, bt, lens, scales));
+}
+
 template <Variant V, KvType KV, int D, int GV>
 __global__ __launch_bounds__(64) void decode_kernel_vec(
     DecodeArgs a, const void* __restrict__ q, const void* __restrict__ kc, const void* __restrict__ vc,
@@ -954,7 +963,8 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
 
 template <Variant V, KvType KV, int D, int GV>
 void* kernel_ptr() {
-  if constexpr (V == Variant::Mfma) return reinterpret_cast<void*>(&decode_kernel<V, KV, D, GV>);
+  if constexpr (V == Variant::Mfma && KV == KvType::FP8) return reinterpret_cast<void*>(&decode_kernel_occ2<V, KV, D, GV>);
+  else if constexpr (V == Variant::Mfma) return reinterpret_cast<void*>(&decode_kernel<V, KV, D, GV>);
   else return reinterpret_cast<void*>(&decode_kernel_vec<V, KV, D, GV>);
 }
 
