@@ -299,6 +299,9 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
   a.len_cap = plan.len_cap;
   a.min_share = plan.min_share;
   a.waves = waves;
+  // Workgroups of 4 (or 2) independent waves when every CU gets whole groups:
+  // fewer, larger workgroups dispatch faster than one-wave groups.
+  a.waves_per_group = wpc % 4 == 0 ? 4 : (wpc % 2 == 0 ? 2 : 1);
   a.out_bf16 = problem->out_dtype == PDA_DTYPE_BF16;
   a.hdr = reinterpret_cast<int32_t*>(base + lay.hdr);
   a.share = a.hdr + 1;

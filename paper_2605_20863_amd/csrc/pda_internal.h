@@ -38,7 +38,8 @@ struct DecodeArgs {
   int64_t num_blocks;   // physical blocks (for the bounds check of table entries)
   int32_t len_cap;      // lengths are clamped into [0, len_cap]
   int32_t min_share;    // smallest per-wave share of block-heads
-  int32_t waves;        // launched persistent waves (one per workgroup)
+  int32_t waves;        // launched persistent waves (a multiple of waves_per_group)
+  int32_t waves_per_group;  // independent stream-K waves per workgroup: 1, 2 or 4
   int32_t out_bf16;     // 1: out is bf16, 0: f32
   // workspace
   int32_t* hdr;         // kHdrWords ints
@@ -58,7 +59,7 @@ inline int64_t partial_slots(int B, int Hkv, int waves) {
 // Launchers (pda_kernels.hip). Return hipSuccess or the launch error.
 hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
-// Max resident workgroups per CU for the decode kernel that (v, kv, D, G) selects.
-hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* wgs_per_cu);
+// Max resident waves per CU for the decode kernel that (v, kv, D, G) selects.
+hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* waves_per_cu);
 
 }  // namespace pda

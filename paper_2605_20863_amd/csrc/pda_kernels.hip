@@ -135,53 +135,90 @@ __device__ __forceinline__ int clamp_len(const DecodeArgs& a, int L) {
   return L < 0 ? 0 : (L > a.len_cap ? a.len_cap : L);
 }
 
-// Total block count over all sequences (wave-uniform). With write_cum, also
-// stores the exclusive prefix sum of per-sequence block counts and flags
-// clamped lengths.
-__device__ int plan_total_blocks(const DecodeArgs& a, bool write_cum) {
-  const int l = lane_id();
-  int carry = 0;
-  int bad = 0;
-  for (int b0 = 0; b0 < a.B; b0 += 64) {
-    const int b = b0 + l;
-    int n = 0;
-    if (b < a.B) {
-      const int raw = a.seq_lens[b];
-      const int L = clamp_len(a, raw);
-      bad |= (raw != L);
-      n = (L + kBlockSize - 1) / kBlockSize;
-    }
-    const int incl = wave_incl_scan(n);
-    if (write_cum && b < a.B) a.cum[b] = carry + incl - n;
-    carry += __shfl(incl, 63, 64);
-  }
-  if (write_cum && __any(bad) && l == 0) atomicOr(a.hdr + kHdrStatus, kStatusLenClamped);
-  return uni(carry);
+// Wave-uniform stream-K plan. Every wave scans seq_lens (block counts and
+// their exclusive prefix over sequences) to find the total, its own share and
+// the first sequence its range touches. Up to kPlanChunks * 64 sequences the
+// scan stays in registers; longer batches re-read seq_lens to locate.
+constexpr int kPlanChunks = 8;
+
+struct WavePlan {
+  int64_t total;  // block-heads in the step
+  int b;          // first sequence whose range contains pos
+  int cum_b;      // blocks of the sequences before b
+};
+
+__device__ __forceinline__ int blocks_of(const DecodeArgs& a, int b, int& bad) {
+  const int raw = a.seq_lens[b];
+  const int L = clamp_len(a, raw);
+  bad |= (raw != L);
+  return (L + kBlockSize - 1) / kBlockSize;
 }
 
-// First sequence whose block-head range contains stream position pos, and its
-// exclusive block prefix. pos must be < Hkv * total.
-__device__ void plan_locate(const DecodeArgs& a, int64_t pos, int& b_out, int& cum_out) {
+// Locate pos in chunk [b0, b0 + 64) whose exclusive prefix per lane is excl.
+__device__ __forceinline__ bool locate_in_chunk(const DecodeArgs& a, int64_t pos, int b0, int excl, int chunk_total,
+                                                int carry, WavePlan& p) {
+  if ((int64_t)(carry + chunk_total) * a.Hkv <= pos) return false;
+  const int b = b0 + lane_id();
+  const uint64_t m = __ballot(b < a.B && (int64_t)excl * a.Hkv <= pos);
+  const int idx = __popcll(m) - 1;
+  p.b = uni(b0 + idx);
+  p.cum_b = uni(__shfl(excl, idx, 64));
+  return true;
+}
+
+// share is filled from the total; returns false when the wave has no work.
+__device__ bool plan_wave(const DecodeArgs& a, int wave, WavePlan& p, int64_t& pos, int64_t& end,
+                          int64_t& share) {
   const int l = lane_id();
-  int carry = 0;
-  for (int b0 = 0; b0 < a.B; b0 += 64) {
-    const int b = b0 + l;
-    int n = 0;
-    if (b < a.B) n = (clamp_len(a, a.seq_lens[b]) + kBlockSize - 1) / kBlockSize;
-    const int incl = wave_incl_scan(n);
-    const int total = __shfl(incl, 63, 64);
-    if ((int64_t)(carry + total) * a.Hkv > pos) {
-      const int excl = carry + incl - n;
-      const uint64_t m = __ballot(b < a.B && (int64_t)excl * a.Hkv <= pos);
-      const int idx = __popcll(m) - 1;
-      b_out = uni(b0 + idx);
-      cum_out = uni(__shfl(excl, idx, 64));
-      return;
+  int carry = 0, bad = 0;
+  int excl_r[kPlanChunks], tot_r[kPlanChunks];
+#pragma unroll
+  for (int k = 0; k < kPlanChunks; ++k) {
+    excl_r[k] = 0;
+    tot_r[k] = 0;
+    const int b = k * 64 + l;
+    if (k * 64 < a.B) {
+      const int n = b < a.B ? blocks_of(a, b, bad) : 0;
+      const int incl = wave_incl_scan(n);
+      excl_r[k] = carry + incl - n;
+      if (wave == 0 && b < a.B) a.cum[b] = excl_r[k];
+      tot_r[k] = __shfl(incl, 63, 64);
+      carry += tot_r[k];
     }
-    carry += total;
   }
-  b_out = a.B;
-  cum_out = carry;
+  for (int b0 = kPlanChunks * 64; b0 < a.B; b0 += 64) {
+    const int b = b0 + l;
+    const int n = b < a.B ? blocks_of(a, b, bad) : 0;
+    const int incl = wave_incl_scan(n);
+    if (wave == 0 && b < a.B) a.cum[b] = carry + incl - n;
+    carry += __shfl(incl, 63, 64);
+  }
+  if (wave == 0 && __any(bad) && l == 0) atomicOr(a.hdr + kHdrStatus, kStatusLenClamped);
+  p.total = (int64_t)uni(carry) * a.Hkv;
+  share = (p.total + a.waves - 1) / a.waves;
+  if (share < a.min_share) share = a.min_share;
+  if (wave == 0 && l == 0) a.share[0] = (int32_t)share;
+  pos = (int64_t)wave * share;
+  end = pos + share < p.total ? pos + share : p.total;
+  if (pos >= end) return false;
+  int c = 0;
+#pragma unroll
+  for (int k = 0; k < kPlanChunks; ++k) {
+    if (k * 64 < a.B) {
+      if (locate_in_chunk(a, pos, k * 64, excl_r[k], tot_r[k], c, p)) return true;
+      c += tot_r[k];
+    }
+  }
+  for (int b0 = kPlanChunks * 64; b0 < a.B; b0 += 64) {
+    const int b = b0 + l;
+    int unused = 0;
+    const int n = b < a.B ? blocks_of(a, b, unused) : 0;
+    const int incl = wave_incl_scan(n);
+    const int t = __shfl(incl, 63, 64);
+    if (locate_in_chunk(a, pos, b0, c + incl - n, t, c, p)) return true;
+    c += t;
+  }
+  return false;  // unreachable: pos < total
 }
 
 // A segment's block ids, staged through a per-wave LDS chunk. Tile addresses
@@ -191,6 +228,7 @@ __device__ void plan_locate(const DecodeArgs& a, int64_t pos, int& b_out, int& c
 // counted separately (lgkmcnt); the chunk refill, which does wait for its own
 // global load, runs once per kIdChunk blocks.
 constexpr int kIdChunk = 128;
+constexpr int kWavesPerGroupMax = 4;  // stream-K waves per workgroup (independent)
 
 struct BlockIds {
   const int32_t* row;
@@ -200,7 +238,11 @@ struct BlockIds {
   __device__ void fill(int j) {
     base = j;
     for (int i = lane_id(); i < kIdChunk; i += 64) lds[i] = j + i < end ? row[j + i] : 0;
-    __syncthreads();  // one-wave workgroup: orders the LDS writes before the reads
+    // the chunk is private to this wave: order its LDS writes before its reads
+    // (waves of one workgroup run independent ranges and never meet at a barrier)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   __device__ int get(int j) {
     if (j >= base + kIdChunk) fill(j);
@@ -788,18 +830,14 @@ __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo
 
 template <Variant V, KvType KV, int D, int GV>
 __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
-  __shared__ int32_t id_lds[kIdChunk];
-  const int wave = blockIdx.x;
-  const int64_t total = (int64_t)plan_total_blocks(a, wave == 0) * a.Hkv;
-  int64_t share = (total + a.waves - 1) / a.waves;
-  if (share < a.min_share) share = a.min_share;
-  if (wave == 0 && lane_id() == 0) a.share[0] = (int32_t)share;
-  int64_t pos = (int64_t)wave * share;
-  const int64_t end = pos + share < total ? pos + share : total;
-  if (pos >= end) return;
-
-  int b, cum_b;
-  plan_locate(a, pos, b, cum_b);
+  __shared__ int32_t id_lds_all[kWavesPerGroupMax][kIdChunk];
+  const int wave_in_group = threadIdx.x >> 6;
+  int32_t* id_lds = id_lds_all[wave_in_group];
+  const int wave = blockIdx.x * (blockDim.x >> 6) + wave_in_group;
+  WavePlan plan;
+  int64_t pos, end, share;
+  if (!plan_wave(a, wave, plan, pos, end, share)) return;
+  int b = plan.b, cum_b = plan.cum_b;
   int status = 0;
   while (pos < end && b < a.B) {
     const int L = clamp_len(a, a.seq_lens[b]);
@@ -846,7 +884,7 @@ __device__ __forceinline__ DecodeArgs with_inputs(DecodeArgs a, const void* __re
 }
 
 template <Variant V, KvType KV, int D, int GV>
-__global__ __launch_bounds__(64) void decode_kernel(
+__global__ __launch_bounds__(256) void decode_kernel(
     DecodeArgs a, const void* __restrict__ q, const void* __restrict__ kc, const void* __restrict__ vc,
     const int32_t* __restrict__ bt, const int32_t* __restrict__ lens, const float* __restrict__ scales) {
   decode_body<V, KV, D, GV>(with_inputs(a, q, kc, vc, bt, lens, scales));
@@ -855,14 +893,14 @@ __global__ __launch_bounds__(64) void decode_kernel(
 // fp8 MFMA waves are held to two per SIMD (<= 256 VGPR + AGPR): the fp8 body
 // spends more VALU time per byte, and a second wave per SIMD covers it.
 template <Variant V, KvType KV, int D, int GV>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel_occ2(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void decode_kernel_occ2(
     DecodeArgs a, const void* __restrict__ q, const void* __restrict__ kc, const void* __restrict__ vc,
     const int32_t* __restrict__ bt, const int32_t* __restrict__ lens, const float* __restrict__ scales) {
   decode_body<V, KV, D, GV>(with_inputs(a, q, kc, vc, bt, lens, scales));
 }
 
 template <Variant V, KvType KV, int D, int GV>
-__global__ __launch_bounds__(64) void decode_kernel_vec(
+__global__ __launch_bounds__(256) void decode_kernel_vec(
     DecodeArgs a, const void* __restrict__ q, const void* __restrict__ kc, const void* __restrict__ vc,
     const int32_t* __restrict__ bt, const int32_t* __restrict__ lens, const float* __restrict__ scales) {
   decode_body<V, KV, D, GV>(with_inputs(a, q, kc, vc, bt, lens, scales));
@@ -1009,7 +1047,8 @@ hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t 
   const int32_t* lens = a.seq_lens;
   const float* scales = a.kv_scales;
   void* params[] = {&args, &q, &kc, &vc, &bt, &lens, &scales};
-  return hipLaunchKernel(fn, dim3(a.waves), dim3(64), params, 0, s);
+  const int wpg = a.waves_per_group;
+  return hipLaunchKernel(fn, dim3(a.waves / wpg), dim3(64 * wpg), params, 0, s);
 }
 
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
@@ -1027,10 +1066,13 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   return hipLaunchKernel(fn, dim3(units), dim3(kCombineThreads), params, 0, s);
 }
 
-hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* wgs_per_cu) {
+hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* waves_per_cu) {
   void* fn = pick(v, kv, D, G);
   if (!fn) return hipErrorInvalidValue;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(wgs_per_cu, fn, 64, 0);
+  int wgs = 0;
+  const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&wgs, fn, 64, 0);
+  *waves_per_cu = wgs;
+  return e;
 }
 
 }  // namespace pda
