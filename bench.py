@@ -165,6 +165,8 @@ def main():
     ap.add_argument("--variant", default="auto", choices=["auto", "vector", "mfma"])
     ap.add_argument("--waves-per-cu", type=int, default=0)
     ap.add_argument("--min-blocks-per-wave", type=int, default=0)
+    ap.add_argument("--chunks-per-wave", type=int, default=0, help="1 = static split; 0 = library default")
+    ap.add_argument("--min-blocks-per-chunk", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle wall time")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
@@ -213,7 +215,8 @@ def main():
     stream = torch.cuda.current_stream(dev)
     prob = _lib.problem_for(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens,
                             inp.layout.max_seq_len, out)
-    opts = _lib.make_options(args.variant, args.waves_per_cu, args.min_blocks_per_wave)
+    opts = _lib.make_options(args.variant, args.waves_per_cu, args.min_blocks_per_wave, args.chunks_per_wave,
+                             args.min_blocks_per_chunk)
     ptrs = [(k.data_ptr(), v.data_ptr(), s.data_ptr() if s is not None else None) for k, v, s in caches]
     sh = stream.cuda_stream
     qp, bp, lp, op = inp.q.data_ptr(), inp.block_table.data_ptr(), inp.seq_lens.data_ptr(), out.data_ptr()
@@ -229,23 +232,26 @@ def main():
     torch.cuda.synchronize()
     assert torch.isfinite(out.float()).all(), "non-finite output"
 
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    # Timed region: K back-to-back calls. Two HIP events on the calls' stream
+    # bracket it (events between calls would add their own GPU time), so the
+    # per-call GPU time is the region's event time / K, directly comparable
+    # with rocprofv3's decode + combine kernel durations.
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev0.record(stream)
     for i in range(args.steps):
-        starts[i].record(stream)
         step(i)
-        ends[i].record(stream)
+    ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_call_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    call_ms = float(np.mean(per_call_ms))
+    call_ms = ev0.elapsed_time(ev1) / args.steps
     ms_per_step = wall * 1e3 / args.steps
     status = _lib.read_device_status()
     print(f"[bench] {w.name}: {ms_per_step * 1e3:.1f} us/step wall, {call_ms * 1e3:.1f} us/call GPU "
-          f"(median {np.median(per_call_ms) * 1e3:.1f}, min {min(per_call_ms) * 1e3:.1f}), "
-          f"{ncopies} cache copies, status {status}", file=sys.stderr, flush=True)
+          f"(HIP events over the timed region), {ncopies} cache copies, status {status}",
+          file=sys.stderr, flush=True)
 
     achieved = nbytes / (call_ms * 1e-3) / 1e9
     value = nbytes / (ms_per_step * 1e-3) / 1e9

@@ -93,25 +93,33 @@ typedef struct pda_problem {
 
 /* Optional tuning knobs; pass NULL for the defaults (all zero). */
 typedef struct pda_options {
-  int32_t variant;             /* pda_variant */
-  int32_t waves_per_cu;        /* persistent waves launched per compute unit; 0 = auto */
-  int32_t min_blocks_per_wave; /* smallest share of KV blocks one wave takes; 0 = auto */
+  int32_t variant;              /* pda_variant */
+  int32_t waves_per_cu;         /* persistent waves launched per compute unit; 0 = auto */
+  int32_t min_blocks_per_wave;  /* no chunk of work is smaller than this many block-heads
+                                   (16 tokens of one KV head); 0 = auto (8) */
+  int32_t chunks_per_wave;      /* 1 = static split (one equal chunk per wave); k > 1 = up to
+                                   k chunks per wave, handed out dynamically; 0 = default (1) */
+  int32_t min_blocks_per_chunk; /* a dynamic split makes no chunk smaller than this many
+                                   block-heads; 0 = auto (512 KiB of K and V) */
 } pda_options;
 
 /* Host-side plan of one call: what pda_paged_decode_attention would launch. */
 typedef struct pda_plan_info {
   int32_t variant;             /* the kernel family that runs (never AUTO) */
-  int32_t waves;               /* persistent waves (one per workgroup) */
+  int32_t waves;               /* persistent waves (workgroups of up to 4 independent waves) */
   int32_t group_size;          /* G = num_q_heads / num_kv_heads */
+  int32_t chunks_max;          /* most chunks the split can cut (waves * chunks_per_wave) */
   int64_t workspace_bytes;     /* library-owned device workspace this call needs */
 } pda_plan_info;
 
 /*
  * One batched decode-attention step, enqueued on `stream` (a hipStream_t; NULL
  * is the null stream). Asynchronous: results are valid once the stream has
- * reached this point. Work is split so every persistent wave reads an equal
- * share of the step's KV blocks; a sequence split between waves is finished by
- * a log-sum-exp combine kernel on the same stream.
+ * reached this point. The step's KV blocks are cut into equal chunks that
+ * persistent waves take in turn (each wave its own first chunk, the rest in
+ * arrival order); a sequence split between chunks is finished by a
+ * log-sum-exp combine kernel on the same stream. The result does not depend
+ * on which wave ran which chunk: repeated calls give identical output.
  *
  * Ownership: the caller owns every buffer; the library keeps no pointer to
  * them after returning. It owns one device workspace per (device, stream),
@@ -139,6 +147,9 @@ int pda_paged_decode_attention(const void* q,
 
 /* Validate `problem` / `options` and describe the launch, on the host only
  * (no HIP call). `num_compute_units` sizes the persistent grid (MI355X: 256).
+ * With options.waves_per_cu = 0 the launch takes the decode kernel's
+ * occupancy (at most 8 waves per CU), which only the device knows: `waves`,
+ * `chunks_max` and `workspace_bytes` are then upper bounds (8 waves per CU).
  * Returns the same error codes as pda_paged_decode_attention. */
 int pda_query_plan(const pda_problem* problem,
                    const pda_options* options,

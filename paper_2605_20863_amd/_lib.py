@@ -64,6 +64,8 @@ class Options(ctypes.Structure):
         ("variant", ctypes.c_int32),
         ("waves_per_cu", ctypes.c_int32),
         ("min_blocks_per_wave", ctypes.c_int32),
+        ("chunks_per_wave", ctypes.c_int32),
+        ("min_blocks_per_chunk", ctypes.c_int32),
     ]
 
 
@@ -72,6 +74,7 @@ class PlanInfo(ctypes.Structure):
         ("variant", ctypes.c_int32),
         ("waves", ctypes.c_int32),
         ("group_size", ctypes.c_int32),
+        ("chunks_max", ctypes.c_int32),
         ("workspace_bytes", ctypes.c_int64),
     ]
 
@@ -119,9 +122,11 @@ def _check(rc):
     return rc
 
 
-def make_options(variant="auto", waves_per_cu=0, min_blocks_per_wave=0) -> Options:
+def make_options(variant="auto", waves_per_cu=0, min_blocks_per_wave=0, chunks_per_wave=0,
+                 min_blocks_per_chunk=0) -> Options:
     v = _VARIANTS[variant] if isinstance(variant, str) else int(variant)
-    return Options(v, int(waves_per_cu), int(min_blocks_per_wave))
+    return Options(v, int(waves_per_cu), int(min_blocks_per_wave), int(chunks_per_wave),
+                   int(min_blocks_per_chunk))
 
 
 def raw_call(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale,
@@ -192,7 +197,8 @@ def problem_for(q, k_cache, v_cache, block_table, seq_lens, max_seq_len=0, out=N
 
 def paged_decode_attention(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out,
                            softmax_scale, max_seq_len=0, stream=None, variant="auto",
-                           waves_per_cu=0, min_blocks_per_wave=0):
+                           waves_per_cu=0, min_blocks_per_wave=0, chunks_per_wave=0,
+                           min_blocks_per_chunk=0):
     """Enqueue one decode-attention step on ``stream`` (default: torch's current stream).
 
     All tensors live on the same HIP device and are contiguous; layouts and
@@ -220,7 +226,7 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, seq_lens, kv_scales
     prob = problem_for(q, k_cache, v_cache, block_table, seq_lens, max_seq_len, out)
     if kv_scales is not None and tuple(kv_scales.shape) != (2, prob.num_blocks, prob.num_kv_heads):
         raise ValueError("kv_scales must be [2, num_blocks, num_kv_heads]")
-    opts = make_options(variant, waves_per_cu, min_blocks_per_wave)
+    opts = make_options(variant, waves_per_cu, min_blocks_per_wave, chunks_per_wave, min_blocks_per_chunk)
     with torch.cuda.device(dev):
         rc = raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
                       seq_lens.data_ptr(), kv_scales.data_ptr() if kv_scales is not None else None,

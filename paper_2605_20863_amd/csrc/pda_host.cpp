@@ -38,6 +38,11 @@ int fail_hip(hipError_t e, const char* what) {
 
 constexpr int kDefaultWavesPerCu = 8;   // upper bound used by pda_query_plan
 constexpr int kDefaultMinShare = 8;     // blocks: below this a wave's fixed costs dominate
+// Static split by default: with chunk switches that drain a wave's load
+// pipeline, handing out chunks dynamically measured slower on every step
+// shape tried (the last chunk's tail outweighs the balance it buys).
+constexpr int kDefaultChunksPerWave = 1;
+constexpr int64_t kChunkMinBytes = 512 << 10;  // of K and V: a chunk outlasts its start-up costs
 constexpr int64_t kAlign = 256;
 
 int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -49,6 +54,8 @@ struct Plan {
   int len_cap;
   int waves_per_cu;  // 0 = decide from occupancy at launch
   int min_share;
+  int chunks_per_wave;
+  int chunk_min;
 };
 
 // Validate everything that does not need a device. Returns PDA_OK or an error.
@@ -110,6 +117,10 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
     return fail(PDA_EINVAL, "options.waves_per_cu = %d (0..64)", op->waves_per_cu);
   if (op && op->min_blocks_per_wave < 0)
     return fail(PDA_EINVAL, "options.min_blocks_per_wave = %d < 0", op->min_blocks_per_wave);
+  if (op && (op->chunks_per_wave < 0 || op->chunks_per_wave > 64))
+    return fail(PDA_EINVAL, "options.chunks_per_wave = %d (0..64)", op->chunks_per_wave);
+  if (op && op->min_blocks_per_chunk < 0)
+    return fail(PDA_EINVAL, "options.min_blocks_per_chunk = %d < 0", op->min_blocks_per_chunk);
 
   plan->variant = variant == PDA_VARIANT_MFMA ? pda::Variant::Mfma : pda::Variant::Vector;
   plan->kv = kd == PDA_DTYPE_F32 ? pda::KvType::F32 : (kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8);
@@ -117,6 +128,11 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
   plan->len_cap = pr->max_seq_len > 0 ? pr->max_seq_len : (int)table_tokens;
   plan->waves_per_cu = op ? op->waves_per_cu : 0;
   plan->min_share = (op && op->min_blocks_per_wave > 0) ? op->min_blocks_per_wave : kDefaultMinShare;
+  plan->chunks_per_wave = (op && op->chunks_per_wave > 0) ? op->chunks_per_wave : kDefaultChunksPerWave;
+  const int esz = kd == PDA_DTYPE_F32 ? 4 : (kd == PDA_DTYPE_BF16 ? 2 : 1);
+  const int64_t block_head_bytes = 2LL * pda::kBlockSize * pr->head_dim * esz;
+  plan->chunk_min = (op && op->min_blocks_per_chunk > 0) ? op->min_blocks_per_chunk
+                                                         : (int)(kChunkMinBytes / block_head_bytes);
   return PDA_OK;
 }
 
@@ -124,9 +140,9 @@ struct Layout {
   int64_t hdr, cum, m, l, acc, total;
 };
 
-Layout workspace_layout(const pda_problem* pr, int G, int waves) {
+Layout workspace_layout(const pda_problem* pr, int G, int chunks_max) {
   Layout w;
-  const int64_t slots = pda::partial_slots(pr->num_seqs, pr->num_kv_heads, waves);
+  const int64_t slots = pda::partial_slots(pr->num_seqs, pr->num_kv_heads, chunks_max);
   w.hdr = 0;
   w.cum = align_up(pda::kHdrWords * 4);
   w.m = w.cum + align_up((int64_t)pr->num_seqs * 4);
@@ -148,6 +164,9 @@ struct Workspace {
   std::mutex mu;
   void* ptr = nullptr;
   int64_t bytes = 0;
+  // The combine kernel zeroes the chunk counter after each decode kernel; if a
+  // combine launch failed, the next call zeroes it first.
+  bool rearm = false;
 };
 
 std::mutex g_mu;
@@ -218,6 +237,7 @@ int ensure_workspace(Workspace* ws, int64_t bytes, hipStream_t s) {
     return fail(PDA_ENOMEM, "hipMalloc(%lld) of the workspace: %s", (long long)want, hipGetErrorString(e));
   }
   ws->bytes = want;
+  ws->rearm = false;
   if ((e = hipMemsetAsync(ws->ptr, 0, pda::kHdrWords * 4, s)) != hipSuccess) return fail_hip(e, "hipMemsetAsync");
   return PDA_OK;
 }
@@ -239,10 +259,13 @@ int pda_query_plan(const pda_problem* problem, const pda_options* options, float
   int rc = validate(problem, options, softmax_scale, &plan);
   if (rc != PDA_OK) return rc;
   const int wpc = plan.waves_per_cu > 0 ? plan.waves_per_cu : kDefaultWavesPerCu;
+  if ((int64_t)num_compute_units * wpc * plan.chunks_per_wave > INT32_MAX)
+    return fail(PDA_EINVAL, "num_compute_units = %d is too large", num_compute_units);
   info->variant = plan.variant == pda::Variant::Mfma ? PDA_VARIANT_MFMA : PDA_VARIANT_VECTOR;
   info->waves = num_compute_units * wpc;
   info->group_size = plan.G;
-  info->workspace_bytes = workspace_layout(problem, plan.G, info->waves).total;
+  info->chunks_max = info->waves * plan.chunks_per_wave;
+  info->workspace_bytes = workspace_layout(problem, plan.G, info->chunks_max).total;
   return PDA_OK;
 }
 
@@ -273,12 +296,18 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
     if (wpc > kDefaultWavesPerCu) wpc = kDefaultWavesPerCu;
   }
   const int waves = di.cus * wpc;
-  const Layout lay = workspace_layout(problem, plan.G, waves);
+  const int chunks_max = waves * plan.chunks_per_wave;
+  const Layout lay = workspace_layout(problem, plan.G, chunks_max);
 
   Workspace* ws = workspace_for(dev, stream);
   std::lock_guard<std::mutex> lk(ws->mu);
   if ((rc = ensure_workspace(ws, lay.total, stream)) != PDA_OK) return rc;
   char* base = static_cast<char*>(ws->ptr);
+  if (ws->rearm) {
+    if ((e = hipMemsetAsync(base + pda::kHdrNext * 4, 0, 4, stream)) != hipSuccess)
+      return fail_hip(e, "hipMemsetAsync");
+    ws->rearm = false;
+  }
 
   pda::DecodeArgs a;
   a.q = q;
@@ -298,13 +327,15 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
   a.num_blocks = problem->num_blocks;
   a.len_cap = plan.len_cap;
   a.min_share = plan.min_share;
+  a.chunk_min = plan.chunk_min;
+  a.chunks_max = chunks_max;
   a.waves = waves;
   // Workgroups of 4 (or 2) independent waves when every CU gets whole groups:
   // fewer, larger workgroups dispatch faster than one-wave groups.
   a.waves_per_group = wpc % 4 == 0 ? 4 : (wpc % 2 == 0 ? 2 : 1);
   a.out_bf16 = problem->out_dtype == PDA_DTYPE_BF16;
   a.hdr = reinterpret_cast<int32_t*>(base + lay.hdr);
-  a.share = a.hdr + 1;
+  a.share = a.hdr + pda::kHdrShare;
   a.cum = reinterpret_cast<int32_t*>(base + lay.cum);
   a.ws_m = reinterpret_cast<float*>(base + lay.m);
   a.ws_l = reinterpret_cast<float*>(base + lay.l);
@@ -312,7 +343,10 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
 
   if ((e = pda::launch_decode(a, plan.variant, plan.kv, stream)) != hipSuccess)
     return fail_hip(e, "decode kernel launch");
-  if ((e = pda::launch_combine(a, stream)) != hipSuccess) return fail_hip(e, "combine kernel launch");
+  if ((e = pda::launch_combine(a, stream)) != hipSuccess) {
+    ws->rearm = true;
+    return fail_hip(e, "combine kernel launch");
+  }
   return PDA_OK;
 }
 

@@ -21,6 +21,8 @@ constexpr int kStatusBadBlock = 2;
 
 // Workspace header words.
 constexpr int kHdrStatus = 0;
+constexpr int kHdrShare = 1;  // block-heads per chunk (decode writes, combine reads)
+constexpr int kHdrNext = 2;   // chunk counter of a dynamic split; zero between calls
 constexpr int kHdrWords = 16;
 
 // Everything one decode step's kernels need. Plain data; passed by value.
@@ -37,23 +39,25 @@ struct DecodeArgs {
   int32_t max_blocks;   // block_table row stride
   int64_t num_blocks;   // physical blocks (for the bounds check of table entries)
   int32_t len_cap;      // lengths are clamped into [0, len_cap]
-  int32_t min_share;    // smallest per-wave share of block-heads
+  int32_t min_share;    // smallest chunk, in block-heads
+  int32_t chunk_min;    // a dynamic split makes no chunk smaller than this
+  int32_t chunks_max;   // at most this many chunks; <= waves means a static split
   int32_t waves;        // launched persistent waves (a multiple of waves_per_group)
   int32_t waves_per_group;  // independent stream-K waves per workgroup: 1, 2 or 4
   int32_t out_bf16;     // 1: out is bf16, 0: f32
   // workspace
   int32_t* hdr;         // kHdrWords ints
   int32_t* cum;         // [B] exclusive prefix sum of blocks per sequence
-  int32_t* share;       // [1] blocks per wave (written by wave 0, read by the combine)
+  int32_t* share;       // [1] block-heads per chunk (written by wave 0, read by the combine)
   float* ws_m;          // [slots, G] running max (base 2) per partial
   float* ws_l;          // [slots, G] softmax denominator per partial
   float* ws_acc;        // [slots, G, D] unnormalised output per partial
 };
 
-// Number of partial-result slots one call can need: one per (unit, wave)
-// intersection, bounded by units + waves.
-inline int64_t partial_slots(int B, int Hkv, int waves) {
-  return (int64_t)B * Hkv + waves;
+// Number of partial-result slots one call can need: one per (unit, chunk)
+// intersection, bounded by units + chunks.
+inline int64_t partial_slots(int B, int Hkv, int chunks_max) {
+  return (int64_t)B * Hkv + chunks_max;
 }
 
 // Launchers (pda_kernels.hip). Return hipSuccess or the launch error.

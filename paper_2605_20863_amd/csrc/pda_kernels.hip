@@ -8,15 +8,17 @@
 // how lengths are distributed:
 //
 // * Stream-K split. The (sequence, KV head) units are laid end to end as one
-//   stream of 16-token block-heads (sequence-major, KV head minor). Wave w of a
-//   persistent grid takes the contiguous range [w*Q, (w+1)*Q) of that stream,
-//   Q = ceil(total / waves). Every wave reads the same number of KV bytes, no
-//   matter how lengths are distributed. A wave whose range covers a whole unit
-//   writes the normalised output; otherwise it writes the unit's partial
-//   softmax state (m, l, acc) to slot (unit + wave), and the combine kernel
-//   merges a unit's partials with log-sum-exp rescaling. Every wave plans its
-//   own range from seq_lens (a prefix sum over sequences), so one call is two
-//   launches and needs neither atomics nor a planning kernel.
+//   stream of 16-token block-heads (sequence-major, KV head minor), cut into
+//   equal chunks. By default wave w of a persistent grid takes chunk w, the
+//   range [w*Q, (w+1)*Q) with Q = ceil(total / waves), so every wave reads the
+//   same number of KV bytes no matter how lengths are distributed; optionally
+//   the chunks are smaller and the waves take the rest from a counter in
+//   arrival order. A chunk that covers a whole unit writes its normalised
+//   output; otherwise it writes the unit's partial softmax state (m, l, acc)
+//   to slot (unit + chunk), and the combine kernel merges a unit's partials
+//   with log-sum-exp rescaling. Every wave plans from seq_lens itself (a
+//   prefix sum over sequences), so one call is two launches and needs no
+//   planning kernel.
 //
 // * Two wave kernels share that driver:
 //   - MFMA (bf16 or fp8 cache, bf16 q): per pair of 16-token blocks,
@@ -135,90 +137,125 @@ __device__ __forceinline__ int clamp_len(const DecodeArgs& a, int L) {
   return L < 0 ? 0 : (L > a.len_cap ? a.len_cap : L);
 }
 
-// Wave-uniform stream-K plan. Every wave scans seq_lens (block counts and
-// their exclusive prefix over sequences) to find the total, its own share and
-// the first sequence its range touches. Up to kPlanChunks * 64 sequences the
-// scan stays in registers; longer batches re-read seq_lens to locate.
-constexpr int kPlanChunks = 8;
+// Stream-K plan, computed by every wave from seq_lens. The stream of
+// block-heads is cut into chunks of Q block-heads, chunk c covering
+// [c*Q, (c+1)*Q). In a static split Q = ceil(total / waves) and wave w runs
+// chunk w only. In a dynamic split Q is smaller (chunks_max > waves chunks at
+// most, none below chunk_min): wave w starts on chunk w and then takes chunks
+// waves, waves + 1, ... in arrival order from a counter in the workspace
+// header, so the waves the hardware serves faster read more of the stream
+// (two waves sharing a SIMD are not served equally). A partial result's slot
+// is (unit + chunk), not (unit + wave), so the values written and merged do
+// not depend on which wave ran a chunk.
+constexpr int kTileSeqs = 512;  // sequences one planning round trip covers, 8 per lane
+constexpr int kLdsSeqs = 512;   // batches up to this size keep their prefix sums in LDS
 
-struct WavePlan {
-  int64_t total;  // block-heads in the step
-  int b;          // first sequence whose range contains pos
-  int cum_b;      // blocks of the sequences before b
+struct StreamPlan {
+  int64_t total;    // block-heads in the step
+  int64_t chunk;    // Q
+  int64_t nchunks;  // ceil(total / Q)
 };
 
-__device__ __forceinline__ int blocks_of(const DecodeArgs& a, int b, int& bad) {
-  const int raw = a.seq_lens[b];
-  const int L = clamp_len(a, raw);
-  bad |= (raw != L);
-  return (L + kBlockSize - 1) / kBlockSize;
+// Block counts of sequences [t0, t0 + 512), lane l owning t0 + 8l .. +7 (all
+// eight lengths are loaded before any is used, so the tile costs one round
+// trip). incl[i] = inclusive prefix within the lane, base = the lane's
+// exclusive prefix within the tile; returns the tile total.
+__device__ __forceinline__ int load_tile(const DecodeArgs& a, int t0, int (&incl)[8], int& base, int& bad) {
+  const int s0 = t0 + 8 * lane_id();
+  int raw[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) raw[i] = s0 + i < a.B ? a.seq_lens[s0 + i] : 0;
+  int run = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int L = clamp_len(a, raw[i]);
+    bad |= (L != raw[i]);
+    run += (L + kBlockSize - 1) / kBlockSize;
+    incl[i] = run;
+  }
+  const int x = wave_incl_scan(run);
+  base = x - run;
+  return __shfl(x, 63, 64);
 }
 
-// Locate pos in chunk [b0, b0 + 64) whose exclusive prefix per lane is excl.
-__device__ __forceinline__ bool locate_in_chunk(const DecodeArgs& a, int64_t pos, int b0, int excl, int chunk_total,
-                                                int carry, WavePlan& p) {
-  if ((int64_t)(carry + chunk_total) * a.Hkv <= pos) return false;
-  const int b = b0 + lane_id();
-  const uint64_t m = __ballot(b < a.B && (int64_t)excl * a.Hkv <= pos);
-  const int idx = __popcll(m) - 1;
-  p.b = uni(b0 + idx);
-  p.cum_b = uni(__shfl(excl, idx, 64));
-  return true;
-}
-
-// share is filled from the total; returns false when the wave has no work.
-__device__ bool plan_wave(const DecodeArgs& a, int wave, WavePlan& p, int64_t& pos, int64_t& end,
-                          int64_t& share) {
-  const int l = lane_id();
+// Wave 0 also publishes the prefix sums (cum) and Q (share) for the combine.
+__device__ void plan_stream(const DecodeArgs& a, int wave, int32_t* pre, StreamPlan& p) {
   int carry = 0, bad = 0;
-  int excl_r[kPlanChunks], tot_r[kPlanChunks];
+  for (int t0 = 0; t0 < a.B; t0 += kTileSeqs) {
+    int incl[8], base;
+    const int tot = load_tile(a, t0, incl, base, bad);
+    const int s0 = t0 + 8 * lane_id();
 #pragma unroll
-  for (int k = 0; k < kPlanChunks; ++k) {
-    excl_r[k] = 0;
-    tot_r[k] = 0;
-    const int b = k * 64 + l;
-    if (k * 64 < a.B) {
-      const int n = b < a.B ? blocks_of(a, b, bad) : 0;
-      const int incl = wave_incl_scan(n);
-      excl_r[k] = carry + incl - n;
-      if (wave == 0 && b < a.B) a.cum[b] = excl_r[k];
-      tot_r[k] = __shfl(incl, 63, 64);
-      carry += tot_r[k];
+    for (int i = 0; i < 8; ++i) {
+      const int excl = carry + base + (i ? incl[i - 1] : 0);
+      if (s0 + i < a.B) {
+        if (s0 + i < kLdsSeqs) pre[s0 + i] = excl;
+        if (wave == 0) a.cum[s0 + i] = excl;
+      }
     }
+    carry += tot;
   }
-  for (int b0 = kPlanChunks * 64; b0 < a.B; b0 += 64) {
-    const int b = b0 + l;
-    const int n = b < a.B ? blocks_of(a, b, bad) : 0;
-    const int incl = wave_incl_scan(n);
-    if (wave == 0 && b < a.B) a.cum[b] = carry + incl - n;
-    carry += __shfl(incl, 63, 64);
-  }
-  if (wave == 0 && __any(bad) && l == 0) atomicOr(a.hdr + kHdrStatus, kStatusLenClamped);
+  if (wave == 0 && __any(bad) && lane_id() == 0) atomicOr(a.hdr + kHdrStatus, kStatusLenClamped);
   p.total = (int64_t)uni(carry) * a.Hkv;
-  share = (p.total + a.waves - 1) / a.waves;
-  if (share < a.min_share) share = a.min_share;
-  if (wave == 0 && l == 0) a.share[0] = (int32_t)share;
-  pos = (int64_t)wave * share;
-  end = pos + share < p.total ? pos + share : p.total;
-  if (pos >= end) return false;
-  int c = 0;
+  int64_t q = (p.total + a.waves - 1) / a.waves;
+  if (a.chunks_max > a.waves && q > a.chunk_min) {
+    q = (p.total + a.chunks_max - 1) / a.chunks_max;
+    if (q < a.chunk_min) q = a.chunk_min;
+  }
+  if (q < a.min_share) q = a.min_share;
+  p.chunk = q;
+  p.nchunks = (p.total + q - 1) / q;
+  if (wave == 0 && lane_id() == 0) a.share[0] = (int32_t)q;
+  // the prefix copy is private to this wave: order its LDS writes before its reads
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The sequence b at which a scan for block-head pos starts (the last one whose
+// first block-head is <= pos; empty sequences after it are skipped by the
+// caller) and cum_b, the blocks of the sequences before it.
+__device__ void locate(const DecodeArgs& a, const int32_t* pre, int64_t pos, int& b, int& cum_b) {
+  const int l = lane_id();
+  if (a.B <= kLdsSeqs) {
+    // first the 64-sequence tile (its first entry), then the sequence in it
+    const int nt = (a.B + 63) >> 6;
+    const int head = l < nt ? pre[64 * l] : 0;
+    uint64_t m = __ballot(l < nt && (int64_t)head * a.Hkv <= pos);
+    const int t = __popcll(m) - 1;  // >= 0: pre[0] = 0 <= pos
+    const int s = 64 * t + l;
+    const int v = s < a.B ? pre[s] : 0;
+    m = __ballot(s < a.B && (int64_t)v * a.Hkv <= pos);
+    const int i = __popcll(m) - 1;
+    b = uni(64 * t + i);
+    cum_b = uni(__shfl(v, i, 64));
+    return;
+  }
+  int carry = 0, unused = 0;
+  for (int t0 = 0; t0 < a.B; t0 += kTileSeqs) {
+    int incl[8], base;
+    const int tot = load_tile(a, t0, incl, base, unused);
+    if ((int64_t)(carry + tot) * a.Hkv > pos || t0 + kTileSeqs >= a.B) {
+      const int s0 = t0 + 8 * l;
+      const uint64_t m = __ballot(s0 < a.B && (int64_t)(carry + base) * a.Hkv <= pos);
+      const int ln = __popcll(m) - 1;  // >= 0: lane 0 starts at carry <= pos
+      int bi = 0, ci = carry + base;
 #pragma unroll
-  for (int k = 0; k < kPlanChunks; ++k) {
-    if (k * 64 < a.B) {
-      if (locate_in_chunk(a, pos, k * 64, excl_r[k], tot_r[k], c, p)) return true;
-      c += tot_r[k];
+      for (int i = 1; i < 8; ++i) {
+        const int e = carry + base + incl[i - 1];
+        if (s0 + i < a.B && (int64_t)e * a.Hkv <= pos) {
+          bi = i;
+          ci = e;
+        }
+      }
+      b = uni(__shfl(s0 + bi, ln, 64));
+      cum_b = uni(__shfl(ci, ln, 64));
+      return;
     }
+    carry += tot;
   }
-  for (int b0 = kPlanChunks * 64; b0 < a.B; b0 += 64) {
-    const int b = b0 + l;
-    int unused = 0;
-    const int n = b < a.B ? blocks_of(a, b, unused) : 0;
-    const int incl = wave_incl_scan(n);
-    const int t = __shfl(incl, 63, 64);
-    if (locate_in_chunk(a, pos, b0, c + incl - n, t, c, p)) return true;
-    c += t;
-  }
-  return false;  // unreachable: pos < total
+  b = a.B;  // not reached for pos < total
+  cum_b = carry;
 }
 
 // A segment's block ids, staged through a per-wave LDS chunk. Tile addresses
@@ -831,36 +868,48 @@ __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo
 template <Variant V, KvType KV, int D, int GV>
 __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   __shared__ int32_t id_lds_all[kWavesPerGroupMax][kIdChunk];
+  __shared__ int32_t pre_all[kWavesPerGroupMax][kLdsSeqs];
   const int wave_in_group = threadIdx.x >> 6;
   int32_t* id_lds = id_lds_all[wave_in_group];
+  int32_t* pre = pre_all[wave_in_group];
   const int wave = blockIdx.x * (blockDim.x >> 6) + wave_in_group;
-  WavePlan plan;
-  int64_t pos, end, share;
-  if (!plan_wave(a, wave, plan, pos, end, share)) return;
-  int b = plan.b, cum_b = plan.cum_b;
+  StreamPlan plan;
+  plan_stream(a, wave, pre, plan);
+  const bool dynamic = plan.nchunks > a.waves;
   int status = 0;
-  while (pos < end && b < a.B) {
-    const int L = clamp_len(a, a.seq_lens[b]);
-    const int nb = (L + kBlockSize - 1) / kBlockSize;
-    const int64_t base = (int64_t)cum_b * a.Hkv;
-    if (pos >= base + (int64_t)nb * a.Hkv) {
-      cum_b += nb;
-      ++b;
-      continue;
+  for (int64_t c = wave; c < plan.nchunks;) {
+    // the next chunk is claimed as this one starts, so the claim's round trip
+    // overlaps the chunk's loads
+    int ticket = 0;
+    if (dynamic && lane_id() == 0) ticket = atomicAdd(a.hdr + kHdrNext, 1);
+    int64_t pos = c * plan.chunk;
+    const int64_t end = pos + plan.chunk < plan.total ? pos + plan.chunk : plan.total;
+    int b, cum_b;
+    locate(a, pre, pos, b, cum_b);
+    while (pos < end && b < a.B) {
+      const int L = clamp_len(a, a.seq_lens[b]);
+      const int nb = (L + kBlockSize - 1) / kBlockSize;
+      const int64_t base = (int64_t)cum_b * a.Hkv;
+      if (pos >= base + (int64_t)nb * a.Hkv) {
+        cum_b += nb;
+        ++b;
+        continue;
+      }
+      const int64_t rel = pos - base;
+      const int kvh = (int)(rel / nb);
+      const int j_lo = (int)(rel - (int64_t)kvh * nb);
+      const int64_t room = end - pos;
+      const int j_hi = (int64_t)(nb - j_lo) <= room ? nb : j_lo + (int)room;
+      const bool final = j_lo == 0 && j_hi == nb;
+      const int64_t slot = (int64_t)b * a.Hkv + kvh + c;
+      if constexpr (V == Variant::Mfma) {
+        mfma_segment<KV, D>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
+      } else {
+        vec_segment<KV, D, GV>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
+      }
+      pos += j_hi - j_lo;
     }
-    const int64_t rel = pos - base;
-    const int kvh = (int)(rel / nb);
-    const int j_lo = (int)(rel - (int64_t)kvh * nb);
-    const int64_t room = end - pos;
-    const int j_hi = (int64_t)(nb - j_lo) <= room ? nb : j_lo + (int)room;
-    const bool final = j_lo == 0 && j_hi == nb;
-    const int64_t slot = (int64_t)b * a.Hkv + kvh + wave;
-    if constexpr (V == Variant::Mfma) {
-      mfma_segment<KV, D>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
-    } else {
-      vec_segment<KV, D, GV>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
-    }
-    pos += j_hi - j_lo;
+    c = dynamic ? (int64_t)a.waves + uni(ticket) : plan.nchunks;
   }
   if (__any(status) && lane_id() == 0) atomicOr(a.hdr + kHdrStatus, status);
 }
@@ -921,6 +970,8 @@ constexpr int kCombineChunk = 8;  // segments whose loads are in flight together
 // in with a running maximum.
 template <bool OUT_BF16, int D>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) {
+  // the decode kernel has finished with the chunk counter: rearm it for the next call
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.hdr[kHdrNext] = 0;
   const int u = blockIdx.x;
   const int b = u / a.Hkv;
   const int kvh = u - b * a.Hkv;

@@ -50,7 +50,8 @@ int main(void) {
   printf("pda_problem %zu\npda_options %zu\npda_plan_info %zu\n",
          sizeof(pda_problem), sizeof(pda_options), sizeof(pda_plan_info));
   F(pda_problem, num_blocks); F(pda_problem, max_seq_len); F(pda_problem, out_dtype);
-  F(pda_options, min_blocks_per_wave); F(pda_plan_info, workspace_bytes);
+  F(pda_options, min_blocks_per_wave); F(pda_options, chunks_per_wave); F(pda_options, min_blocks_per_chunk);
+  F(pda_plan_info, chunks_max); F(pda_plan_info, workspace_bytes);
   return 0;
 }
 """)
@@ -69,6 +70,9 @@ int main(void) {
     assert int(got["pda_problem.out_dtype"]) == L.Problem.out_dtype.offset
     assert int(got["pda_options.min_blocks_per_wave"]) == L.Options.min_blocks_per_wave.offset
     assert int(got["pda_plan_info.workspace_bytes"]) == L.PlanInfo.workspace_bytes.offset
+    assert int(got["pda_options.chunks_per_wave"]) == L.Options.chunks_per_wave.offset
+    assert int(got["pda_options.min_blocks_per_chunk"]) == L.Options.min_blocks_per_chunk.offset
+    assert int(got["pda_plan_info.chunks_max"]) == L.PlanInfo.chunks_max.offset
 
 
 BAD = [
@@ -112,6 +116,9 @@ def test_bad_scale_and_options_rejected():
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(5, 0, 0)) == L.EINVAL
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(0, -1, 0)) == L.EINVAL
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(0, 0, -3)) == L.EINVAL
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(0, 0, 0, -1)) == L.EINVAL
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(0, 0, 0, 65)) == L.EINVAL
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(), L.Options(0, 0, 0, 0, -2)) == L.EINVAL
     # vector kernel: at most 8 query heads per KV head
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(num_q_heads=32, num_kv_heads=2),
                       L.Options(L.VARIANT_VECTOR, 0, 0)) == L.EUNSUPPORTED
@@ -143,12 +150,18 @@ def test_query_plan_variants_and_workspace():
     assert L.query_plan(prob(q_dtype=L.F32, kv_dtype=L.F32, num_q_heads=4, num_kv_heads=4)).variant == L.VARIANT_VECTOR
     info = L.query_plan(prob(num_seqs=64, num_q_heads=28, num_kv_heads=4), num_compute_units=256)
     assert info.group_size == 7 and info.waves == 256 * 8
-    slots = 64 * 4 + info.waves
+    # default split: static, one chunk per wave; one partial slot per (unit, chunk) boundary
+    assert info.chunks_max == info.waves
+    slots = 64 * 4 + info.chunks_max
     # header + cum + (m, l) + acc, each rounded up to 256 bytes
     up = lambda x: (x + 255) // 256 * 256
     assert info.workspace_bytes == up(64) + up(64 * 4) + 2 * up(slots * 7 * 4) + up(slots * 7 * 128 * 4)
     info = L.query_plan(prob(), L.make_options("vector", waves_per_cu=3), num_compute_units=10)
-    assert info.waves == 30 and info.variant == L.VARIANT_VECTOR
+    assert info.waves == 30 and info.variant == L.VARIANT_VECTOR and info.chunks_max == 30
+    info = L.query_plan(prob(), L.make_options(waves_per_cu=3, chunks_per_wave=8), num_compute_units=10)
+    assert info.chunks_max == 240  # dynamic split: up to 8 chunks per wave
+    with pytest.raises(L.PdaError):
+        L.query_plan(prob(), L.make_options(chunks_per_wave=64), num_compute_units=1 << 24)
 
 
 def test_one_hip_runtime_in_process():

@@ -71,7 +71,8 @@ def test_edge_lengths(lib, kv, G, D):
     ref = U.oracle_for(inp)
     vs = variants_for(w)
     for v in vs:
-        for split in ({}, {"min_blocks_per_wave": 1, "waves_per_cu": 32}, {"min_blocks_per_wave": 1 << 20}):
+        for split in ({}, {"min_blocks_per_wave": 1, "waves_per_cu": 32}, {"min_blocks_per_wave": 1 << 20},
+                      {"chunks_per_wave": 1, "min_blocks_per_wave": 1}):
             print(f"[parity] edge kv={kv} G={G} D={D} variant={v} split={split}", flush=True)
             got = U.out_to_f64(run(lib, inp, variant=v, **split))
             U.assert_close(got, ref, kv, f"edge {kv} G={G} D={D} {v} {split}")
@@ -96,6 +97,41 @@ def test_peaked_softmax(lib, name):
         U.assert_close(U.out_to_f64(out32), ref, w.kv_dtype, f"peaked {name}/{v} f32 out")
         U.assert_close(U.out_to_f64(run(lib, inp, variant=v)), ref, w.kv_dtype, f"peaked {name}/{v}",
                        bf16_out_rounding=w.q_dtype == "bf16")
+
+
+# Dynamic split: waves_per_cu = 1 (256 waves) and chunks of 1-3 block-heads, so
+# there are several chunks per wave, handed out by the counter, and long
+# sequences are cut into hundreds of partials that the combine merges.
+# Batches above 512 sequences take the planner's multi-tile path (chunk starts
+# found by re-reading seq_lens instead of the LDS copy).
+SPLITS = {
+    "auto": {},
+    "static": {"chunks_per_wave": 1, "min_blocks_per_wave": 1, "waves_per_cu": 1},
+    "dynamic": {"chunks_per_wave": 16, "min_blocks_per_chunk": 1, "min_blocks_per_wave": 1, "waves_per_cu": 1},
+    "dynamic3": {"chunks_per_wave": 4, "min_blocks_per_chunk": 3, "min_blocks_per_wave": 1, "waves_per_cu": 2},
+}
+
+
+@pytest.mark.parametrize("B", [300, 700, 1100])
+@pytest.mark.parametrize("kv,G", [("bf16", 4), ("fp8_e4m3", 8), ("bf16", 2)])
+def test_dynamic_split_and_large_batches(lib, B, kv, G):
+    rng = np.random.default_rng(B + G)
+    lens = np.minimum(np.round(rng.lognormal(np.log(120), 1.0, B)), 4000).astype(int)
+    lens[rng.choice(B, B // 20, replace=False)] = 0          # a few empty sequences
+    lens[rng.choice(B, 2, replace=False)] = [2500, 3999]   # and two long ones
+    w = W.Workload(f"dyn_{kv}_{G}_{B}", B, 2 * G, 2, 64, "bf16", kv, ("uniform", 1, 1), cfg_id=70 + G)
+    inp = W.generate(w, DEV, seq_lens=lens.tolist())
+    ref = U.oracle_for(inp)
+    for v in variants_for(w):
+        for name, split in SPLITS.items():
+            print(f"[parity] dynamic B={B} kv={kv} G={G} variant={v} split={name}", flush=True)
+            got = run(lib, inp, variant=v, **split)
+            U.assert_close(U.out_to_f64(got), ref, kv, f"B={B} {kv} G={G} {v} {name}")
+            if name.startswith("dynamic"):
+                again = run(lib, inp, variant=v, **split)
+                assert torch.equal(got.view(torch.int16), again.view(torch.int16)), \
+                    "a dynamic split must not change the result"
+    assert lib.read_device_status() == 0
 
 
 def test_deterministic_and_stream(lib):
