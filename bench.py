@@ -32,16 +32,24 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2605_20863_amd", "csrc", "pda_kernels.hip")
 
 
-def algorithmic_bytes(workload, seq_lens):
+def algorithmic_bytes(workload, seq_lens, shared=None):
     """Bytes one step must move at least: each token's K and V once, plus
-    fp8 scales, q, out, block-table entries and lengths."""
+    fp8 scales, q, out, block-table entries and lengths. With ``shared`` =
+    (group_size, shared_blocks) the blocks a group's members share count once
+    (the unique bytes of a GRPO step); the token count stays the logical one."""
     e_kv = {"f32": 4, "bf16": 2, "fp8_e4m3": 1}[workload.kv_dtype]
     e_q = 4 if workload.q_dtype == "f32" else 2
     tokens = int(seq_lens.sum())
     blocks = int(((seq_lens.astype("int64") + 15) // 16).sum())
     B, hq, hkv, d = len(seq_lens), workload.num_q_heads, workload.num_kv_heads, workload.head_dim
-    kv = tokens * hkv * 2 * d * e_kv
-    scales = blocks * hkv * 2 * 4 if workload.kv_dtype == "fp8_e4m3" else 0
+    kv_tokens, kv_blocks = tokens, blocks
+    if shared is not None:
+        gs, sb = shared
+        dup = int((gs - 1) * sb.astype("int64").sum())   # shared blocks beyond one copy per group
+        kv_tokens -= 16 * dup
+        kv_blocks -= dup
+    kv = kv_tokens * hkv * 2 * d * e_kv
+    scales = kv_blocks * hkv * 2 * 4 if workload.kv_dtype == "fp8_e4m3" else 0
     return kv + scales + 2 * B * hq * d * e_q + 4 * blocks + 4 * B, tokens
 
 
@@ -171,6 +179,9 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--shared-prefix", action="store_true",
+                    help="GRPO workloads: read each group's shared prompt blocks once for several members "
+                         "(pda_paged_decode_attention_shared_prefix); bytes count the shared blocks once")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -202,7 +213,13 @@ def main():
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     inp = W.generate(w, dev)
     lens = inp.layout.seq_lens
-    nbytes, tokens = algorithmic_bytes(w, lens)
+    gp = W.group_prefix(w, inp.layout)
+    if args.shared_prefix and gp is None:
+        print(f"--shared-prefix needs a GRPO workload (groups sharing prompt blocks); {w.name} has none",
+              file=sys.stderr)
+        sys.exit(2)
+    shared = gp if args.shared_prefix else None
+    nbytes, tokens = algorithmic_bytes(w, lens, shared)
     kv_bytes = inp.k_cache.numel() * inp.k_cache.element_size() * 2
     # rotate over >= 4 GB of cache copies (16x the last-level cache) between steps
     ncopies = max(1, min(16, math.ceil(16 * LLC_BYTES / kv_bytes)))
@@ -221,9 +238,16 @@ def main():
     sh = stream.cuda_stream
     qp, bp, lp, op = inp.q.data_ptr(), inp.block_table.data_ptr(), inp.seq_lens.data_ptr(), out.data_ptr()
 
+    if shared is not None:
+        sb_dev = torch.as_tensor(shared[1], device=dev)
+
     def step(i):
         kp, vp, sp = ptrs[i % ncopies]
-        rc = _lib.raw_call(qp, kp, vp, bp, lp, sp, op, inp.softmax_scale, prob, opts, sh)
+        if shared is not None:
+            rc = _lib.raw_call_shared_prefix(qp, kp, vp, bp, lp, sp, op, inp.softmax_scale, shared[0],
+                                             sb_dev.data_ptr(), prob, opts, sh)
+        else:
+            rc = _lib.raw_call(qp, kp, vp, bp, lp, sp, op, inp.softmax_scale, prob, opts, sh)
         if rc != 0:
             raise RuntimeError(f"pda error {rc}: {_lib.last_error()}")
 
@@ -255,7 +279,7 @@ def main():
 
     achieved = nbytes / (call_ms * 1e-3) / 1e9
     value = nbytes / (ms_per_step * 1e-3) / 1e9
-    traffic = measured_traffic(w.name, nbytes)
+    traffic = measured_traffic(w.name + ("_shared" if shared is not None else ""), nbytes)
     dtype = {"f32": "f32", "bf16": "bf16", "fp8_e4m3": "fp8e4m3-kv/bf16-q"}[w.kv_dtype]
     res = {
         "metric": "paged decode attention achieved HBM GB/s (% of peak) + KV tokens/s read",
@@ -284,10 +308,12 @@ def main():
             "max_seq_len": int(lens.max()),
             "variant": args.variant,
             "cache_copies": ncopies,
+            "shared_prefix": shared is not None,
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "decode step (stream-K decode + LSE combine, one call)",
+            "kernel": ("decode step (prefix check + stream-K decode + LSE combine, one call)" if shared is not None
+                       else "decode step (stream-K decode + LSE combine, one call)"),
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

@@ -157,9 +157,57 @@ int pda_query_plan(const pda_problem* problem,
                    int32_t num_compute_units,
                    pda_plan_info* info);
 
+/*
+ * The same decode step for batches of equal-size groups whose members share
+ * leading KV blocks: GRPO-style rollouts, where every prompt is sampled
+ * group_size times and the samples' block tables start with the prompt's
+ * blocks. Sequences g*group_size .. g*group_size + group_size - 1 form group g,
+ * and shared_blocks[g] (device, [num_seqs / group_size] int32) bounds how many
+ * leading 16-token blocks its members share. The result is the same attention
+ * pda_paged_decode_attention computes; only the work differs: each shared
+ * block is read once for up to 16 query heads of several members (ceil(
+ * group_size * G / 16) reads instead of group_size). GRPO, one of the RLVR
+ * objectives of the paper's Sec. 2.3 and the setup of its Sec. 6.3
+ * simulation, samples a group of responses for every prompt, so a rollout
+ * batch is made of such groups.
+ *
+ * The library verifies the bound on the device: a group shares at most
+ * shared_blocks[g] blocks, at most every member's full blocks, and only as
+ * long as every member's block-table row holds the same block ids; a bound that
+ * ids contradict sets status bit 4 (see pda_read_device_status). A wrong bound
+ * therefore costs speed, never correctness.
+ *
+ * Errors as for pda_paged_decode_attention, and PDA_EINVAL if group_size < 1,
+ * num_seqs is not a multiple of group_size or shared_blocks is NULL;
+ * PDA_EUNSUPPORTED for an f32 KV cache or options.variant = VECTOR (the
+ * shared-prefix path runs on the MFMA kernel).
+ */
+int pda_paged_decode_attention_shared_prefix(const void* q,
+                                             const void* k_cache,
+                                             const void* v_cache,
+                                             const int32_t* block_table,
+                                             const int32_t* seq_lens,
+                                             const float* kv_scales,
+                                             void* out,
+                                             float softmax_scale,
+                                             int32_t group_size,
+                                             const int32_t* shared_blocks,
+                                             const pda_problem* problem,
+                                             const pda_options* options,
+                                             hipStream_t stream);
+
+/* pda_query_plan for pda_paged_decode_attention_shared_prefix with this group_size. */
+int pda_query_plan_shared_prefix(const pda_problem* problem,
+                                 const pda_options* options,
+                                 float softmax_scale,
+                                 int32_t group_size,
+                                 int32_t num_compute_units,
+                                 pda_plan_info* info);
+
 /* Wait for `stream`, then return (and clear) the device-side status bits that
  * calls on it recorded: 1 = a sequence length was clamped, 2 = a block-table
- * entry outside [0, num_blocks) was skipped. 0 when clean; negative on error. */
+ * entry outside [0, num_blocks) was skipped, 4 = a group's members share fewer
+ * leading blocks than shared_blocks declared. 0 when clean; negative on error. */
 int pda_read_device_status(hipStream_t stream);
 
 /* Free every workspace the library holds (waits for the owning streams). */

@@ -86,6 +86,13 @@ _lib.pda_paged_decode_attention.restype = ctypes.c_int
 _lib.pda_query_plan.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Options), ctypes.c_float,
                                 ctypes.c_int32, ctypes.POINTER(PlanInfo)]
 _lib.pda_query_plan.restype = ctypes.c_int
+_lib.pda_paged_decode_attention_shared_prefix.argtypes = [
+    _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_float, ctypes.c_int32, _vp,
+    ctypes.POINTER(Problem), ctypes.POINTER(Options), _vp]
+_lib.pda_paged_decode_attention_shared_prefix.restype = ctypes.c_int
+_lib.pda_query_plan_shared_prefix.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Options), ctypes.c_float,
+                                              ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(PlanInfo)]
+_lib.pda_query_plan_shared_prefix.restype = ctypes.c_int
 _lib.pda_read_device_status.argtypes = [_vp]
 _lib.pda_read_device_status.restype = ctypes.c_int
 _lib.pda_release_workspaces.argtypes = []
@@ -135,6 +142,26 @@ def raw_call(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax
     return _lib.pda_paged_decode_attention(
         q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, ctypes.c_float(softmax_scale),
         ctypes.byref(problem), ctypes.byref(options) if options is not None else None, stream)
+
+
+def raw_call_shared_prefix(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale,
+                           group_size, shared_blocks, problem: Problem, options: Options | None = None,
+                           stream=None) -> int:
+    """pda_paged_decode_attention_shared_prefix with integer pointers; returns the status code."""
+    return _lib.pda_paged_decode_attention_shared_prefix(
+        q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, ctypes.c_float(softmax_scale),
+        int(group_size), shared_blocks, ctypes.byref(problem),
+        ctypes.byref(options) if options is not None else None, stream)
+
+
+def query_plan_shared_prefix(problem: Problem, group_size: int, options: Options | None = None,
+                             softmax_scale: float = 1.0, num_compute_units: int = 256) -> PlanInfo:
+    info = PlanInfo()
+    _check(_lib.pda_query_plan_shared_prefix(ctypes.byref(problem),
+                                             ctypes.byref(options) if options is not None else None,
+                                             ctypes.c_float(softmax_scale), int(group_size),
+                                             int(num_compute_units), ctypes.byref(info)))
+    return info
 
 
 def query_plan(problem: Problem, options: Options | None = None, softmax_scale: float = 1.0,
@@ -207,6 +234,43 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, seq_lens, kv_scales
     kv_scales [2, NB, Hkv] fp32). ``out`` has q's shape and q's dtype or float32.
     """
     torch = _torch()
+    prob, opts = _prepare(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, max_seq_len,
+                          variant, waves_per_cu, min_blocks_per_wave, chunks_per_wave, min_blocks_per_chunk)
+    with torch.cuda.device(q.device):
+        rc = raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
+                      seq_lens.data_ptr(), kv_scales.data_ptr() if kv_scales is not None else None,
+                      out.data_ptr(), float(softmax_scale), prob, opts, _stream_handle(stream, q.device))
+    _check(rc)
+    return out
+
+
+def paged_decode_attention_shared_prefix(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out,
+                                         softmax_scale, group_size, shared_blocks, max_seq_len=0, stream=None,
+                                         variant="auto", waves_per_cu=0, min_blocks_per_wave=0,
+                                         chunks_per_wave=0, min_blocks_per_chunk=0):
+    """The same step for groups of ``group_size`` consecutive sequences whose
+    block tables share leading blocks; ``shared_blocks`` is an int32 device
+    tensor [num_seqs / group_size] bounding each group's shared blocks (the
+    library checks the bound against the block tables)."""
+    torch = _torch()
+    prob, opts = _prepare(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, max_seq_len,
+                          variant, waves_per_cu, min_blocks_per_wave, chunks_per_wave, min_blocks_per_chunk)
+    if shared_blocks.device != q.device or not shared_blocks.is_contiguous() or shared_blocks.dtype != torch.int32:
+        raise ValueError(f"shared_blocks must be a contiguous int32 tensor on {q.device}")
+    if group_size < 1 or q.shape[0] % group_size or shared_blocks.numel() != q.shape[0] // group_size:
+        raise ValueError("shared_blocks must have num_seqs / group_size entries")
+    with torch.cuda.device(q.device):
+        rc = raw_call_shared_prefix(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
+                                    seq_lens.data_ptr(), kv_scales.data_ptr() if kv_scales is not None else None,
+                                    out.data_ptr(), float(softmax_scale), group_size, shared_blocks.data_ptr(),
+                                    prob, opts, _stream_handle(stream, q.device))
+    _check(rc)
+    return out
+
+
+def _prepare(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, max_seq_len, variant, waves_per_cu,
+             min_blocks_per_wave, chunks_per_wave, min_blocks_per_chunk):
+    torch = _torch()
     tensors = {"q": q, "k_cache": k_cache, "v_cache": v_cache, "block_table": block_table,
                "seq_lens": seq_lens, "out": out}
     if kv_scales is not None:
@@ -227,12 +291,7 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, seq_lens, kv_scales
     if kv_scales is not None and tuple(kv_scales.shape) != (2, prob.num_blocks, prob.num_kv_heads):
         raise ValueError("kv_scales must be [2, num_blocks, num_kv_heads]")
     opts = make_options(variant, waves_per_cu, min_blocks_per_wave, chunks_per_wave, min_blocks_per_chunk)
-    with torch.cuda.device(dev):
-        rc = raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
-                      seq_lens.data_ptr(), kv_scales.data_ptr() if kv_scales is not None else None,
-                      out.data_ptr(), float(softmax_scale), prob, opts, _stream_handle(stream, dev))
-    _check(rc)
-    return out
+    return prob, opts
 
 
 def read_device_status(stream=None, device=None) -> int:

@@ -48,6 +48,7 @@ constexpr int64_t kAlign = 256;
 int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Plan {
+  int requested;  // the pda_variant the options asked for
   pda::Variant variant;
   pda::KvType kv;
   int G;
@@ -122,6 +123,7 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
   if (op && op->min_blocks_per_chunk < 0)
     return fail(PDA_EINVAL, "options.min_blocks_per_chunk = %d < 0", op->min_blocks_per_chunk);
 
+  plan->requested = op ? op->variant : PDA_VARIANT_AUTO;
   plan->variant = variant == PDA_VARIANT_MFMA ? pda::Variant::Mfma : pda::Variant::Vector;
   plan->kv = kd == PDA_DTYPE_F32 ? pda::KvType::F32 : (kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8);
   plan->G = G;
@@ -136,19 +138,57 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
   return PDA_OK;
 }
 
-struct Layout {
-  int64_t hdr, cum, m, l, acc, total;
+// Shared-prefix mode: groups of group_size consecutive sequences; each
+// group's shared blocks become nsub work entries of M members (M * G <= 16
+// query columns), ahead of one entry per sequence for the rest of it.
+struct Groups {
+  bool on = false;
+  int group_size = 1, M = 1, nsub = 0, num_groups = 0;
+  int64_t n_prefix = 0;
+  const int32_t* shared_blocks = nullptr;
 };
 
-Layout workspace_layout(const pda_problem* pr, int G, int chunks_max) {
+int validate_groups(const pda_problem* pr, int32_t group_size, const int32_t* shared_blocks, Plan* plan,
+                    Groups* gr) {
+  if (group_size < 1) return fail(PDA_EINVAL, "group_size = %d < 1", group_size);
+  if (pr->num_seqs % group_size)
+    return fail(PDA_EINVAL, "num_seqs = %d is not a multiple of group_size = %d", pr->num_seqs, group_size);
+  if (plan->kv == pda::KvType::F32)
+    return fail(PDA_EUNSUPPORTED, "shared-prefix decode runs on the MFMA kernel: it needs a bf16 or fp8 KV cache");
+  if (plan->requested == PDA_VARIANT_VECTOR)
+    return fail(PDA_EUNSUPPORTED, "shared-prefix decode runs on the MFMA kernel, not the vector kernel");
+  if (pr->num_seqs > 0 && !shared_blocks) return fail(PDA_EINVAL, "shared_blocks is NULL");
+  plan->variant = pda::Variant::Mfma;
+  gr->on = true;
+  gr->group_size = group_size;
+  const int per = pda::kMaxGroup / plan->G;
+  gr->M = group_size < per ? group_size : (per > 0 ? per : 1);
+  gr->nsub = (group_size + gr->M - 1) / gr->M;
+  gr->num_groups = pr->num_seqs / group_size;
+  gr->n_prefix = (int64_t)gr->num_groups * gr->nsub;
+  gr->shared_blocks = shared_blocks;
+  if ((gr->n_prefix + pr->num_seqs) * pr->max_blocks_per_seq * pr->num_kv_heads > INT32_MAX)
+    return fail(PDA_EINVAL, "(entries) * max_blocks_per_seq * num_kv_heads overflows int32");
+  return PDA_OK;
+}
+
+struct Layout {
+  int64_t hdr, sg, cum, m, l, acc, total;
+};
+
+// header | sg[num_groups] | cum[entries] | m, l [slots, Gp] | acc [slots, Gp, D]
+Layout workspace_layout(const pda_problem* pr, const Plan& plan, const Groups& gr, int chunks_max) {
   Layout w;
-  const int64_t slots = pda::partial_slots(pr->num_seqs, pr->num_kv_heads, chunks_max);
+  const int64_t entries = gr.n_prefix + pr->num_seqs;
+  const int64_t gp = gr.on ? (int64_t)gr.M * plan.G : plan.G;
+  const int64_t slots = pda::partial_slots(entries, pr->num_kv_heads, chunks_max);
   w.hdr = 0;
-  w.cum = align_up(pda::kHdrWords * 4);
-  w.m = w.cum + align_up((int64_t)pr->num_seqs * 4);
-  w.l = w.m + align_up(slots * G * 4);
-  w.acc = w.l + align_up(slots * G * 4);
-  w.total = w.acc + align_up(slots * G * pr->head_dim * 4);
+  w.sg = align_up(pda::kHdrWords * 4);
+  w.cum = w.sg + align_up((int64_t)gr.num_groups * 4);
+  w.m = w.cum + align_up(entries * 4);
+  w.l = w.m + align_up(slots * gp * 4);
+  w.acc = w.l + align_up(slots * gp * 4);
+  w.total = w.acc + align_up(slots * gp * pr->head_dim * 4);
   return w;
 }
 
@@ -250,14 +290,21 @@ int pda_version(void) { return PDA_VERSION; }
 
 const char* pda_last_error(void) { return g_error.c_str(); }
 
-int pda_query_plan(const pda_problem* problem, const pda_options* options, float softmax_scale,
-                   int32_t num_compute_units, pda_plan_info* info) {
+}  // extern "C"
+
+namespace {
+
+int query_plan(const pda_problem* problem, const pda_options* options, float softmax_scale,
+               int32_t num_compute_units, const int32_t* group_size, pda_plan_info* info) {
   g_error.clear();
   if (!info) return fail(PDA_EINVAL, "info is NULL");
   if (num_compute_units < 1) return fail(PDA_EINVAL, "num_compute_units = %d < 1", num_compute_units);
   Plan plan;
   int rc = validate(problem, options, softmax_scale, &plan);
   if (rc != PDA_OK) return rc;
+  Groups gr;
+  static const int32_t kAny = 0;  // shared_blocks is not read by a plan query
+  if (group_size && (rc = validate_groups(problem, *group_size, &kAny, &plan, &gr)) != PDA_OK) return rc;
   const int wpc = plan.waves_per_cu > 0 ? plan.waves_per_cu : kDefaultWavesPerCu;
   if ((int64_t)num_compute_units * wpc * plan.chunks_per_wave > INT32_MAX)
     return fail(PDA_EINVAL, "num_compute_units = %d is too large", num_compute_units);
@@ -265,18 +312,20 @@ int pda_query_plan(const pda_problem* problem, const pda_options* options, float
   info->waves = num_compute_units * wpc;
   info->group_size = plan.G;
   info->chunks_max = info->waves * plan.chunks_per_wave;
-  info->workspace_bytes = workspace_layout(problem, plan.G, info->chunks_max).total;
+  info->workspace_bytes = workspace_layout(problem, plan, gr, info->chunks_max).total;
   return PDA_OK;
 }
 
-int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v_cache,
-                               const int32_t* block_table, const int32_t* seq_lens, const float* kv_scales,
-                               void* out, float softmax_scale, const pda_problem* problem,
-                               const pda_options* options, hipStream_t stream) {
+int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
+        const int32_t* seq_lens, const float* kv_scales, void* out, float softmax_scale,
+        const int32_t* group_size, const int32_t* shared_blocks, const pda_problem* problem,
+        const pda_options* options, hipStream_t stream) {
   g_error.clear();
   Plan plan;
   int rc = validate(problem, options, softmax_scale, &plan);
   if (rc != PDA_OK) return rc;
+  Groups gr;
+  if (group_size && (rc = validate_groups(problem, *group_size, shared_blocks, &plan, &gr)) != PDA_OK) return rc;
   if (problem->num_seqs == 0) return PDA_OK;
   if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out)
     return fail(PDA_EINVAL, "a required pointer (q, k_cache, v_cache, block_table, seq_lens, out) is NULL");
@@ -297,7 +346,7 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
   }
   const int waves = di.cus * wpc;
   const int chunks_max = waves * plan.chunks_per_wave;
-  const Layout lay = workspace_layout(problem, plan.G, chunks_max);
+  const Layout lay = workspace_layout(problem, plan, gr, chunks_max);
 
   Workspace* ws = workspace_for(dev, stream);
   std::lock_guard<std::mutex> lk(ws->mu);
@@ -334,6 +383,15 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
   // fewer, larger workgroups dispatch faster than one-wave groups.
   a.waves_per_group = wpc % 4 == 0 ? 4 : (wpc % 2 == 0 ? 2 : 1);
   a.out_bf16 = problem->out_dtype == PDA_DTYPE_BF16;
+  a.E = (int32_t)(gr.n_prefix + problem->num_seqs);
+  a.shared = gr.on ? 1 : 0;
+  a.group_size = gr.group_size;
+  a.M = gr.M;
+  a.nsub = gr.nsub;
+  a.n_prefix = (int32_t)gr.n_prefix;
+  a.Gp = gr.on ? gr.M * plan.G : plan.G;
+  a.shared_blocks = gr.shared_blocks;
+  a.sg = reinterpret_cast<int32_t*>(base + lay.sg);
   a.hdr = reinterpret_cast<int32_t*>(base + lay.hdr);
   a.share = a.hdr + pda::kHdrShare;
   a.cum = reinterpret_cast<int32_t*>(base + lay.cum);
@@ -341,6 +399,8 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
   a.ws_l = reinterpret_cast<float*>(base + lay.l);
   a.ws_acc = reinterpret_cast<float*>(base + lay.acc);
 
+  if (gr.on && (e = pda::launch_prefix(a, gr.num_groups, stream)) != hipSuccess)
+    return fail_hip(e, "prefix kernel launch");
   if ((e = pda::launch_decode(a, plan.variant, plan.kv, stream)) != hipSuccess)
     return fail_hip(e, "decode kernel launch");
   if ((e = pda::launch_combine(a, stream)) != hipSuccess) {
@@ -348,6 +408,38 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
     return fail_hip(e, "combine kernel launch");
   }
   return PDA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int pda_query_plan(const pda_problem* problem, const pda_options* options, float softmax_scale,
+                   int32_t num_compute_units, pda_plan_info* info) {
+  return query_plan(problem, options, softmax_scale, num_compute_units, nullptr, info);
+}
+
+int pda_query_plan_shared_prefix(const pda_problem* problem, const pda_options* options, float softmax_scale,
+                                 int32_t group_size, int32_t num_compute_units, pda_plan_info* info) {
+  return query_plan(problem, options, softmax_scale, num_compute_units, &group_size, info);
+}
+
+int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                               const int32_t* block_table, const int32_t* seq_lens, const float* kv_scales,
+                               void* out, float softmax_scale, const pda_problem* problem,
+                               const pda_options* options, hipStream_t stream) {
+  return run(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale, nullptr, nullptr,
+             problem, options, stream);
+}
+
+int pda_paged_decode_attention_shared_prefix(const void* q, const void* k_cache, const void* v_cache,
+                                             const int32_t* block_table, const int32_t* seq_lens,
+                                             const float* kv_scales, void* out, float softmax_scale,
+                                             int32_t group_size, const int32_t* shared_blocks,
+                                             const pda_problem* problem, const pda_options* options,
+                                             hipStream_t stream) {
+  return run(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale, &group_size,
+             shared_blocks, problem, options, stream);
 }
 
 int pda_read_device_status(hipStream_t stream) {

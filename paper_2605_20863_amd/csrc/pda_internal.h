@@ -18,6 +18,7 @@ enum class Variant : int { Vector = 1, Mfma = 2 };
 // Device-side status bits (workspace header word kHdrStatus).
 constexpr int kStatusLenClamped = 1;
 constexpr int kStatusBadBlock = 2;
+constexpr int kStatusPrefixShortened = 4;  // a group's members share fewer leading blocks than declared
 
 // Workspace header words.
 constexpr int kHdrStatus = 0;
@@ -45,24 +46,39 @@ struct DecodeArgs {
   int32_t waves;        // launched persistent waves (a multiple of waves_per_group)
   int32_t waves_per_group;  // independent stream-K waves per workgroup: 1, 2 or 4
   int32_t out_bf16;     // 1: out is bf16, 0: f32
+  // Work entries. Plain mode: entry b is sequence b (E = B). Shared-prefix
+  // mode: entries [0, n_prefix) are the groups' shared leading blocks, nsub
+  // per group, each applied to the queries of up to M members (M * G query
+  // columns); entry n_prefix + m is the rest of sequence m.
+  int32_t E;
+  int32_t shared;       // 1: shared-prefix mode
+  int32_t group_size;   // members per group (sequences g * group_size ..)
+  int32_t M;            // members per prefix entry (M * G <= 16)
+  int32_t nsub;         // prefix entries per group = ceil(group_size / M)
+  int32_t n_prefix;     // num_groups * nsub
+  int32_t Gp;           // query columns per partial row: G, or M * G in shared-prefix mode
+  const int32_t* shared_blocks;  // [num_groups] caller's bound on each group's shared blocks
   // workspace
   int32_t* hdr;         // kHdrWords ints
-  int32_t* cum;         // [B] exclusive prefix sum of blocks per sequence
+  int32_t* sg;          // [num_groups] shared blocks each group really has (prefix kernel)
+  int32_t* cum;         // [E] exclusive prefix sum of blocks per entry
   int32_t* share;       // [1] block-heads per chunk (written by wave 0, read by the combine)
-  float* ws_m;          // [slots, G] running max (base 2) per partial
-  float* ws_l;          // [slots, G] softmax denominator per partial
-  float* ws_acc;        // [slots, G, D] unnormalised output per partial
+  float* ws_m;          // [slots, Gp] running max (base 2) per partial
+  float* ws_l;          // [slots, Gp] softmax denominator per partial
+  float* ws_acc;        // [slots, Gp, D] unnormalised output per partial
 };
 
 // Number of partial-result slots one call can need: one per (unit, chunk)
-// intersection, bounded by units + chunks.
-inline int64_t partial_slots(int B, int Hkv, int chunks_max) {
-  return (int64_t)B * Hkv + chunks_max;
+// intersection, bounded by units + chunks (a unit is an (entry, KV head)).
+inline int64_t partial_slots(int64_t entries, int Hkv, int chunks_max) {
+  return entries * Hkv + chunks_max;
 }
 
 // Launchers (pda_kernels.hip). Return hipSuccess or the launch error.
 hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
+// Shared-prefix mode: the groups' real shared block counts, before the decode kernel.
+hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s);
 // Max resident waves per CU for the decode kernel that (v, kv, D, G) selects.
 hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* waves_per_cu);
 

@@ -137,6 +137,58 @@ __device__ __forceinline__ int clamp_len(const DecodeArgs& a, int L) {
   return L < 0 ? 0 : (L > a.len_cap ? a.len_cap : L);
 }
 
+// One work entry: a run of blocks read through one block-table row and
+// applied to up to 16 query columns. In plain mode entry b is sequence b with
+// its G query heads. In shared-prefix mode (GRPO-style groups of equal size
+// whose members share leading blocks) entry (g, s) < n_prefix is group g's
+// shared blocks applied to the heads of members s*M .. s*M + M - 1 (column r
+// = member r / G, head r % G), and entry n_prefix + m is sequence m's blocks
+// after its group's shared ones. Results equal plain attention over each
+// sequence: the combine merges a sequence's prefix and suffix partials.
+struct Entry {
+  const int32_t* row;  // block ids, from the entry's first block on
+  int L;               // valid tokens from the entry's first block
+  int nb;              // blocks
+  int qs;              // sequence of query column 0
+  int ncols;           // query columns: G, or members * G
+  bool may_final;      // a chunk that covers the whole entry writes the output
+};
+
+__device__ __forceinline__ Entry entry_of(const DecodeArgs& a, int v) {
+  Entry e;
+  if (!a.shared) {
+    e.L = clamp_len(a, a.seq_lens[v]);
+    e.nb = (e.L + kBlockSize - 1) / kBlockSize;
+    e.row = a.block_table + (int64_t)v * a.max_blocks;
+    e.qs = v;
+    e.ncols = a.G;
+    e.may_final = true;
+  } else if (v < a.n_prefix) {
+    const int g = v / a.nsub, s = v - g * a.nsub;
+    const int S = a.sg[g];
+    const int first = g * a.group_size;
+    const int nm = a.group_size - s * a.M < a.M ? a.group_size - s * a.M : a.M;
+    e.row = a.block_table + (int64_t)first * a.max_blocks;
+    e.L = S * kBlockSize;
+    e.nb = S;
+    e.qs = first + s * a.M;
+    e.ncols = nm * a.G;
+    e.may_final = false;
+  } else {
+    const int m = v - a.n_prefix;
+    const int S = a.sg[m / a.group_size];
+    const int Lf = clamp_len(a, a.seq_lens[m]);
+    const int nb = (Lf + kBlockSize - 1) / kBlockSize - S;
+    e.row = a.block_table + (int64_t)m * a.max_blocks + S;
+    e.L = Lf - S * kBlockSize;
+    e.nb = nb > 0 ? nb : 0;
+    e.qs = m;
+    e.ncols = a.G;
+    e.may_final = S == 0;
+  }
+  return e;
+}
+
 // Stream-K plan, computed by every wave from seq_lens. The stream of
 // block-heads is cut into chunks of Q block-heads, chunk c covering
 // [c*Q, (c+1)*Q). In a static split Q = ceil(total / waves) and wave w runs
@@ -148,7 +200,7 @@ __device__ __forceinline__ int clamp_len(const DecodeArgs& a, int L) {
 // is (unit + chunk), not (unit + wave), so the values written and merged do
 // not depend on which wave ran a chunk.
 constexpr int kTileSeqs = 512;  // sequences one planning round trip covers, 8 per lane
-constexpr int kLdsSeqs = 512;   // batches up to this size keep their prefix sums in LDS
+constexpr int kLdsSeqs = 512;   // up to this many entries keep their prefix sums in LDS
 
 struct StreamPlan {
   int64_t total;    // block-heads in the step
@@ -156,21 +208,43 @@ struct StreamPlan {
   int64_t nchunks;  // ceil(total / Q)
 };
 
-// Block counts of sequences [t0, t0 + 512), lane l owning t0 + 8l .. +7 (all
+// Block counts of entries [t0, t0 + 512), lane l owning t0 + 8l .. +7 (all
 // eight lengths are loaded before any is used, so the tile costs one round
 // trip). incl[i] = inclusive prefix within the lane, base = the lane's
-// exclusive prefix within the tile; returns the tile total.
+// exclusive prefix within the tile; returns the tile total. The counts are
+// the ones entry_of gives.
 __device__ __forceinline__ int load_tile(const DecodeArgs& a, int t0, int (&incl)[8], int& base, int& bad) {
   const int s0 = t0 + 8 * lane_id();
-  int raw[8];
+  int raw[8], sh[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) raw[i] = s0 + i < a.B ? a.seq_lens[s0 + i] : 0;
+  for (int i = 0; i < 8; ++i) {
+    const int v = s0 + i;
+    raw[i] = 0;
+    sh[i] = 0;
+    if (!a.shared) {
+      if (v < a.E) raw[i] = a.seq_lens[v];
+    } else if (v < a.n_prefix) {
+      sh[i] = a.sg[v / a.nsub];
+    } else if (v < a.E) {
+      const int m = v - a.n_prefix;
+      raw[i] = a.seq_lens[m];
+      sh[i] = a.sg[m / a.group_size];
+    }
+  }
   int run = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const int L = clamp_len(a, raw[i]);
-    bad |= (L != raw[i]);
-    run += (L + kBlockSize - 1) / kBlockSize;
+    const int v = s0 + i;
+    int n;
+    if (a.shared && v < a.n_prefix) {
+      n = sh[i];
+    } else {
+      const int L = clamp_len(a, raw[i]);
+      bad |= (L != raw[i]);
+      n = (L + kBlockSize - 1) / kBlockSize - sh[i];
+      n = n > 0 ? n : 0;
+    }
+    run += n;
     incl[i] = run;
   }
   const int x = wave_incl_scan(run);
@@ -181,14 +255,14 @@ __device__ __forceinline__ int load_tile(const DecodeArgs& a, int t0, int (&incl
 // Wave 0 also publishes the prefix sums (cum) and Q (share) for the combine.
 __device__ void plan_stream(const DecodeArgs& a, int wave, int32_t* pre, StreamPlan& p) {
   int carry = 0, bad = 0;
-  for (int t0 = 0; t0 < a.B; t0 += kTileSeqs) {
+  for (int t0 = 0; t0 < a.E; t0 += kTileSeqs) {
     int incl[8], base;
     const int tot = load_tile(a, t0, incl, base, bad);
     const int s0 = t0 + 8 * lane_id();
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int excl = carry + base + (i ? incl[i - 1] : 0);
-      if (s0 + i < a.B) {
+      if (s0 + i < a.E) {
         if (s0 + i < kLdsSeqs) pre[s0 + i] = excl;
         if (wave == 0) a.cum[s0 + i] = excl;
       }
@@ -217,33 +291,33 @@ __device__ void plan_stream(const DecodeArgs& a, int wave, int32_t* pre, StreamP
 // caller) and cum_b, the blocks of the sequences before it.
 __device__ void locate(const DecodeArgs& a, const int32_t* pre, int64_t pos, int& b, int& cum_b) {
   const int l = lane_id();
-  if (a.B <= kLdsSeqs) {
+  if (a.E <= kLdsSeqs) {
     // first the 64-sequence tile (its first entry), then the sequence in it
-    const int nt = (a.B + 63) >> 6;
+    const int nt = (a.E + 63) >> 6;
     const int head = l < nt ? pre[64 * l] : 0;
     uint64_t m = __ballot(l < nt && (int64_t)head * a.Hkv <= pos);
     const int t = __popcll(m) - 1;  // >= 0: pre[0] = 0 <= pos
     const int s = 64 * t + l;
-    const int v = s < a.B ? pre[s] : 0;
-    m = __ballot(s < a.B && (int64_t)v * a.Hkv <= pos);
+    const int v = s < a.E ? pre[s] : 0;
+    m = __ballot(s < a.E && (int64_t)v * a.Hkv <= pos);
     const int i = __popcll(m) - 1;
     b = uni(64 * t + i);
     cum_b = uni(__shfl(v, i, 64));
     return;
   }
   int carry = 0, unused = 0;
-  for (int t0 = 0; t0 < a.B; t0 += kTileSeqs) {
+  for (int t0 = 0; t0 < a.E; t0 += kTileSeqs) {
     int incl[8], base;
     const int tot = load_tile(a, t0, incl, base, unused);
-    if ((int64_t)(carry + tot) * a.Hkv > pos || t0 + kTileSeqs >= a.B) {
+    if ((int64_t)(carry + tot) * a.Hkv > pos || t0 + kTileSeqs >= a.E) {
       const int s0 = t0 + 8 * l;
-      const uint64_t m = __ballot(s0 < a.B && (int64_t)(carry + base) * a.Hkv <= pos);
+      const uint64_t m = __ballot(s0 < a.E && (int64_t)(carry + base) * a.Hkv <= pos);
       const int ln = __popcll(m) - 1;  // >= 0: lane 0 starts at carry <= pos
       int bi = 0, ci = carry + base;
 #pragma unroll
       for (int i = 1; i < 8; ++i) {
         const int e = carry + base + incl[i - 1];
-        if (s0 + i < a.B && (int64_t)e * a.Hkv <= pos) {
+        if (s0 + i < a.E && (int64_t)e * a.Hkv <= pos) {
           bi = i;
           ci = e;
         }
@@ -254,7 +328,7 @@ __device__ void locate(const DecodeArgs& a, const int32_t* pre, int64_t pos, int
     }
     carry += tot;
   }
-  b = a.B;  // not reached for pos < total
+  b = a.E;  // not reached for pos < total
   cum_b = carry;
 }
 
@@ -311,6 +385,17 @@ __device__ __forceinline__ Blk block_at(const DecodeArgs& a, BlockIds& ids, int 
   r.tile = (int64_t)p * a.Hkv + kvh;
   return r;
 }
+
+// One segment: blocks [j_lo, j_hi) of an entry under KV head kvh.
+struct Seg {
+  const int32_t* row;  // the entry's block ids
+  int L;               // the entry's valid tokens
+  int j_lo, j_hi;
+  int kvh;
+  int qs, ncols;       // query columns (see Entry)
+  bool final;          // write the normalised output (ncols == G), else a partial
+  int64_t slot;
+};
 
 // ------------------------------------------------------------- MFMA wave kernel
 
@@ -515,25 +600,27 @@ __device__ __forceinline__ void mfma_step(const MfmaPair<KV, D>& bf, const bf16x
 }
 
 template <KvType KV, int D>
-__device__ void mfma_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo, int j_hi, bool final,
-                             int64_t slot, int& status, int32_t* id_lds) {
+__device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds) {
   using C = MfmaCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
+  const int kvh = sg.kvh, L = sg.L, j_lo = sg.j_lo, j_hi = sg.j_hi;
 
-  // Q^T B-operand: head r of the group, dims qdim(j, c) .. +8 for k-step j.
+  // Q^T B-operand: column r (member r / G, head r % G), dims qdim(j, c) .. +8 for k-step j.
   bf16x8 qb[C::KSTEPS];
   {
-    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.Hq + kvh * a.G + r) * D;
+    const int mem = r / a.G;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) +
+                           ((int64_t)(sg.qs + mem) * a.Hq + kvh * a.G + (r - mem * a.G)) * D;
 #pragma unroll
     for (int j = 0; j < C::KSTEPS; ++j) {
       u32x4 w = {0, 0, 0, 0};
-      if (r < a.G) w = ld<u32x4>(qrow + C::qdim(j, c));
+      if (r < sg.ncols) w = ld<u32x4>(qrow + C::qdim(j, c));
       qb[j] = __builtin_bit_cast(bf16x8, w);
     }
   }
 
-  BlockIds ids{a.block_table + (int64_t)b * a.max_blocks, j_hi, 0, id_lds};
+  BlockIds ids{sg.row, j_hi, 0, id_lds};
   ids.fill(j_lo);
 
   f32x4 acc[C::MT];
@@ -563,11 +650,10 @@ __device__ void mfma_segment(const DecodeArgs& a, int b, int kvh, int L, int j_l
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
 
-  if (r >= a.G) return;
-  const int h = kvh * a.G + r;
-  if (final) {
+  if (r >= sg.ncols) return;
+  if (sg.final) {  // ncols == G: column r is head r of sequence qs
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    const int64_t orow = ((int64_t)b * a.Hq + h) * D;
+    const int64_t orow = ((int64_t)sg.qs * a.Hq + kvh * a.G + r) * D;
     if (a.out_bf16) {
       uint16_t* o = static_cast<uint16_t*>(a.out) + orow;
 #pragma unroll
@@ -583,12 +669,13 @@ __device__ void mfma_segment(const DecodeArgs& a, int b, int kvh, int L, int j_l
       for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m] * inv;
     }
   } else {
-    float* arow = a.ws_acc + (slot * a.G + r) * D;
+    const int64_t prow = sg.slot * a.Gp + r;
+    float* arow = a.ws_acc + prow * D;
 #pragma unroll
     for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(arow + 16 * m + 4 * c) = acc[m];
     if (c == 0) {
-      a.ws_m[slot * a.G + r] = m_run;
-      a.ws_l[slot * a.G + r] = l_run;
+      a.ws_m[prow] = m_run;
+      a.ws_l[prow] = l_run;
     }
   }
 }
@@ -767,12 +854,15 @@ __device__ __forceinline__ void vec_step(const VecBlock<KV, D>& bk, const float 
     vec_compute<KV, D, GV, true>(bk, qf, scale_log2, acc, m_run, l_run);
 }
 
+// Plain mode only (the host sends shared-prefix calls to the MFMA kernel).
 template <KvType KV, int D, int GV>
-__device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo, int j_hi, bool final,
-                            int64_t slot, int& status, int32_t* id_lds) {
+__device__ void vec_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds) {
   using C = VecCfg<KV, D>;
   const int l = lane_id();
   const int r4 = l >> 4, c16 = l & 15;
+  const int b = sg.qs, kvh = sg.kvh, L = sg.L, j_lo = sg.j_lo, j_hi = sg.j_hi;
+  const bool final = sg.final;
+  const int64_t slot = sg.slot;
 
   float qf[GV][C::ED];
 #pragma unroll
@@ -792,7 +882,7 @@ __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo
     }
   }
 
-  BlockIds ids{a.block_table + (int64_t)b * a.max_blocks, j_hi, 0, id_lds};
+  BlockIds ids{sg.row, j_hi, 0, id_lds};
   ids.fill(j_lo);
 
   float acc[GV][C::ED];
@@ -852,12 +942,12 @@ __device__ void vec_segment(const DecodeArgs& a, int b, int kvh, int L, int j_lo
         }
       }
     } else {
-      float* arow = a.ws_acc + (slot * a.G + h) * D;
+      float* arow = a.ws_acc + (slot * a.Gp + h) * D;
 #pragma unroll
       for (int e = 0; e < C::ED; ++e) arow[c16 + 16 * e] = acc[h][e];
       if (c16 == 0) {
-        a.ws_m[slot * a.G + h] = m_run[h];
-        a.ws_l[slot * a.G + h] = l_run[h];
+        a.ws_m[slot * a.Gp + h] = m_run[h];
+        a.ws_l[slot * a.Gp + h] = l_run[h];
       }
     }
   }
@@ -884,15 +974,15 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     if (dynamic && lane_id() == 0) ticket = atomicAdd(a.hdr + kHdrNext, 1);
     int64_t pos = c * plan.chunk;
     const int64_t end = pos + plan.chunk < plan.total ? pos + plan.chunk : plan.total;
-    int b, cum_b;
-    locate(a, pre, pos, b, cum_b);
-    while (pos < end && b < a.B) {
-      const int L = clamp_len(a, a.seq_lens[b]);
-      const int nb = (L + kBlockSize - 1) / kBlockSize;
-      const int64_t base = (int64_t)cum_b * a.Hkv;
+    int v, cum_v;
+    locate(a, pre, pos, v, cum_v);
+    while (pos < end && v < a.E) {
+      const Entry e = entry_of(a, v);
+      const int nb = e.nb;
+      const int64_t base = (int64_t)cum_v * a.Hkv;
       if (pos >= base + (int64_t)nb * a.Hkv) {
-        cum_b += nb;
-        ++b;
+        cum_v += nb;
+        ++v;
         continue;
       }
       const int64_t rel = pos - base;
@@ -900,12 +990,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       const int j_lo = (int)(rel - (int64_t)kvh * nb);
       const int64_t room = end - pos;
       const int j_hi = (int64_t)(nb - j_lo) <= room ? nb : j_lo + (int)room;
-      const bool final = j_lo == 0 && j_hi == nb;
-      const int64_t slot = (int64_t)b * a.Hkv + kvh + c;
+      const Seg sg{e.row, e.L, j_lo, j_hi, kvh, e.qs, e.ncols, e.may_final && j_lo == 0 && j_hi == nb,
+                   (int64_t)v * a.Hkv + kvh + c};
       if constexpr (V == Variant::Mfma) {
-        mfma_segment<KV, D>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
+        mfma_segment<KV, D>(a, sg, status, id_lds);
       } else {
-        vec_segment<KV, D, GV>(a, b, kvh, L, j_lo, j_hi, final, slot, status, id_lds);
+        vec_segment<KV, D, GV>(a, sg, status, id_lds);
       }
       pos += j_hi - j_lo;
     }
@@ -960,14 +1050,18 @@ __global__ __launch_bounds__(256) void decode_kernel_vec(
 constexpr int kCombineThreads = 256;
 constexpr int kCombineChunk = 8;  // segments whose loads are in flight together
 
-// One workgroup per (sequence, KV head) unit: merges the partial softmax states
-// (m_w, l_w, acc_w) of the waves w that shared the unit,
+// One workgroup per (sequence, KV head): merges the partial softmax states
+// (m_w, l_w, acc_w) of the chunks w that computed parts of the sequence's
+// attention for that head,
 //     out = sum_w 2^(m_w - M) acc_w / sum_w 2^(m_w - M) l_w,   M = max_w m_w,
-// and writes zeros for empty sequences. The kernel is latency-bound (a few KB
-// per unit), so it is organised around round trips: one for the unit's
-// segment range, then one per chunk of segments in which every thread loads
-// the (m, l) of its heads and its accumulator elements together and folds them
-// in with a running maximum.
+// and writes zeros for empty sequences. The partials come from up to two
+// entries: the sequence's own (its suffix in shared-prefix mode) and, in
+// shared-prefix mode, its group's prefix entry, whose columns
+// col0 .. col0 + G - 1 are this sequence's heads. The kernel is latency-bound
+// (a few KB per sequence and head), so it is organised around round trips:
+// one for the entries' chunk ranges, then one per group of 8 chunks in which
+// every thread loads the (m, l) of its head and its accumulator elements
+// together and folds them in with a running maximum.
 template <bool OUT_BF16, int D>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) {
   // the decode kernel has finished with the chunk counter: rearm it for the next call
@@ -975,24 +1069,46 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   const int u = blockIdx.x;
   const int b = u / a.Hkv;
   const int kvh = u - b * a.Hkv;
-  const int L = clamp_len(a, a.seq_lens[b]);
-  const int nb = (L + kBlockSize - 1) / kBlockSize;
   const int G = a.G;
   const int tid = threadIdx.x;
   const int64_t obase = ((int64_t)b * a.Hq + (int64_t)kvh * G) * D;
-  if (nb == 0) {
+  const int64_t share = a.share[0];
+
+  int64_t slot0[2];
+  int nseg[2], col0[2];
+  int parts = 0;
+  const int v_own = a.shared ? a.n_prefix + b : b;
+  const Entry own = entry_of(a, v_own);
+  if (own.nb > 0) {
+    const int64_t start = (int64_t)a.cum[v_own] * a.Hkv + (int64_t)kvh * own.nb;
+    const int64_t w0 = start / share;
+    nseg[parts] = (int)((start + own.nb - 1) / share - w0) + 1;
+    slot0[parts] = (int64_t)v_own * a.Hkv + kvh + w0;
+    col0[parts] = 0;
+    ++parts;
+  }
+  if (a.shared) {
+    const int g = b / a.group_size, i = b - g * a.group_size;
+    const int sub = i / a.M;
+    const int v = g * a.nsub + sub;
+    const int S = a.sg[g];
+    if (S > 0) {
+      const int64_t start = (int64_t)a.cum[v] * a.Hkv + (int64_t)kvh * S;
+      const int64_t w0 = start / share;
+      nseg[parts] = (int)((start + S - 1) / share - w0) + 1;
+      slot0[parts] = (int64_t)v * a.Hkv + kvh + w0;
+      col0[parts] = (i - sub * a.M) * G;
+      ++parts;
+    }
+  }
+  if (parts == 0) {
     for (int i = tid; i < G * D; i += kCombineThreads) {
       if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = 0;
       else static_cast<float*>(a.out)[obase + i] = 0.f;
     }
     return;
   }
-  const int64_t share = a.share[0];
-  const int64_t start = (int64_t)a.cum[b] * a.Hkv + (int64_t)kvh * nb;
-  const int64_t w0 = start / share;
-  const int nseg = (int)((start + nb - 1) / share - w0) + 1;
-  if (nseg == 1) return;  // one wave covered the unit and wrote the output
-  const int64_t slot0 = (int64_t)u + w0;
+  if (parts == 1 && nseg[0] == 1 && own.may_final) return;  // one chunk wrote the output
 
   // thread t owns head h = t / 16 (if < G) and dims [ (t % 16) * D/16, +D/16 )
   constexpr int DE = D / 16;
@@ -1003,41 +1119,49 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
 #pragma unroll
   for (int e = 0; e < DE; ++e) acc[e] = 0.f;
   float M = kNegInf, den = 0.f;
-  for (int s0 = 0; s0 < nseg; s0 += kCombineChunk) {
-    const int ns = nseg - s0 < kCombineChunk ? nseg - s0 : kCombineChunk;
-    float vm[kCombineChunk], vl[kCombineChunk];
-    f32x4 va[kCombineChunk][DE / 4];
+  // the parts' segments as one list (part 0 first), so a sequence with few
+  // segments in all takes one round trip whatever entries they come from
+  const int n0 = nseg[0];
+  const int ntot = n0 + (parts > 1 ? nseg[1] : 0);
+  {
+    for (int s0 = 0; s0 < ntot; s0 += kCombineChunk) {
+      const int ns = ntot - s0 < kCombineChunk ? ntot - s0 : kCombineChunk;
+      float vm[kCombineChunk], vl[kCombineChunk];
+      f32x4 va[kCombineChunk][DE / 4];
 #pragma unroll
-    for (int q = 0; q < kCombineChunk; ++q) {
-      const bool live = q < ns;
-      const int64_t at = (slot0 + s0 + (live ? q : 0)) * G + h;
-      vm[q] = live ? a.ws_m[at] : kNegInf;
-      vl[q] = live ? a.ws_l[at] : 0.f;
-      const f32x4* row = reinterpret_cast<const f32x4*>(a.ws_acc + at * D + d0);
+      for (int q = 0; q < kCombineChunk; ++q) {
+        const bool live = q < ns;
+        const int k = s0 + (live ? q : 0);
+        const int part = k < n0 ? 0 : 1;
+        const int64_t at = (slot0[part] + (k - (part ? n0 : 0))) * a.Gp + col0[part] + h;
+        vm[q] = live ? a.ws_m[at] : kNegInf;
+        vl[q] = live ? a.ws_l[at] : 0.f;
+        const f32x4* row = reinterpret_cast<const f32x4*>(a.ws_acc + at * D + d0);
 #pragma unroll
-      for (int e = 0; e < DE / 4; ++e) va[q][e] = live ? row[e] : f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    float mc = M;
-#pragma unroll
-    for (int q = 0; q < kCombineChunk; ++q) mc = fmaxf(mc, vm[q]);
-    const float ms = mc == kNegInf ? 0.f : mc;
-    const float r = fast_exp2((M == kNegInf ? ms : M) - ms);
-    den *= r;
-#pragma unroll
-    for (int e = 0; e < DE; ++e) acc[e] *= r;
-#pragma unroll
-    for (int q = 0; q < kCombineChunk; ++q) {
-      const float w = fast_exp2(vm[q] - ms);  // 0 for padded segments (m = -inf)
-      den = fmaf(w, vl[q], den);
-#pragma unroll
-      for (int e = 0; e < DE / 4; ++e) {
-        acc[4 * e] = fmaf(w, va[q][e][0], acc[4 * e]);
-        acc[4 * e + 1] = fmaf(w, va[q][e][1], acc[4 * e + 1]);
-        acc[4 * e + 2] = fmaf(w, va[q][e][2], acc[4 * e + 2]);
-        acc[4 * e + 3] = fmaf(w, va[q][e][3], acc[4 * e + 3]);
+        for (int e = 0; e < DE / 4; ++e) va[q][e] = live ? row[e] : f32x4{0.f, 0.f, 0.f, 0.f};
       }
+      float mc = M;
+#pragma unroll
+      for (int q = 0; q < kCombineChunk; ++q) mc = fmaxf(mc, vm[q]);
+      const float ms = mc == kNegInf ? 0.f : mc;
+      const float r = fast_exp2((M == kNegInf ? ms : M) - ms);
+      den *= r;
+#pragma unroll
+      for (int e = 0; e < DE; ++e) acc[e] *= r;
+#pragma unroll
+      for (int q = 0; q < kCombineChunk; ++q) {
+        const float w = fast_exp2(vm[q] - ms);  // 0 for padded segments (m = -inf)
+        den = fmaf(w, vl[q], den);
+#pragma unroll
+        for (int e = 0; e < DE / 4; ++e) {
+          acc[4 * e] = fmaf(w, va[q][e][0], acc[4 * e]);
+          acc[4 * e + 1] = fmaf(w, va[q][e][1], acc[4 * e + 1]);
+          acc[4 * e + 2] = fmaf(w, va[q][e][2], acc[4 * e + 2]);
+          acc[4 * e + 3] = fmaf(w, va[q][e][3], acc[4 * e + 3]);
+        }
+      }
+      M = mc;
     }
-    M = mc;
   }
   const float inv = den > 0.f ? 1.f / den : 0.f;
   const int64_t o = obase + (int64_t)h * D + d0;
@@ -1045,6 +1169,70 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   for (int e = 0; e < DE; ++e) {
     if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[o + e] = (uint16_t)f32_to_bf16_bits(acc[e] * inv);
     else static_cast<float*>(a.out)[o + e] = acc[e] * inv;
+  }
+}
+
+// ------------------------------------------------------------- shared prefix
+
+// Shared-prefix mode, before the decode kernel: the number of leading blocks
+// group g's members really share. It is at most the caller's bound, at most
+// every member's full blocks, and only as long as every member's block-table
+// row holds the same ids, so a wrong bound costs speed, never correctness (a
+// bound cut short by differing ids is flagged). One workgroup per group: each
+// thread compares one block position across the members, 8 loads in flight.
+constexpr int kPrefixThreads = 256;
+
+__device__ __forceinline__ int block_min(int x, int* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const int y = __shfl_xor(x, o, 64);
+    x = x < y ? x : y;
+  }
+  __syncthreads();  // red is reused: earlier readers are done
+  if (lane_id() == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kPrefixThreads / 64; ++w) x = x < red[w] ? x : red[w];
+  return x;
+}
+
+__global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(DecodeArgs a, int num_groups) {
+  __shared__ int red[kPrefixThreads / 64];
+  const int g = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int gs = a.group_size, first = g * gs;
+  int S = a.shared_blocks[g];
+  S = S < 0 ? 0 : (S > a.max_blocks ? a.max_blocks : S);
+  for (int i = tid; i < gs; i += kPrefixThreads) {
+    const int full = clamp_len(a, a.seq_lens[first + i]) / kBlockSize;
+    S = S < full ? S : full;
+  }
+  S = block_min(S, red);
+  const int32_t* row0 = a.block_table + (int64_t)first * a.max_blocks;
+  int common = S;
+  for (int j0 = 0; j0 < S; j0 += kPrefixThreads) {
+    const int j = j0 + tid;
+    bool same = true;
+    if (j < S) {
+      const int id = row0[j];
+      for (int i = 1; i < gs; i += 8) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          v[u] = i + u < gs ? a.block_table[(int64_t)(first + i + u) * a.max_blocks + j] : id;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) same &= v[u] == id;
+      }
+    }
+    const int d = block_min(j < S && !same ? j : INT32_MAX, red);
+    if (d != INT32_MAX) {
+      common = d;
+      break;
+    }
+  }
+  if (tid == 0) {
+    a.sg[g] = common;
+    if (common < S) atomicOr(a.hdr + kHdrStatus, kStatusPrefixShortened);
   }
 }
 
@@ -1115,6 +1303,15 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   DecodeArgs args = a;
   void* params[] = {&args};
   return hipLaunchKernel(fn, dim3(units), dim3(kCombineThreads), params, 0, s);
+}
+
+hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s) {
+  if (num_groups <= 0) return hipSuccess;
+  DecodeArgs args = a;
+  int ng = num_groups;
+  void* params[] = {&args, &ng};
+  return hipLaunchKernel(reinterpret_cast<void*>(&prefix_kernel), dim3(num_groups), dim3(kPrefixThreads), params, 0,
+                         s);
 }
 
 hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* waves_per_cu) {

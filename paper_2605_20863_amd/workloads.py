@@ -91,6 +91,10 @@ WORKLOADS = {
     # fp8 (OCP e4m3) KV cache at scale with per-(block, KV head) scales.
     "fp8kv": Workload("fp8kv", 512, 64, 8, 128, "bf16", "fp8_e4m3",
                       ("lognormal", 8192, 0.9, 128, 65536), cfg_id=4),
+    # GRPO groups over long shared contexts (3-6k-token prompts, ~1k-token
+    # responses): the shape where reading shared blocks once matters most.
+    "grpo_longprompt_bf16": Workload("grpo_longprompt_bf16", 256, 32, 8, 128, "bf16", "bf16",
+                                     ("grpo", 32, 8, 3072, 6144, 1024, 0.8, 8192), cfg_id=5),
 }
 
 # Reduced versions with the same heads, dtypes and length structure, sized so the
@@ -215,6 +219,16 @@ def make_layout(w: Workload, seq_lens=None) -> Layout:
     used[perm[:nvirt]] = True
     copies_phys = [(int(perm[a]), int(perm[b]), n) for (a, b, n) in copies]
     return Layout(lens, table, NB, used, prompt_lens, copies_phys)
+
+
+def group_prefix(w: Workload, layout: Layout):
+    """For a GRPO workload: (group_size, shared_blocks) with shared_blocks[g]
+    the number of leading full blocks (the prompt's) that the block tables of
+    group g's samples share. None for other workloads."""
+    if w.lengths[0] != "grpo" or layout.prompt_lens is None:
+        return None
+    samples = int(w.lengths[2])
+    return samples, (layout.prompt_lens[::samples] // w.block_size).astype(np.int32)
 
 
 @dataclasses.dataclass

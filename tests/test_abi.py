@@ -24,7 +24,8 @@ def prob(**kw):
 def test_exports_every_declared_symbol():
     declared = L.header_symbols()
     assert set(declared) == {"pda_paged_decode_attention", "pda_query_plan", "pda_read_device_status",
-                             "pda_release_workspaces", "pda_last_error", "pda_version"}
+                             "pda_release_workspaces", "pda_last_error", "pda_version",
+                             "pda_paged_decode_attention_shared_prefix", "pda_query_plan_shared_prefix"}
     for name in declared:
         assert hasattr(L._lib, name), name
     nm = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True).stdout
@@ -174,3 +175,31 @@ def test_one_hip_runtime_in_process():
     hip = {os.path.realpath(l.split()[-1]) for l in maps.splitlines() if "libamdhip64" in l}
     hsa = {os.path.realpath(l.split()[-1]) for l in maps.splitlines() if "libhsa-runtime64" in l}
     assert len(hip) == 1 and len(hsa) == 1, (hip, hsa)
+
+
+def test_shared_prefix_argument_checks():
+    p = prob(num_seqs=8, num_q_heads=32, num_kv_heads=8)
+    call = lambda gs, sb=16, pr=p, opt=None: L.raw_call_shared_prefix(16, 16, 16, 16, 16, 16, 16, 0.1, gs, sb, pr, opt)
+    assert call(0) == L.EINVAL              # group_size < 1
+    assert call(3) == L.EINVAL              # 8 sequences are not groups of 3
+    assert call(4, sb=None) == L.EINVAL     # shared_blocks missing
+    assert call(4, opt=L.make_options("vector")) == L.EUNSUPPORTED
+    assert call(4, pr=prob(num_seqs=8, q_dtype=L.F32, kv_dtype=L.F32)) == L.EUNSUPPORTED
+    # an empty batch is a no-op
+    assert call(4, sb=None, pr=prob(num_seqs=0)) == L.OK
+
+
+def test_shared_prefix_plan_and_workspace():
+    # GRPO step: 256 sequences = 32 groups of 8, 32/8 heads (G = 4): entries hold 4 members
+    # (16 query columns), so each group's shared blocks form 2 entries ahead of 256 suffix entries.
+    p = prob(num_seqs=256, num_q_heads=32, num_kv_heads=8, max_blocks_per_seq=2048)
+    info = L.query_plan_shared_prefix(p, 8, L.make_options(waves_per_cu=4), num_compute_units=256)
+    assert info.variant == L.VARIANT_MFMA and info.waves == 1024 and info.chunks_max == 1024
+    entries = 32 * 2 + 256
+    slots = entries * 8 + info.chunks_max
+    up = lambda x: (x + 255) // 256 * 256
+    gp = 4 * 4
+    assert info.workspace_bytes == (up(64) + up(32 * 4) + up(entries * 4) + 2 * up(slots * gp * 4)
+                                    + up(slots * gp * 128 * 4))
+    # G = 4 with a small group: a G < 4 batch also runs on the MFMA kernel in this mode
+    assert L.query_plan_shared_prefix(prob(num_seqs=6, num_q_heads=4, num_kv_heads=4), 2).variant == L.VARIANT_MFMA

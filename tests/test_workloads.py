@@ -75,3 +75,18 @@ def test_values_and_poison():
     assert torch.all(codes <= 448) and codes.max() == 448
     t = W.generate(W.SMALL_WORKLOADS["gqa7b_bf16"])
     assert t.k_cache.dtype == torch.bfloat16 and t.v_cache.shape[2:] == (128, 16)
+
+
+def test_group_prefix_matches_the_shared_blocks():
+    """group_prefix reports exactly the leading block ids a GRPO group's samples share."""
+    for name in ("grpo_bf16", "grpo_longprompt_bf16"):
+        w = W.WORKLOADS[name]
+        lay = W.make_layout(w)
+        gs, sb = W.group_prefix(w, lay)
+        assert gs == w.lengths[2] and sb.shape == (w.num_seqs // gs,)
+        for g in range(len(sb)):
+            rows = lay.block_table[g * gs:(g + 1) * gs]
+            assert (rows[:, :sb[g]] == rows[0, :sb[g]]).all()
+            nxt = rows[:, sb[g]]                 # first private block (prompt tail or response)
+            assert len(np.unique(nxt[nxt >= 0])) == (nxt >= 0).sum()
+    assert W.group_prefix(W.WORKLOADS["gqa7b_bf16"], W.make_layout(W.WORKLOADS["gqa7b_bf16"])) is None
