@@ -23,6 +23,9 @@ the new token's query to the keys and values cached for its sequence:
 with K_b, V_b the sequence's cached keys/values for KV head h // G, read
 through a block table as in the paged KV-cache memory management the paper
 cites in Sec. 8 (vLLM / PagedAttention).
+
+``kv_append`` restates the step before it: writing each sequence's new key and
+value into its paged cache, with the fp8 tile-scale policy the library uses.
 """
 
 from .decode_attention import (  # noqa: F401
@@ -36,3 +39,4 @@ from .decode_attention import (  # noqa: F401
     attend_partial,
     combine_partials,
 )
+from .kv_append import encode_bf16, encode_e4m3fn, append_tile_fp8, paged_kv_append  # noqa: F401,E402
