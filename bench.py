@@ -53,6 +53,17 @@ def algorithmic_bytes(workload, seq_lens, shared=None):
     return kv + scales + 2 * B * hq * d * e_q + 4 * blocks + 4 * B, tokens
 
 
+def append_bytes(workload, B):
+    """Bytes one KV append of a decode step must move: every sequence's new K
+    and V rows read (bf16) and written in the cache dtype, fp8 tile scales read
+    and written, positions and block-table entries. Re-encoding a tile whose
+    scale grows is data-dependent and not counted."""
+    e_kv = {"f32": 4, "bf16": 2, "fp8_e4m3": 1}[workload.kv_dtype]
+    hkv, d = workload.num_kv_heads, workload.head_dim
+    scales = 2 * 2 * B * hkv * 4 if workload.kv_dtype == "fp8_e4m3" else 0
+    return 2 * B * hkv * d * (2 + e_kv) + scales + 8 * B
+
+
 # ----------------------------------------------------------------- CPU baseline
 
 def _worker_init():
@@ -179,6 +190,9 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op", default="decode", choices=["decode", "append"],
+                    help="decode: one attention step (default); append: the KV append of one decode step "
+                         "(each sequence's new token written into its last slot)")
     ap.add_argument("--shared-prefix", action="store_true",
                     help="GRPO workloads: read each group's shared prompt blocks once for several members "
                          "(pda_paged_decode_attention_shared_prefix); bytes count the shared blocks once")
@@ -241,9 +255,23 @@ def main():
     if shared is not None:
         sb_dev = torch.as_tensor(shared[1], device=dev)
 
+    if args.op == "append":
+        # one new token per sequence, written into its last slot (the block exists)
+        gen = torch.Generator(device=dev).manual_seed(7)
+        B, hkv, d = len(lens), w.num_kv_heads, w.head_dim
+        k_new = torch.randn((B, hkv, d), generator=gen, device=dev).to(torch.bfloat16)
+        v_new = torch.randn((B, hkv, d), generator=gen, device=dev).to(torch.bfloat16)
+        positions = torch.clamp(inp.seq_lens - 1, min=-1).to(torch.int32)
+        aprob = _lib.AppendProblem(B, hkv, d, w.block_size, inp.block_table.shape[1], inp.k_cache.shape[0],
+                                   _lib.BF16, _lib._dtype_code(inp.k_cache, "k_cache"))
+        nbytes, tokens = append_bytes(w, B), B
+
     def step(i):
         kp, vp, sp = ptrs[i % ncopies]
-        if shared is not None:
+        if args.op == "append":
+            rc = _lib.raw_kv_append(k_new.data_ptr(), v_new.data_ptr(), kp, vp, sp, bp, positions.data_ptr(),
+                                    aprob, sh)
+        elif shared is not None:
             rc = _lib.raw_call_shared_prefix(qp, kp, vp, bp, lp, sp, op, inp.softmax_scale, shared[0],
                                              sb_dev.data_ptr(), prob, opts, sh)
         else:
@@ -254,7 +282,8 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    assert torch.isfinite(out.float()).all(), "non-finite output"
+    if args.op == "decode":
+        assert torch.isfinite(out.float()).all(), "non-finite output"
 
     # Timed region: K back-to-back calls. Two HIP events on the calls' stream
     # bracket it (events between calls would add their own GPU time), so the
@@ -279,10 +308,12 @@ def main():
 
     achieved = nbytes / (call_ms * 1e-3) / 1e9
     value = nbytes / (ms_per_step * 1e-3) / 1e9
-    traffic = measured_traffic(w.name + ("_shared" if shared is not None else ""), nbytes)
+    traffic = (measured_traffic(w.name + ("_shared" if shared is not None else ""), nbytes)
+               if args.op == "decode" else None)
     dtype = {"f32": "f32", "bf16": "bf16", "fp8_e4m3": "fp8e4m3-kv/bf16-q"}[w.kv_dtype]
     res = {
-        "metric": "paged decode attention achieved HBM GB/s (% of peak) + KV tokens/s read",
+        "metric": ("paged decode attention achieved HBM GB/s (% of peak) + KV tokens/s read" if args.op == "decode"
+                   else "paged KV append achieved HBM GB/s (% of peak) + new tokens/s written"),
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -309,10 +340,12 @@ def main():
             "variant": args.variant,
             "cache_copies": ncopies,
             "shared_prefix": shared is not None,
+            "op": args.op,
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": ("decode step (prefix check + stream-K decode + LSE combine, one call)" if shared is not None
+            "kernel": ("KV append (one call)" if args.op == "append"
+                       else "decode step (prefix check + stream-K decode + LSE combine, one call)" if shared is not None
                        else "decode step (stream-K decode + LSE combine, one call)"),
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
@@ -324,7 +357,7 @@ def main():
         },
         "cpu_baseline": None,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.op == "decode":
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
     print(json.dumps(res), flush=True)

@@ -204,6 +204,63 @@ int pda_query_plan_shared_prefix(const pda_problem* problem,
                                  int32_t num_compute_units,
                                  pda_plan_info* info);
 
+/* Shapes and dtypes of one KV append (see pda_paged_kv_append). */
+typedef struct pda_append_problem {
+  int32_t num_seqs;            /* B */
+  int32_t num_kv_heads;        /* Hkv */
+  int32_t head_dim;            /* D: 64 or 128 */
+  int32_t block_size;          /* tokens per KV block: 16 */
+  int32_t max_blocks_per_seq;  /* block_table row stride */
+  int64_t num_blocks;          /* NB */
+  int32_t new_dtype;           /* k_new / v_new: PDA_DTYPE_F32 or PDA_DTYPE_BF16 */
+  int32_t kv_dtype;            /* cache: PDA_DTYPE_F32, PDA_DTYPE_BF16 or PDA_DTYPE_FP8_E4M3 */
+} pda_append_problem;
+
+/*
+ * The step before attention in every decode step (the paper's Sec. 2.2 rollout
+ * decoding, over the paged cache of the vLLM work cited in its Sec. 8): write
+ * each sequence's new key and value into its paged cache, enqueued on
+ * `stream`.
+ *
+ *   k_new, v_new  [B, Hkv, D] device, new_dtype (finite values)
+ *   k_cache       [NB, Hkv, 16, D], v_cache [NB, Hkv, D, 16]: the layouts
+ *                 pda_paged_decode_attention reads
+ *   kv_scales     [2, NB, Hkv] fp32 (fp8 caches; NULL otherwise), read and written
+ *   block_table   [B, max_blocks_per_seq] int32
+ *   positions     [B] int32 device: index of the new token (the sequence's
+ *                 length before the append); a negative position skips the
+ *                 sequence
+ *
+ * Token t of sequence b goes to block block_table[b, t / 16], slot t % 16: a
+ * row of the K tile and a column of the V tile, rounded to nearest even for a
+ * bf16 cache. An fp8 (E4M3) cache keeps each (block, KV head) tile's K and V
+ * scales at max(amax / 448, 2^-126) over the tokens written to the tile so
+ * far: a token whose amax exceeds 448 * scale raises the scale to its own
+ * amax / 448 and re-encodes the tile's earlier codes (decoded value * old /
+ * new scale); slot 0 starts a fresh scale. A full tile therefore ends with its
+ * amax scale, as in a per-tile quantisation. All code decisions are float32
+ * steps (correctly rounded division), encoding rounds to nearest even after
+ * clamping to +-448.
+ *
+ * A position at or past 16 * max_blocks_per_seq, or a block-table entry
+ * outside [0, num_blocks), skips that sequence and sets status bit 1 or 2
+ * (pda_read_device_status). Two sequences writing the same (block, slot) in
+ * one call race; sequences normally append to private blocks.
+ *
+ * Errors: all checks run on the host before any HIP call: PDA_EINVAL for bad
+ * sizes, dtypes or NULL pointers, PDA_EUNSUPPORTED for head_dim not in {64,
+ * 128} or block_size != 16. Uses the stream's workspace (status word).
+ */
+int pda_paged_kv_append(const void* k_new,
+                        const void* v_new,
+                        void* k_cache,
+                        void* v_cache,
+                        float* kv_scales,
+                        const int32_t* block_table,
+                        const int32_t* positions,
+                        const pda_append_problem* problem,
+                        hipStream_t stream);
+
 /* Wait for `stream`, then return (and clear) the device-side status bits that
  * calls on it recorded: 1 = a sequence length was clamped, 2 = a block-table
  * entry outside [0, num_blocks) was skipped, 4 = a group's members share fewer

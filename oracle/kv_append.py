@@ -57,29 +57,16 @@ def encode_e4m3fn(z):
     or 0xFF.
     """
     z = np.asarray(z, dtype=np.float32)
-    out = np.empty(z.shape, dtype=np.uint8)
-    flat_z = z.reshape(-1)
-    flat_o = out.reshape(-1)
-    for i, v in enumerate(flat_z.astype(np.float64)):
-        sign = 0x80 if np.signbit(v) else 0
-        if np.isnan(v):
-            flat_o[i] = 0x7F | sign
-            continue
-        a = min(abs(v), E4M3_MAX)
-        hi = int(np.searchsorted(_POS_VALUES, a, side="left"))  # first value >= a
-        if _POS_VALUES[hi] == a:
-            code = hi
-        else:
-            lo = hi - 1
-            d_lo, d_hi = a - _POS_VALUES[lo], _POS_VALUES[hi] - a
-            if d_lo < d_hi:
-                code = lo
-            elif d_hi < d_lo:
-                code = hi
-            else:
-                code = lo if lo % 2 == 0 else hi
-        flat_o[i] = code | sign
-    return out
+    v = z.astype(np.float64)
+    sign = np.where(np.signbit(v), 0x80, 0).astype(np.uint8)
+    a = np.minimum(np.abs(np.nan_to_num(v, nan=0.0)), E4M3_MAX)
+    hi = np.searchsorted(_POS_VALUES, a, side="left")          # first value >= a
+    lo = np.maximum(hi - 1, 0)
+    d_lo = a - _POS_VALUES[lo]
+    d_hi = _POS_VALUES[hi] - a
+    pick_lo = (d_lo < d_hi) | ((d_lo == d_hi) & (lo % 2 == 0))
+    code = np.where(_POS_VALUES[hi] == a, hi, np.where(pick_lo, lo, hi)).astype(np.uint8)
+    return np.where(np.isnan(v), np.uint8(0x7F) | sign, code | sign).astype(np.uint8)
 
 
 def encode_bf16(x):
@@ -90,28 +77,16 @@ def encode_bf16(x):
     a tie goes to the even pattern. NaN stays a quiet NaN.
     """
     x = np.asarray(x, dtype=np.float32)
-    out = np.empty(x.shape, dtype=np.uint16)
-    flat_x = x.reshape(-1)
-    flat_o = out.reshape(-1)
-    for i, v in enumerate(flat_x):
-        bits = int(np.array(v, dtype=np.float32).view(np.uint32))
-        if np.isnan(v):
-            flat_o[i] = (bits >> 16) | 0x40
-            continue
-        down = bits >> 16
-        up = down + 1
-        vd = float(bf16_to_f64(np.uint16(down)))
-        vu = float(bf16_to_f64(np.uint16(up & 0xFFFF)))
-        exact = float(v)
-        if vd == exact:
-            flat_o[i] = down
-            continue
-        dd, du = abs(exact - vd), abs(vu - exact)
-        if dd < du or (dd == du and down % 2 == 0):
-            flat_o[i] = down
-        else:
-            flat_o[i] = up
-    return out
+    bits = x.view(np.uint32).astype(np.uint64)
+    down = bits >> 16
+    up = down + 1
+    vd = bf16_to_f64(down.astype(np.uint16))
+    vu = bf16_to_f64((up & 0xFFFF).astype(np.uint16))
+    exact = x.astype(np.float64)
+    dd, du = np.abs(exact - vd), np.abs(vu - exact)
+    take_down = (vd == exact) | (dd < du) | ((dd == du) & (down % 2 == 0))
+    out = np.where(take_down, down, up).astype(np.uint16)
+    return np.where(np.isnan(x), ((bits >> 16) | 0x40).astype(np.uint16), out).astype(np.uint16)
 
 
 def _as_f32(x, dtype):

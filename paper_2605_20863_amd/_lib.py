@@ -79,6 +79,19 @@ class PlanInfo(ctypes.Structure):
     ]
 
 
+class AppendProblem(ctypes.Structure):
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("max_blocks_per_seq", ctypes.c_int32),
+        ("num_blocks", ctypes.c_int64),
+        ("new_dtype", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+    ]
+
+
 _vp = ctypes.c_void_p
 _lib.pda_paged_decode_attention.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_float,
                                             ctypes.POINTER(Problem), ctypes.POINTER(Options), _vp]
@@ -93,6 +106,8 @@ _lib.pda_paged_decode_attention_shared_prefix.restype = ctypes.c_int
 _lib.pda_query_plan_shared_prefix.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Options), ctypes.c_float,
                                               ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(PlanInfo)]
 _lib.pda_query_plan_shared_prefix.restype = ctypes.c_int
+_lib.pda_paged_kv_append.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.POINTER(AppendProblem), _vp]
+_lib.pda_paged_kv_append.restype = ctypes.c_int
 _lib.pda_read_device_status.argtypes = [_vp]
 _lib.pda_read_device_status.restype = ctypes.c_int
 _lib.pda_release_workspaces.argtypes = []
@@ -152,6 +167,13 @@ def raw_call_shared_prefix(q, k_cache, v_cache, block_table, seq_lens, kv_scales
         q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, ctypes.c_float(softmax_scale),
         int(group_size), shared_blocks, ctypes.byref(problem),
         ctypes.byref(options) if options is not None else None, stream)
+
+
+def raw_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, positions, problem: AppendProblem,
+                  stream=None) -> int:
+    """pda_paged_kv_append with integer pointers; returns the status code."""
+    return _lib.pda_paged_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, positions,
+                                    ctypes.byref(problem), stream)
 
 
 def query_plan_shared_prefix(problem: Problem, group_size: int, options: Options | None = None,
@@ -292,6 +314,41 @@ def _prepare(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, max_seq
         raise ValueError("kv_scales must be [2, num_blocks, num_kv_heads]")
     opts = make_options(variant, waves_per_cu, min_blocks_per_wave, chunks_per_wave, min_blocks_per_chunk)
     return prob, opts
+
+
+def paged_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, positions, stream=None):
+    """Enqueue the write of one decode step's new keys / values ([B, Hkv, D],
+    float32 or bfloat16) into the paged cache at ``positions`` (int32 [B]);
+    layouts as for paged_decode_attention. fp8 caches update ``kv_scales``."""
+    torch = _torch()
+    tensors = {"k_new": k_new, "v_new": v_new, "k_cache": k_cache, "v_cache": v_cache,
+               "block_table": block_table, "positions": positions}
+    if kv_scales is not None:
+        tensors["kv_scales"] = kv_scales
+    dev = k_new.device
+    for name, t in tensors.items():
+        if not t.is_cuda or t.device != dev:
+            raise ValueError(f"{name} must be on {dev}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if block_table.dtype != torch.int32 or positions.dtype != torch.int32:
+        raise TypeError("block_table and positions must be int32")
+    if v_new.shape != k_new.shape or v_new.dtype != k_new.dtype:
+        raise ValueError("k_new and v_new must match")
+    B, hkv, d = k_new.shape
+    nb, hkv2, bs, d2 = k_cache.shape
+    if (hkv2, d2) != (hkv, d) or tuple(v_cache.shape) != (nb, hkv, d, bs) or positions.shape != (B,):
+        raise ValueError("shapes: k_cache [NB, Hkv, 16, D], v_cache [NB, Hkv, D, 16], positions [B]")
+    kv_dt = _dtype_code(k_cache, "k_cache")
+    if kv_dt == FP8_E4M3 and (kv_scales is None or tuple(kv_scales.shape) != (2, nb, hkv)
+                              or kv_scales.dtype != torch.float32):
+        raise ValueError("an fp8 cache needs float32 kv_scales [2, num_blocks, num_kv_heads]")
+    prob = AppendProblem(B, hkv, d, bs, block_table.shape[1], nb, _dtype_code(k_new, "k_new"), kv_dt)
+    with torch.cuda.device(dev):
+        rc = raw_kv_append(k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                           kv_scales.data_ptr() if kv_scales is not None else None, block_table.data_ptr(),
+                           positions.data_ptr(), prob, _stream_handle(stream, dev))
+    _check(rc)
 
 
 def read_device_status(stream=None, device=None) -> int:

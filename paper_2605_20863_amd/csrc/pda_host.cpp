@@ -410,6 +410,66 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   return PDA_OK;
 }
 
+int append_run(const void* k_new, const void* v_new, void* k_cache, void* v_cache, float* kv_scales,
+               const int32_t* block_table, const int32_t* positions, const pda_append_problem* pr,
+               hipStream_t stream) {
+  g_error.clear();
+  if (!pr) return fail(PDA_EINVAL, "problem is NULL");
+  if (pr->num_seqs < 0) return fail(PDA_EINVAL, "num_seqs = %d < 0", pr->num_seqs);
+  if (pr->num_kv_heads < 1) return fail(PDA_EINVAL, "num_kv_heads = %d < 1", pr->num_kv_heads);
+  if (pr->head_dim != 64 && pr->head_dim != 128)
+    return fail(PDA_EUNSUPPORTED, "head_dim = %d (supported: 64, 128)", pr->head_dim);
+  if (pr->block_size != pda::kBlockSize)
+    return fail(PDA_EUNSUPPORTED, "block_size = %d (supported: 16)", pr->block_size);
+  if (pr->max_blocks_per_seq < 1) return fail(PDA_EINVAL, "max_blocks_per_seq = %d < 1", pr->max_blocks_per_seq);
+  if ((int64_t)pr->max_blocks_per_seq * pda::kBlockSize > INT32_MAX)
+    return fail(PDA_EINVAL, "max_blocks_per_seq * 16 overflows int32");
+  if ((int64_t)pr->num_seqs * pr->num_kv_heads > INT32_MAX) return fail(PDA_EINVAL, "num_seqs * num_kv_heads too large");
+  if (pr->num_blocks < 1) return fail(PDA_EINVAL, "num_blocks = %lld < 1", (long long)pr->num_blocks);
+  const int64_t tile = (int64_t)pda::kBlockSize * pr->head_dim * 4;
+  if (pr->num_blocks > INT64_MAX / pr->num_kv_heads / tile) return fail(PDA_EINVAL, "num_blocks too large");
+  if (pr->new_dtype != PDA_DTYPE_F32 && pr->new_dtype != PDA_DTYPE_BF16)
+    return fail(PDA_EINVAL, "new_dtype = %d (supported: F32, BF16)", pr->new_dtype);
+  const int kd = pr->kv_dtype;
+  if (kd != PDA_DTYPE_F32 && kd != PDA_DTYPE_BF16 && kd != PDA_DTYPE_FP8_E4M3)
+    return fail(PDA_EINVAL, "kv_dtype = %d is not a pda_dtype", kd);
+  if (pr->num_seqs == 0) return PDA_OK;
+  if (!k_new || !v_new || !k_cache || !v_cache || !block_table || !positions)
+    return fail(PDA_EINVAL, "a required pointer (k_new, v_new, k_cache, v_cache, block_table, positions) is NULL");
+  if (kd == PDA_DTYPE_FP8_E4M3 && !kv_scales) return fail(PDA_EINVAL, "an fp8 KV cache needs kv_scales");
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  DeviceInfo di;
+  int rc;
+  if ((rc = device_info(dev, &di)) != PDA_OK) return rc;
+  if (!di.ok) return fail(PDA_EUNSUPPORTED, "device %d is %s; this library is built for gfx950", dev, di.arch.c_str());
+  Workspace* ws = workspace_for(dev, stream);
+  std::lock_guard<std::mutex> lk(ws->mu);
+  if ((rc = ensure_workspace(ws, align_up(pda::kHdrWords * 4), stream)) != PDA_OK) return rc;
+
+  pda::AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.kv_scales = kv_scales;
+  a.block_table = block_table;
+  a.positions = positions;
+  a.B = pr->num_seqs;
+  a.Hkv = pr->num_kv_heads;
+  a.D = pr->head_dim;
+  a.max_blocks = pr->max_blocks_per_seq;
+  a.num_blocks = pr->num_blocks;
+  a.new_bf16 = pr->new_dtype == PDA_DTYPE_BF16;
+  a.status = static_cast<int32_t*>(ws->ptr) + pda::kHdrStatus;
+  const pda::KvType kv = kd == PDA_DTYPE_F32 ? pda::KvType::F32
+                         : kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8;
+  if ((e = pda::launch_append(a, kv, stream)) != hipSuccess) return fail_hip(e, "append kernel launch");
+  return PDA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -430,6 +490,12 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
                                const pda_options* options, hipStream_t stream) {
   return run(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale, nullptr, nullptr,
              problem, options, stream);
+}
+
+int pda_paged_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache, float* kv_scales,
+                        const int32_t* block_table, const int32_t* positions, const pda_append_problem* problem,
+                        hipStream_t stream) {
+  return append_run(k_new, v_new, k_cache, v_cache, kv_scales, block_table, positions, problem, stream);
 }
 
 int pda_paged_decode_attention_shared_prefix(const void* q, const void* k_cache, const void* v_cache,

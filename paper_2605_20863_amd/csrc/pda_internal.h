@@ -74,6 +74,23 @@ inline int64_t partial_slots(int64_t entries, int Hkv, int chunks_max) {
   return entries * Hkv + chunks_max;
 }
 
+// One step's KV append (pda_append.hip).
+struct AppendArgs {
+  const void* k_new;    // [B, Hkv, D] f32 or bf16
+  const void* v_new;
+  void* k_cache;        // [NB, Hkv, 16, D]
+  void* v_cache;        // [NB, Hkv, D, 16]
+  float* kv_scales;     // [2, NB, Hkv] (fp8 caches)
+  const int32_t* block_table;
+  const int32_t* positions;  // [B] slot of the new token; < 0 skips the sequence
+  int32_t B, Hkv, D, max_blocks;
+  int64_t num_blocks;
+  int32_t new_bf16;     // 1: k_new / v_new are bf16, 0: f32
+  int32_t* status;      // workspace status word
+};
+
+hipError_t launch_append(const AppendArgs& a, KvType kv, hipStream_t s);
+
 // Launchers (pda_kernels.hip). Return hipSuccess or the launch error.
 hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);

@@ -25,7 +25,8 @@ def test_exports_every_declared_symbol():
     declared = L.header_symbols()
     assert set(declared) == {"pda_paged_decode_attention", "pda_query_plan", "pda_read_device_status",
                              "pda_release_workspaces", "pda_last_error", "pda_version",
-                             "pda_paged_decode_attention_shared_prefix", "pda_query_plan_shared_prefix"}
+                             "pda_paged_decode_attention_shared_prefix", "pda_query_plan_shared_prefix",
+                             "pda_paged_kv_append"}
     for name in declared:
         assert hasattr(L._lib, name), name
     nm = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True).stdout
@@ -48,8 +49,9 @@ def test_struct_layout_matches_header(tmp_path):
 #include "pda.h"
 #define F(T, m) printf(#T "." #m " %zu\n", offsetof(T, m))
 int main(void) {
-  printf("pda_problem %zu\npda_options %zu\npda_plan_info %zu\n",
-         sizeof(pda_problem), sizeof(pda_options), sizeof(pda_plan_info));
+  printf("pda_problem %zu\npda_options %zu\npda_plan_info %zu\npda_append_problem %zu\n",
+         sizeof(pda_problem), sizeof(pda_options), sizeof(pda_plan_info), sizeof(pda_append_problem));
+  F(pda_append_problem, num_blocks); F(pda_append_problem, kv_dtype);
   F(pda_problem, num_blocks); F(pda_problem, max_seq_len); F(pda_problem, out_dtype);
   F(pda_options, min_blocks_per_wave); F(pda_options, chunks_per_wave); F(pda_options, min_blocks_per_chunk);
   F(pda_plan_info, chunks_max); F(pda_plan_info, workspace_bytes);
@@ -66,6 +68,9 @@ int main(void) {
     assert int(got["pda_problem"]) == ctypes.sizeof(L.Problem)
     assert int(got["pda_options"]) == ctypes.sizeof(L.Options)
     assert int(got["pda_plan_info"]) == ctypes.sizeof(L.PlanInfo)
+    assert int(got["pda_append_problem"]) == ctypes.sizeof(L.AppendProblem)
+    assert int(got["pda_append_problem.num_blocks"]) == L.AppendProblem.num_blocks.offset
+    assert int(got["pda_append_problem.kv_dtype"]) == L.AppendProblem.kv_dtype.offset
     assert int(got["pda_problem.num_blocks"]) == L.Problem.num_blocks.offset
     assert int(got["pda_problem.max_seq_len"]) == L.Problem.max_seq_len.offset
     assert int(got["pda_problem.out_dtype"]) == L.Problem.out_dtype.offset
@@ -203,3 +208,28 @@ def test_shared_prefix_plan_and_workspace():
                                     + up(slots * gp * 128 * 4))
     # G = 4 with a small group: a G < 4 batch also runs on the MFMA kernel in this mode
     assert L.query_plan_shared_prefix(prob(num_seqs=6, num_q_heads=4, num_kv_heads=4), 2).variant == L.VARIANT_MFMA
+
+
+def aprob(**kw):
+    base = dict(num_seqs=4, num_kv_heads=2, head_dim=128, block_size=16, max_blocks_per_seq=8, num_blocks=64,
+                new_dtype=L.BF16, kv_dtype=L.FP8_E4M3)
+    base.update(kw)
+    return L.AppendProblem(**base)
+
+
+def test_append_argument_checks():
+    ok_ptrs = [16] * 7
+    call = lambda pr, ptrs=ok_ptrs: L.raw_kv_append(*ptrs, pr)
+    assert call(aprob(num_seqs=-1)) == L.EINVAL
+    assert call(aprob(num_kv_heads=0)) == L.EINVAL
+    assert call(aprob(head_dim=96)) == L.EUNSUPPORTED
+    assert call(aprob(block_size=32)) == L.EUNSUPPORTED
+    assert call(aprob(max_blocks_per_seq=0)) == L.EINVAL
+    assert call(aprob(num_blocks=0)) == L.EINVAL
+    assert call(aprob(new_dtype=L.FP8_E4M3)) == L.EINVAL
+    assert call(aprob(kv_dtype=7)) == L.EINVAL
+    for i in range(7):       # every pointer is required (kv_scales because the cache is fp8)
+        ptrs = list(ok_ptrs)
+        ptrs[i] = None
+        assert call(aprob(), ptrs) == L.EINVAL, i
+    assert call(aprob(num_seqs=0), [None] * 7) == L.OK   # empty batch: no-op
