@@ -35,6 +35,7 @@ from .decode_attention import (  # noqa: F401
     decode,
     gather_sequence,
     paged_decode_attention,
+    paged_multi_token_attention,
     attend,
     attend_partial,
     combine_partials,

@@ -177,3 +177,36 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, seq_lens, softmax_s
             for h in range(g * G, (g + 1) * G):
                 out[i, h] = attend(qd[b, h], K, V, softmax_scale)
     return out
+
+
+def paged_multi_token_attention(q, k_cache, v_cache, block_table, seq_lens, softmax_scale,
+                                q_dtype, kv_dtype, kv_scales=None, seqs=None):
+    """Reference output of one step with Q new query tokens per sequence,
+    float64 [len(seqs), Q, Hq, D].
+
+    Speculative rollouts (named among RLVR rollout strategies in the paper's
+    Sec. 1) verify several drafted tokens in one step: the cache already holds
+    the Q new tokens as the last Q of the sequence's L, and query token i
+    (0-based among the Q) sits at position L - Q + i, so causally it attends to
+    tokens 0 .. L - Q + i. A query with no visible token (L - Q + i < 0) gives
+    zeros. Q = 1 is the decode step above.
+    """
+    B, Q, hq, d = q.shape
+    hkv = k_cache.shape[1]
+    if hq % hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    G = hq // hkv
+    if kv_dtype == "fp8_e4m3" and kv_scales is None:
+        raise ValueError("fp8 caches need kv_scales")
+    seqs = range(B) if seqs is None else list(seqs)
+    qd = decode(q, q_dtype)
+    out = np.zeros((len(seqs), Q, hq, d), dtype=np.float64)
+    for n, b in enumerate(seqs):
+        L = int(seq_lens[b])
+        for g in range(hkv):
+            K, V = gather_sequence(k_cache, v_cache, block_table, L, b, g, kv_dtype, kv_scales)
+            for i in range(Q):
+                visible = max(L - Q + i + 1, 0)
+                for h in range(g * G, (g + 1) * G):
+                    out[n, i, h] = attend(qd[b, i, h], K[:visible], V[:visible], softmax_scale)
+    return out
