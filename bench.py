@@ -50,7 +50,7 @@ def algorithmic_bytes(workload, seq_lens, shared=None):
         kv_blocks -= dup
     kv = kv_tokens * hkv * 2 * d * e_kv
     scales = kv_blocks * hkv * 2 * 4 if workload.kv_dtype == "fp8_e4m3" else 0
-    return kv + scales + 2 * B * hq * d * e_q + 4 * blocks + 4 * B, tokens
+    return kv + scales + 2 * B * workload.q_tokens * hq * d * e_q + 4 * blocks + 4 * B, tokens
 
 
 def append_bytes(workload, B):
@@ -340,6 +340,7 @@ def main():
             "variant": args.variant,
             "cache_copies": ncopies,
             "shared_prefix": shared is not None,
+            "q_tokens": w.q_tokens,
             "op": args.op,
         },
         "roofline": {
@@ -357,7 +358,7 @@ def main():
         },
         "cpu_baseline": None,
     }
-    if not args.no_cpu_baseline and args.op == "decode":
+    if not args.no_cpu_baseline and args.op == "decode" and w.q_tokens == 1:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
     print(json.dumps(res), flush=True)

@@ -89,6 +89,13 @@ typedef struct pda_problem {
   int32_t q_dtype;             /* pda_dtype: F32 or BF16 */
   int32_t kv_dtype;            /* pda_dtype: F32 (needs F32 q), BF16 or FP8_E4M3 (need BF16 q) */
   int32_t out_dtype;           /* pda_dtype of out: q_dtype or F32 (accumulation stays fp32) */
+  int32_t q_tokens;            /* query tokens per sequence; 0 or 1: one (a decode step). Q > 1
+                                  (speculative verification of drafted tokens, named among the RLVR
+                                  rollout strategies of the paper's Sec. 1): q and out are
+                                  [B, Q, Hq, D], the cache already holds the Q new tokens as the
+                                  sequence's last Q, and query token i attends causally to tokens
+                                  0 .. L - Q + i (zeros if none). Needs the MFMA kernel (bf16 or fp8
+                                  cache) and Q * G <= 16. */
 } pda_problem;
 
 /* Optional tuning knobs; pass NULL for the defaults (all zero). */

@@ -56,6 +56,7 @@ class Problem(ctypes.Structure):
         ("q_dtype", ctypes.c_int32),
         ("kv_dtype", ctypes.c_int32),
         ("out_dtype", ctypes.c_int32),
+        ("q_tokens", ctypes.c_int32),
     ]
 
 
@@ -221,10 +222,15 @@ def _stream_handle(stream, device):
 
 
 def problem_for(q, k_cache, v_cache, block_table, seq_lens, max_seq_len=0, out=None) -> Problem:
-    """Problem descriptor from tensor shapes and dtypes (checks they agree)."""
-    if q.dim() != 3:
-        raise ValueError("q must be [num_seqs, num_q_heads, head_dim]")
-    B, hq, d = q.shape
+    """Problem descriptor from tensor shapes and dtypes (checks they agree).
+    q is [num_seqs, num_q_heads, head_dim], or [num_seqs, q_tokens, num_q_heads,
+    head_dim] for several query tokens per sequence."""
+    if q.dim() == 4:
+        B, ntok, hq, d = q.shape
+    elif q.dim() == 3:
+        (B, hq, d), ntok = q.shape, 1
+    else:
+        raise ValueError("q must be [num_seqs, num_q_heads, head_dim] or [num_seqs, q_tokens, num_q_heads, head_dim]")
     if k_cache.dim() != 4 or v_cache.dim() != 4:
         raise ValueError("k_cache must be [NB, Hkv, 16, D] and v_cache [NB, Hkv, D, 16]")
     nb, hkv, bs, dk = k_cache.shape
@@ -241,7 +247,7 @@ def problem_for(q, k_cache, v_cache, block_table, seq_lens, max_seq_len=0, out=N
         raise TypeError("k_cache and v_cache dtypes differ")
     q_dt = _dtype_code(q, "q")
     out_dt = _dtype_code(out, "out") if out is not None else q_dt
-    return Problem(B, hq, hkv, d, bs, block_table.shape[1], nb, int(max_seq_len), q_dt, kv_dt, out_dt)
+    return Problem(B, hq, hkv, d, bs, block_table.shape[1], nb, int(max_seq_len), q_dt, kv_dt, out_dt, ntok)
 
 
 def paged_decode_attention(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out,

@@ -49,6 +49,7 @@ int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Plan {
   int requested;  // the pda_variant the options asked for
+  int Q;          // query tokens per sequence
   pda::Variant variant;
   pda::KvType kv;
   int G;
@@ -103,10 +104,21 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
   if (pr->out_dtype != qd && pr->out_dtype != PDA_DTYPE_F32)
     return fail(PDA_EINVAL, "out_dtype = %d (must be q_dtype or F32)", pr->out_dtype);
   if (!std::isfinite(softmax_scale)) return fail(PDA_EINVAL, "softmax_scale is not finite");
+  if (pr->q_tokens < 0) return fail(PDA_EINVAL, "q_tokens = %d < 0", pr->q_tokens);
+  const int Q = pr->q_tokens > 1 ? pr->q_tokens : 1;
+  if ((int64_t)pr->num_seqs * Q * pr->num_q_heads > INT32_MAX)
+    return fail(PDA_EINVAL, "num_seqs * q_tokens * num_q_heads too large");
 
   int variant = op ? op->variant : PDA_VARIANT_AUTO;
   if (variant != PDA_VARIANT_AUTO && variant != PDA_VARIANT_VECTOR && variant != PDA_VARIANT_MFMA)
     return fail(PDA_EINVAL, "options.variant = %d is not a pda_variant", variant);
+  if (Q > 1) {  // several query tokens: MFMA columns are (token, head) pairs
+    if (kd == PDA_DTYPE_F32 || variant == PDA_VARIANT_VECTOR)
+      return fail(PDA_EUNSUPPORTED, "q_tokens > 1 runs on the MFMA kernel: it needs a bf16 or fp8 KV cache");
+    if (Q * G > pda::kMaxGroup)
+      return fail(PDA_EUNSUPPORTED, "q_tokens * (num_q_heads / num_kv_heads) = %d exceeds %d", Q * G, pda::kMaxGroup);
+    variant = PDA_VARIANT_MFMA;
+  }
   if (variant == PDA_VARIANT_AUTO)
     variant = (kd != PDA_DTYPE_F32 && G >= 4) ? PDA_VARIANT_MFMA : PDA_VARIANT_VECTOR;
   if (variant == PDA_VARIANT_MFMA && kd == PDA_DTYPE_F32)
@@ -127,6 +139,7 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
   plan->variant = variant == PDA_VARIANT_MFMA ? pda::Variant::Mfma : pda::Variant::Vector;
   plan->kv = kd == PDA_DTYPE_F32 ? pda::KvType::F32 : (kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8);
   plan->G = G;
+  plan->Q = Q;
   plan->len_cap = pr->max_seq_len > 0 ? pr->max_seq_len : (int)table_tokens;
   plan->waves_per_cu = op ? op->waves_per_cu : 0;
   plan->min_share = (op && op->min_blocks_per_wave > 0) ? op->min_blocks_per_wave : kDefaultMinShare;
@@ -158,6 +171,7 @@ int validate_groups(const pda_problem* pr, int32_t group_size, const int32_t* sh
   if (plan->requested == PDA_VARIANT_VECTOR)
     return fail(PDA_EUNSUPPORTED, "shared-prefix decode runs on the MFMA kernel, not the vector kernel");
   if (pr->num_seqs > 0 && !shared_blocks) return fail(PDA_EINVAL, "shared_blocks is NULL");
+  if (plan->Q > 1) return fail(PDA_EUNSUPPORTED, "shared-prefix decode takes one query token per sequence");
   plan->variant = pda::Variant::Mfma;
   gr->on = true;
   gr->group_size = group_size;
@@ -180,7 +194,7 @@ struct Layout {
 Layout workspace_layout(const pda_problem* pr, const Plan& plan, const Groups& gr, int chunks_max) {
   Layout w;
   const int64_t entries = gr.n_prefix + pr->num_seqs;
-  const int64_t gp = gr.on ? (int64_t)gr.M * plan.G : plan.G;
+  const int64_t gp = gr.on ? (int64_t)gr.M * plan.G : (int64_t)plan.Q * plan.G;
   const int64_t slots = pda::partial_slots(entries, pr->num_kv_heads, chunks_max);
   w.hdr = 0;
   w.sg = align_up(pda::kHdrWords * 4);
@@ -389,7 +403,8 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   a.M = gr.M;
   a.nsub = gr.nsub;
   a.n_prefix = (int32_t)gr.n_prefix;
-  a.Gp = gr.on ? gr.M * plan.G : plan.G;
+  a.Gp = gr.on ? gr.M * plan.G : plan.Q * plan.G;
+  a.Qn = plan.Q;
   a.shared_blocks = gr.shared_blocks;
   a.sg = reinterpret_cast<int32_t*>(base + lay.sg);
   a.hdr = reinterpret_cast<int32_t*>(base + lay.hdr);

@@ -46,6 +46,7 @@ struct DecodeArgs {
   int32_t waves;        // launched persistent waves (a multiple of waves_per_group)
   int32_t waves_per_group;  // independent stream-K waves per workgroup: 1, 2 or 4
   int32_t out_bf16;     // 1: out is bf16, 0: f32
+  int32_t Qn;           // query tokens per sequence: q and out are [B, Qn, Hq, D]
   // Work entries. Plain mode: entry b is sequence b (E = B). Shared-prefix
   // mode: entries [0, n_prefix) are the groups' shared leading blocks, nsub
   // per group, each applied to the queries of up to M members (M * G query
@@ -56,7 +57,7 @@ struct DecodeArgs {
   int32_t M;            // members per prefix entry (M * G <= 16)
   int32_t nsub;         // prefix entries per group = ceil(group_size / M)
   int32_t n_prefix;     // num_groups * nsub
-  int32_t Gp;           // query columns per partial row: G, or M * G in shared-prefix mode
+  int32_t Gp;           // query columns per partial row: Qn * G, or M * G in shared-prefix mode
   const int32_t* shared_blocks;  // [num_groups] caller's bound on each group's shared blocks
   // workspace
   int32_t* hdr;         // kHdrWords ints

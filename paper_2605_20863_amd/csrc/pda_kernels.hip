@@ -161,7 +161,7 @@ __device__ __forceinline__ Entry entry_of(const DecodeArgs& a, int v) {
     e.nb = (e.L + kBlockSize - 1) / kBlockSize;
     e.row = a.block_table + (int64_t)v * a.max_blocks;
     e.qs = v;
-    e.ncols = a.G;
+    e.ncols = a.Qn * a.G;
     e.may_final = true;
   } else if (v < a.n_prefix) {
     const int g = v / a.nsub, s = v - g * a.nsub;
@@ -361,27 +361,29 @@ struct BlockIds {
   }
 };
 
-// Physical block of logical block j, or block 0 with lim = 0 when the table
-// entry is out of range (flagged). lim = valid tokens in the block (0..16).
+// Physical block of logical block j, or block 0 with lim = rem = 0 when the
+// table entry is out of range (flagged). rem = valid tokens from the block's
+// first slot to the entry's end (may exceed 16), lim = min(rem, 16).
 struct Blk {
   int64_t tile;  // (p * Hkv + kvh): tile index into either cache
   int p;
   int lim;
+  int rem;
 };
 
 __device__ __forceinline__ Blk block_at(const DecodeArgs& a, BlockIds& ids, int j, int L, int kvh,
                                         int& status) {
   Blk r;
   int p = ids.get(j);
-  int lim = L - j * kBlockSize;
-  lim = lim > kBlockSize ? kBlockSize : lim;
+  int rem = L - j * kBlockSize;
   if ((unsigned)p >= (uint64_t)a.num_blocks) {
     status |= kStatusBadBlock;
     p = 0;
-    lim = 0;
+    rem = 0;
   }
   r.p = p;
-  r.lim = lim;
+  r.rem = rem;
+  r.lim = rem > kBlockSize ? kBlockSize : rem;
   r.tile = (int64_t)p * a.Hkv + kvh;
   return r;
 }
@@ -425,7 +427,7 @@ struct MfmaPair {
   u32x4 k[2][C::NK4];
   VSlice<KV> v[2][C::MT];
   float ks[2], vs[2];
-  int lim[2];
+  int rem[2];  // valid tokens from each block's first slot to the entry's end
 };
 
 // K A-operand of k-step j (8 bf16: dims qdim(j, c) .. +8 of token row r).
@@ -458,7 +460,7 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
     const int j = j0 + s;
     if (s == 0 || j < j_hi) {
       const Blk blk = block_at(a, ids, j, L, kvh, status);
-      bf.lim[s] = blk.lim;
+      bf.rem[s] = blk.rem;
       const uint8_t* kt = kc + blk.tile * TILE + r * D * C::ESZ + 16 * c;
 #pragma unroll
       for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = ld_stream<u32x4>(kt + 64 * i);
@@ -476,7 +478,7 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
         bf.vs[s] = 1.f;
       }
     } else {
-      bf.lim[s] = 0;
+      bf.rem[s] = 0;
 #pragma unroll
       for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = u32x4{0, 0, 0, 0};
 #pragma unroll
@@ -495,12 +497,14 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
 // for any reference max.
 constexpr float kMaxSlack = 8.f;
 
-// One pair of 16-token blocks. MASKED handles pairs with slots at or past the
-// sequence end (or a skipped block): those tokens get logit -inf and zero V.
+// One pair of 16-token blocks. MASKED handles pairs with slots that some of
+// the lane's column may not see -- past the sequence end, a skipped block, or
+// (several query tokens per sequence) past the column's causal end, `hide`
+// tokens before the end: those tokens get logit -inf and zero V.
 template <KvType KV, int D, bool MASKED>
 __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[MfmaCfg<KV, D>::KSTEPS],
                                              float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT],
-                                             float& m_run, float& l_run) {
+                                             float& m_run, float& l_run, int hide) {
   using C = MfmaCfg<KV, D>;
   const int l = lane_id();
   const int c = l >> 4;
@@ -515,16 +519,19 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
   const float c0 = scale_log2 * bf.ks[0];
   const float c1 = scale_log2 * bf.ks[1];
   float x[8];
-  bool valid[8];
+  // live: the lane's token slot holds a token of the entry (the V rows this
+  // lane feeds to PV are these tokens, for every column); the lane's column
+  // sees the token only if it is also `hide` or more slots before the end
+  bool live[8];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     x[i] = s0[i] * c0;
     x[4 + i] = s1[i] * c1;
     if constexpr (MASKED) {
-      valid[i] = 4 * c + i < bf.lim[0];
-      valid[4 + i] = 4 * c + i < bf.lim[1];
-      x[i] = valid[i] ? x[i] : kNegInf;
-      x[4 + i] = valid[4 + i] ? x[4 + i] : kNegInf;
+      live[i] = 4 * c + i < bf.rem[0];
+      live[4 + i] = 4 * c + i < bf.rem[1];
+      x[i] = 4 * c + i < bf.rem[0] - hide ? x[i] : kNegInf;
+      x[4 + i] = 4 * c + i < bf.rem[1] - hide ? x[4 + i] : kNegInf;
     }
   }
   float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
@@ -566,10 +573,10 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
   uint32_t m0a = ~0u, m0b = ~0u, m1a = ~0u, m1b = ~0u;
   if constexpr (MASKED) {
     // select, so NaN poison in dead slots cannot leak through 0 * NaN
-    m0a = (valid[0] ? 0xFFFFu : 0u) | (valid[1] ? 0xFFFF0000u : 0u);
-    m0b = (valid[2] ? 0xFFFFu : 0u) | (valid[3] ? 0xFFFF0000u : 0u);
-    m1a = (valid[4] ? 0xFFFFu : 0u) | (valid[5] ? 0xFFFF0000u : 0u);
-    m1b = (valid[6] ? 0xFFFFu : 0u) | (valid[7] ? 0xFFFF0000u : 0u);
+    m0a = (live[0] ? 0xFFFFu : 0u) | (live[1] ? 0xFFFF0000u : 0u);
+    m0b = (live[2] ? 0xFFFFu : 0u) | (live[3] ? 0xFFFF0000u : 0u);
+    m1a = (live[4] ? 0xFFFFu : 0u) | (live[5] ? 0xFFFF0000u : 0u);
+    m1b = (live[6] ? 0xFFFFu : 0u) | (live[7] ? 0xFFFF0000u : 0u);
   }
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
@@ -589,14 +596,16 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
   }
 }
 
+// `full`: rem at which every column sees all 16 tokens of a block (16 plus
+// the largest `hide`, wave-uniform).
 template <KvType KV, int D>
 __device__ __forceinline__ void mfma_step(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[MfmaCfg<KV, D>::KSTEPS],
                                           float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT], float& m_run,
-                                          float& l_run) {
-  if ((bf.lim[0] & bf.lim[1]) == kBlockSize)  // both blocks full (lim <= 16)
-    mfma_compute<KV, D, false>(bf, qb, scale_log2, acc, m_run, l_run);
+                                          float& l_run, int full, int hide) {
+  if (bf.rem[0] >= full && bf.rem[1] >= full)
+    mfma_compute<KV, D, false>(bf, qb, scale_log2, acc, m_run, l_run, hide);
   else
-    mfma_compute<KV, D, true>(bf, qb, scale_log2, acc, m_run, l_run);
+    mfma_compute<KV, D, true>(bf, qb, scale_log2, acc, m_run, l_run, hide);
 }
 
 template <KvType KV, int D>
@@ -606,12 +615,17 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
   const int r = l & 15, c = l >> 4;
   const int kvh = sg.kvh, L = sg.L, j_lo = sg.j_lo, j_hi = sg.j_hi;
 
-  // Q^T B-operand: column r (member r / G, head r % G), dims qdim(j, c) .. +8 for k-step j.
+  // Q^T B-operand: column r = (mem, head) with mem = r / G the member
+  // (shared-prefix entries) or the query token (several per sequence), dims
+  // qdim(j, c) .. +8 for k-step j. q rows are [sequence, query token, head].
+  const int mem = r / a.G, head = r - mem * a.G;
+  const int64_t qo_row = ((int64_t)sg.qs * a.Qn + mem) * a.Hq + kvh * a.G + head;
+  // query token mem of Qn sits Qn - 1 - mem tokens before the sequence end
+  const int hide = a.Qn > 1 && mem < a.Qn ? a.Qn - 1 - mem : 0;
+  const int full = kBlockSize + a.Qn - 1;
   bf16x8 qb[C::KSTEPS];
   {
-    const int mem = r / a.G;
-    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) +
-                           ((int64_t)(sg.qs + mem) * a.Hq + kvh * a.G + (r - mem * a.G)) * D;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + qo_row * D;
 #pragma unroll
     for (int j = 0; j < C::KSTEPS; ++j) {
       u32x4 w = {0, 0, 0, 0};
@@ -634,26 +648,26 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
   if (npairs > 1) mfma_issue<KV, D>(b1, a, ids, j_lo + 2, j_hi, L, kvh, status);
   int i = 0;
   for (; i + 3 < npairs; i += 2) {
-    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run, full, hide);
     mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
-    mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run, full, hide);
     mfma_issue<KV, D>(b1, a, ids, j_lo + 2 * (i + 3), j_hi, L, kvh, status);
   }
   if (i < npairs) {
-    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run, full, hide);
     if (i + 2 < npairs) mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
   }
-  if (i + 1 < npairs) mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run);
-  if (i + 2 < npairs) mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run);
+  if (i + 1 < npairs) mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run, full, hide);
+  if (i + 2 < npairs) mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run, full, hide);
 
   // Lanes c = 0..3 hold disjoint token subsets of head r: total the denominator.
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
 
   if (r >= sg.ncols) return;
-  if (sg.final) {  // ncols == G: column r is head r of sequence qs
+  if (sg.final) {  // plain entry: column r is query token mem, head `head` of sequence qs
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    const int64_t orow = ((int64_t)sg.qs * a.Hq + kvh * a.G + r) * D;
+    const int64_t orow = qo_row * D;
     if (a.out_bf16) {
       uint16_t* o = static_cast<uint16_t*>(a.out) + orow;
 #pragma unroll
@@ -1071,7 +1085,8 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   const int kvh = u - b * a.Hkv;
   const int G = a.G;
   const int tid = threadIdx.x;
-  const int64_t obase = ((int64_t)b * a.Hq + (int64_t)kvh * G) * D;
+  // this sequence's columns for the KV head: G heads times its query tokens
+  const int ncol = a.Qn * G;
   const int64_t share = a.share[0];
 
   int64_t slot0[2];
@@ -1101,20 +1116,23 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
       ++parts;
     }
   }
+  // output row of column r: query token r / G, head kvh * G + r % G of sequence b
+  auto out_row = [&](int r) { return (((int64_t)b * a.Qn + r / G) * a.Hq + (int64_t)kvh * G + r % G) * D; };
   if (parts == 0) {
-    for (int i = tid; i < G * D; i += kCombineThreads) {
-      if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[obase + i] = 0;
-      else static_cast<float*>(a.out)[obase + i] = 0.f;
+    for (int i = tid; i < ncol * D; i += kCombineThreads) {
+      const int64_t at = out_row(i / D) + i % D;
+      if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[at] = 0;
+      else static_cast<float*>(a.out)[at] = 0.f;
     }
     return;
   }
   if (parts == 1 && nseg[0] == 1 && own.may_final) return;  // one chunk wrote the output
 
-  // thread t owns head h = t / 16 (if < G) and dims [ (t % 16) * D/16, +D/16 )
+  // thread t owns column h = t / 16 (if < ncol) and dims [ (t % 16) * D/16, +D/16 )
   constexpr int DE = D / 16;
   const int h = tid >> 4;
   const int d0 = (tid & 15) * DE;
-  if (h >= G) return;
+  if (h >= ncol) return;
   float acc[DE];
 #pragma unroll
   for (int e = 0; e < DE; ++e) acc[e] = 0.f;
@@ -1164,7 +1182,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
     }
   }
   const float inv = den > 0.f ? 1.f / den : 0.f;
-  const int64_t o = obase + (int64_t)h * D + d0;
+  const int64_t o = out_row(h) + d0;
 #pragma unroll
   for (int e = 0; e < DE; ++e) {
     if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[o + e] = (uint16_t)f32_to_bf16_bits(acc[e] * inv);

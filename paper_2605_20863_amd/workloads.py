@@ -62,6 +62,7 @@ class Workload:
     lengths: tuple
     cfg_id: int
     block_size: int = BLOCK_SIZE
+    q_tokens: int = 1      # query tokens per sequence (> 1: q is [B, q_tokens, Hq, D])
 
     @property
     def group(self) -> int:
@@ -95,6 +96,10 @@ WORKLOADS = {
     # responses): the shape where reading shared blocks once matters most.
     "grpo_longprompt_bf16": Workload("grpo_longprompt_bf16", 256, 32, 8, 128, "bf16", "bf16",
                                      ("grpo", 32, 8, 3072, 6144, 1024, 0.8, 8192), cfg_id=5),
+    # Speculative verification on the 7B GQA step: 2 query tokens per sequence
+    # (the drafted one and the next), 14 of the 16 MFMA columns.
+    "spec2_gqa7b_bf16": Workload("spec2_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
+                                 ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, q_tokens=2),
 }
 
 # Reduced versions with the same heads, dtypes and length structure, sized so the
@@ -288,7 +293,8 @@ def generate(w: Workload, device="cpu", seq_lens=None, q_scale: float = 1.0) -> 
     NB = lay.num_blocks
 
     gq = torch.Generator(device=device).manual_seed(_torch_seed(w, _STREAM_Q))
-    q = (torch.randn((B, hq, d), generator=gq, device=device, dtype=torch.float32) * q_scale)
+    qshape = (B, hq, d) if w.q_tokens == 1 else (B, w.q_tokens, hq, d)
+    q = (torch.randn(qshape, generator=gq, device=device, dtype=torch.float32) * q_scale)
     q = q.to(_TORCH_DTYPE[w.q_dtype])
 
     store = torch.uint8 if w.kv_dtype == "fp8_e4m3" else _TORCH_DTYPE[w.kv_dtype]

@@ -233,3 +233,21 @@ def test_append_argument_checks():
         ptrs[i] = None
         assert call(aprob(), ptrs) == L.EINVAL, i
     assert call(aprob(num_seqs=0), [None] * 7) == L.OK   # empty batch: no-op
+
+
+def test_multi_token_checks_and_plan():
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=-1)) == L.EINVAL
+    # several query tokens need the MFMA kernel (bf16 / fp8 cache) and Q * G <= 16
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1,
+                      prob(q_tokens=2, q_dtype=L.F32, kv_dtype=L.F32)) == L.EUNSUPPORTED
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=5)) == L.EUNSUPPORTED   # G = 4: 20 columns
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=4),
+                      L.make_options("vector")) == L.EUNSUPPORTED
+    assert L.raw_call_shared_prefix(16, 16, 16, 16, 16, 16, 16, 0.1, 2, 16, prob(q_tokens=2)) == L.EUNSUPPORTED
+    # Q = 4, G = 2: MFMA (even though G < 4), partial rows of Q * G = 8 columns
+    p = prob(num_seqs=64, num_q_heads=8, num_kv_heads=4, q_tokens=4)
+    info = L.query_plan(p, L.make_options(waves_per_cu=4), num_compute_units=256)
+    assert info.variant == L.VARIANT_MFMA
+    slots = 64 * 4 + info.chunks_max
+    up = lambda x: (x + 255) // 256 * 256
+    assert info.workspace_bytes == up(64) + up(64 * 4) + 2 * up(slots * 8 * 4) + up(slots * 8 * 128 * 4)
