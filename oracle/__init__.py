@@ -36,6 +36,7 @@ from .decode_attention import (  # noqa: F401
     gather_sequence,
     paged_decode_attention,
     paged_multi_token_attention,
+    paged_prefill_attention,
     attend,
     attend_partial,
     combine_partials,

@@ -210,3 +210,40 @@ def paged_multi_token_attention(q, k_cache, v_cache, block_table, seq_lens, soft
                 for h in range(g * G, (g + 1) * G):
                     out[n, i, h] = attend(qd[b, i, h], K[:visible], V[:visible], softmax_scale)
     return out
+
+
+def paged_prefill_attention(q, q_offsets, k_cache, v_cache, block_table, seq_lens, softmax_scale,
+                            q_dtype, kv_dtype, kv_scales=None, seqs=None):
+    """Reference output of a variable-length prefill over the paged cache,
+    float64 [T, Hq, D] (rows of the listed ``seqs`` only when given; others 0).
+
+    The log-prob forward of RLVR training (the compute_log_prob phase of the
+    paper's Sec. 6.2 phase breakdown, one of the forward calls of its Sec. 3
+    interface) and chunked prefill run attention for many query tokens per
+    sequence at once. Packed q rows q_offsets[b] .. q_offsets[b + 1] - 1 are
+    the last n_b tokens of sequence b (whose cache holds all L_b tokens), so
+    query token i sits at position L_b - n_b + i and attends causally to
+    tokens 0 .. L_b - n_b + i; a query with no visible token gives zeros.
+    """
+    T, hq, d = q.shape
+    hkv = k_cache.shape[1]
+    if hq % hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    G = hq // hkv
+    if kv_dtype == "fp8_e4m3" and kv_scales is None:
+        raise ValueError("fp8 caches need kv_scales")
+    B = len(seq_lens)
+    seqs = range(B) if seqs is None else list(seqs)
+    qd = decode(q, q_dtype)
+    out = np.zeros((T, hq, d), dtype=np.float64)
+    for b in seqs:
+        L = int(seq_lens[b])
+        r0, r1 = int(q_offsets[b]), int(q_offsets[b + 1])
+        n = r1 - r0
+        for g in range(hkv):
+            K, V = gather_sequence(k_cache, v_cache, block_table, L, b, g, kv_dtype, kv_scales)
+            for i in range(n):
+                visible = min(max(L - n + i + 1, 0), L)
+                for h in range(g * G, (g + 1) * G):
+                    out[r0 + i, h] = attend(qd[r0 + i, h], K[:visible], V[:visible], softmax_scale)
+    return out
