@@ -3,7 +3,10 @@
 
 A "step" is one call of the library's decode attention (the stream-K decode
 kernel plus the log-sum-exp combine kernel) over one synthetic decode batch
-whose inputs are already resident in HBM. Default workload: the 7B-class GQA
+whose inputs are already resident in HBM. ``--op append`` times the KV append
+of a decode step instead, and ``--op prefill`` the causal varlen prefill of a
+log-prob forward (plan kernel plus attention kernel, MFMA-bound: reported in
+TFLOP/s of the causal QK^T and PV products). Default workload: the 7B-class GQA
 step (64 sequences, 28 query / 4 KV heads, head_dim 128, bf16, lognormal
 lengths with median 2048). The KV cache is rotated over enough copies that
 consecutive steps never find their cache in the 256 MB last-level cache.
@@ -27,6 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFS = 2500.0   # dense bf16 matrix-core peak of MI355X
 LLC_BYTES = 256 << 20
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2605_20863_amd", "csrc", "pda_kernels.hip")
@@ -62,6 +66,19 @@ def append_bytes(workload, B):
     hkv, d = workload.num_kv_heads, workload.head_dim
     scales = 2 * 2 * B * hkv * 4 if workload.kv_dtype == "fp8_e4m3" else 0
     return 2 * B * hkv * d * (2 + e_kv) + scales + 8 * B
+
+
+def prefill_flops(workload, seq_lens, counts):
+    """Multiply-add flops of a causal prefill: query i of sequence b sees
+    min(max(L - n + i + 1, 0), L) keys, and each visible (query head, key) pair
+    costs D multiply-adds in QK^T and D in PV (2 flops each)."""
+    import numpy as np
+
+    pairs = 0
+    for L, n in zip(seq_lens.astype(np.int64), counts.astype(np.int64)):
+        vis = np.clip(L - n + np.arange(1, n + 1), 0, L)
+        pairs += int(vis.sum())
+    return 4 * workload.head_dim * workload.num_q_heads * pairs, pairs
 
 
 # ----------------------------------------------------------------- CPU baseline
@@ -100,6 +117,90 @@ def _sequence_problem(inp, b, raw):
     w = inp.workload
     return (raw(inp.q[b:b + 1]), kc, vc, table, lay.seq_lens[b:b + 1].copy(), inp.softmax_scale,
             w.q_dtype, w.kv_dtype, ks)
+
+
+def _oracle_prefill_rows(args):
+    import oracle  # the CPU fp64 reference; test infrastructure
+
+    t0 = time.perf_counter()
+    oracle.paged_prefill_attention(**args)
+    return time.perf_counter() - t0
+
+
+def _prefill_rows_problem(pin, b, rows, raw):
+    """Query rows ``rows`` of sequence b as one-token prefills over its cache cut
+    at each row's position (a causal query sees nothing past it); host copies of
+    the blocks they need (data movement only)."""
+    import numpy as np
+    import torch
+
+    c = pin.cache
+    L, n = int(c.layout.seq_lens[b]), int(pin.counts[b])
+    pos = np.array([L - n + int(i) for i in rows], dtype=np.int64)
+    nb = int(pos.max()) // 16 + 1
+    idx = torch.from_numpy(c.layout.block_table[b, :nb].astype(np.int64)).to(c.device)
+    w = c.workload
+    qrows = torch.tensor([int(pin.offsets[b]) + int(i) for i in rows], dtype=torch.long, device=c.device)
+    return dict(q=raw(pin.q.index_select(0, qrows)), q_offsets=np.arange(len(rows) + 1, dtype=np.int32),
+                k_cache=raw(c.k_cache.index_select(0, idx)), v_cache=raw(c.v_cache.index_select(0, idx)),
+                block_table=np.tile(np.arange(nb, dtype=np.int32), (len(rows), 1)),
+                seq_lens=(pos + 1).astype(np.int32), softmax_scale=c.softmax_scale, q_dtype="bf16",
+                kv_dtype=w.kv_dtype,
+                kv_scales=raw(c.kv_scales.index_select(1, idx)) if c.kv_scales is not None else None), pos
+
+
+def cpu_baseline_prefill(pin, budget_s, rows_per_job=4):
+    """Time the oracle on seeded query rows of the prefill, all host cores (<= 16)."""
+    import multiprocessing as mp
+
+    import numpy as np
+    import torch
+
+    def raw(t):
+        t = t.detach().cpu().contiguous()
+        if t.dtype == torch.bfloat16:
+            return t.view(torch.int16).numpy().view(np.uint16)
+        return t.numpy()
+
+    w = pin.cache.workload
+    cores = min(len(os.sched_getaffinity(0)), 16)
+    rng = np.random.default_rng(0)
+    seq_of_row = np.repeat(np.arange(len(pin.counts)), pin.counts)
+    ctx = mp.get_context("spawn")
+    pairs, nrows, t_cpu = 0, 0, 0.0
+    with ctx.Pool(cores, initializer=_worker_init) as pool:
+        t0 = time.perf_counter()
+        pending = []
+        while True:
+            r = int(rng.integers(0, len(seq_of_row)))
+            b = int(seq_of_row[r])
+            i0 = r - int(pin.offsets[b])
+            rows = list(range(i0, min(i0 + rows_per_job, int(pin.counts[b]))))
+            job, pos = _prefill_rows_problem(pin, b, rows, raw)
+            pending.append((int((pos + 1).sum()), len(rows), pool.apply_async(_oracle_prefill_rows, (job,))))
+            if len(pending) >= 2 * cores:
+                pp, nr, res = pending.pop(0)
+                t_cpu += res.get()
+                pairs, nrows = pairs + pp, nrows + nr
+                if time.perf_counter() - t0 > budget_s:
+                    break
+        for pp, nr, res in pending:
+            t_cpu += res.get()
+            pairs, nrows = pairs + pp, nrows + nr
+        wall = time.perf_counter() - t0
+    flops = 4 * w.head_dim * w.num_q_heads * pairs
+    return {
+        "value": round(flops / wall / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": cores,
+        "kind": "oracle",
+        "tokens_per_s": round(nrows / wall, 2),
+        "seconds": round(wall, 2),
+        "cpu_seconds": round(t_cpu, 2),
+        "sample": f"{nrows} query rows (all {w.num_q_heads} heads; runs of {rows_per_job} consecutive rows from "
+                  f"seeded positions) of the same prefill, {pairs} visible (row, key) pairs, fp64 numpy oracle, "
+                  f"one process per core",
+    }
 
 
 def cpu_baseline(inp, budget_s):
@@ -180,7 +281,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="gqa7b_bf16")
+    ap.add_argument("--workload", default=None,
+                    help="default: gqa7b_bf16 (decode, append), logprob_gqa7b_bf16 (prefill)")
     ap.add_argument("--variant", default="auto", choices=["auto", "vector", "mfma"])
     ap.add_argument("--waves-per-cu", type=int, default=0)
     ap.add_argument("--min-blocks-per-wave", type=int, default=0)
@@ -190,9 +292,10 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="decode", choices=["decode", "append"],
+    ap.add_argument("--op", default="decode", choices=["decode", "append", "prefill"],
                     help="decode: one attention step (default); append: the KV append of one decode step "
-                         "(each sequence's new token written into its last slot)")
+                         "(each sequence's new token written into its last slot); prefill: the causal varlen "
+                         "prefill of a log-prob forward")
     ap.add_argument("--shared-prefix", action="store_true",
                     help="GRPO workloads: read each group's shared prompt blocks once for several members "
                          "(pda_paged_decode_attention_shared_prefix); bytes count the shared blocks once")
@@ -223,7 +326,15 @@ def main():
                           "bytes_written_per_dispatch": 1 << 30, "dispatches": args.warmup + args.steps}))
         return
 
+    if args.workload is None:
+        args.workload = "logprob_gqa7b_bf16" if args.op == "prefill" else "gqa7b_bf16"
     w = W.WORKLOADS[args.workload]
+    if (args.op == "prefill") != (w.prefill_frac > 0):
+        print(f"--op {args.op} does not fit workload {w.name}", file=sys.stderr)
+        sys.exit(2)
+    if args.op == "prefill":
+        prefill_main(args, w, dev)
+        return
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     inp = W.generate(w, dev)
     lens = inp.layout.seq_lens
@@ -361,6 +472,110 @@ def main():
     if not args.no_cpu_baseline and args.op == "decode" and w.q_tokens == 1:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+def prefill_main(args, w, dev):
+    """--op prefill: one call = the plan kernel + the attention kernel over all
+    packed query tokens of the log-prob forward."""
+    import numpy as np
+    import torch
+
+    from paper_2605_20863_amd import _lib
+    from paper_2605_20863_amd import workloads as W
+
+    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    pin = W.generate_prefill(w, dev)
+    c = pin.cache
+    lens = c.layout.seq_lens
+    flops, pairs = prefill_flops(w, lens, pin.counts)
+    T = int(pin.q.shape[0])
+    # two cache copies, alternated: a step never starts on the previous step's cached tiles
+    caches = [(c.k_cache, c.v_cache, c.kv_scales),
+              (c.k_cache.clone(), c.v_cache.clone(), c.kv_scales.clone() if c.kv_scales is not None else None)]
+    out = torch.empty_like(pin.q)
+    stream = torch.cuda.current_stream(dev)
+    prob = _lib.PrefillProblem(len(lens), T, w.num_q_heads, w.num_kv_heads, w.head_dim, w.block_size,
+                               c.block_table.shape[1], c.k_cache.shape[0], c.layout.max_seq_len, _lib.BF16,
+                               _lib._dtype_code(c.k_cache, "k_cache"), _lib.BF16)
+    ptrs = [(k.data_ptr(), v.data_ptr(), s.data_ptr() if s is not None else None) for k, v, s in caches]
+    sh = stream.cuda_stream
+    args_fixed = (pin.q.data_ptr(), pin.q_offsets.data_ptr())
+
+    def step(i):
+        kp, vp, sp = ptrs[i % 2]
+        rc = _lib.raw_prefill(args_fixed[0], args_fixed[1], kp, vp, c.block_table.data_ptr(), c.seq_lens.data_ptr(),
+                              sp, out.data_ptr(), c.softmax_scale, prob, sh)
+        if rc != 0:
+            raise RuntimeError(f"pda error {rc}: {_lib.last_error()}")
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all(), "non-finite output"
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    call_ms = ev0.elapsed_time(ev1) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    status = _lib.read_device_status()
+    print(f"[bench] {w.name}: {ms_per_step * 1e3:.1f} us/step wall, {call_ms * 1e3:.1f} us/call GPU, status {status}",
+          file=sys.stderr, flush=True)
+    achieved = flops / (call_ms * 1e-3) / 1e12
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    dtype = {"bf16": "bf16", "fp8_e4m3": "fp8e4m3-kv/bf16-q"}[w.kv_dtype]
+    res = {
+        "metric": "paged varlen causal prefill achieved TFLOP/s (% of bf16 dense MFMA peak) + query tokens/s",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "pct_of_peak": round(100 * value / MFMA_BF16_PEAK_TFS, 2),
+        "tokens_per_s": round(T / (ms_per_step * 1e-3), 1),
+        "config": {
+            "workload": w.name,
+            "num_seqs": len(lens),
+            "q_heads": w.num_q_heads,
+            "kv_heads": w.num_kv_heads,
+            "head_dim": w.head_dim,
+            "kv_dtype": w.kv_dtype,
+            "block_size": w.block_size,
+            "query_tokens": T,
+            "cached_tokens": int(lens.sum()),
+            "max_seq_len": int(lens.max()),
+            "visible_pairs": pairs,
+            "op": "prefill",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "prefill (plan + attention kernel, one call)",
+            "achieved": round(achieved, 2),
+            "peak": MFMA_BF16_PEAK_TFS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4),
+            "traffic": None,
+            "algorithmic_flops_per_call": flops,
+            "call_us": round(call_ms * 1e3, 2),
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline_prefill(pin, args.cpu_budget)
     print(json.dumps(res), flush=True)
 
 

@@ -268,10 +268,69 @@ int pda_paged_kv_append(const void* k_new,
                         const pda_append_problem* problem,
                         hipStream_t stream);
 
+/* Shapes and dtypes of one variable-length prefill (see pda_paged_prefill_attention). */
+typedef struct pda_prefill_problem {
+  int32_t num_seqs;            /* B */
+  int32_t num_tokens;          /* T: packed query rows of q and out */
+  int32_t num_q_heads;         /* Hq */
+  int32_t num_kv_heads;        /* Hkv; G = Hq / Hkv <= 16 */
+  int32_t head_dim;            /* D: 64 or 128 */
+  int32_t block_size;          /* tokens per KV block: 16 */
+  int32_t max_blocks_per_seq;  /* block_table row stride */
+  int64_t num_blocks;          /* NB */
+  int32_t max_seq_len;         /* host bound on seq_lens (0 = max_blocks_per_seq * 16) */
+  int32_t q_dtype;             /* PDA_DTYPE_BF16 */
+  int32_t kv_dtype;            /* PDA_DTYPE_BF16 or PDA_DTYPE_FP8_E4M3 */
+  int32_t out_dtype;           /* PDA_DTYPE_BF16 or PDA_DTYPE_F32 */
+} pda_prefill_problem;
+
+/*
+ * Causal attention of many query tokens per sequence over the paged cache,
+ * enqueued on `stream`: the log-prob forward of RLVR training (the
+ * compute_log_prob phase of the paper's Sec. 6.2 breakdown, a forward call of
+ * its Sec. 3 interface) and chunked prefill. The cache already holds every
+ * token's key and value (pda_paged_kv_append, or the caller's own writes).
+ *
+ *   q            [T, Hq, D] bf16: rows q_offsets[b] .. q_offsets[b+1]-1 are the
+ *                last n_b = q_offsets[b+1] - q_offsets[b] tokens of sequence b
+ *   q_offsets    [B + 1] int32 device, non-decreasing, q_offsets[0] >= 0,
+ *                q_offsets[B] <= T
+ *   k_cache, v_cache, block_table, seq_lens, kv_scales: as for
+ *                pda_paged_decode_attention (seq_lens[b] = L_b, all cached tokens)
+ *   out          [T, Hq, D] out_dtype; rows outside every sequence are not written
+ *
+ * Query token i of sequence b sits at position L_b - n_b + i and attends to
+ * tokens 0 .. L_b - n_b + i of its sequence (softmax_scale on the logits, KV
+ * head h / G); a token at a negative position (n_b > L_b) gets zeros. Every
+ * output row is computed by one workgroup with no split of the keys, so the
+ * result does not depend on the launch order.
+ *
+ * Device-checked: lengths are clamped as in decode (status bit 1), block-table
+ * entries outside [0, num_blocks) are skipped (bit 2), and offsets that are not
+ * non-decreasing within [0, T] make the call write nothing (bit 8).
+ *
+ * Errors: all checks run on the host before any HIP call: PDA_EINVAL for bad
+ * sizes, dtypes or NULL pointers; PDA_EUNSUPPORTED for head_dim not in {64,
+ * 128}, block_size != 16, G > 16, or an f32 cache. Uses the stream's
+ * workspace (16 bytes per work item of 256 / G query tokens).
+ */
+int pda_paged_prefill_attention(const void* q,
+                                const int32_t* q_offsets,
+                                const void* k_cache,
+                                const void* v_cache,
+                                const int32_t* block_table,
+                                const int32_t* seq_lens,
+                                const float* kv_scales,
+                                void* out,
+                                float softmax_scale,
+                                const pda_prefill_problem* problem,
+                                hipStream_t stream);
+
 /* Wait for `stream`, then return (and clear) the device-side status bits that
  * calls on it recorded: 1 = a sequence length was clamped, 2 = a block-table
  * entry outside [0, num_blocks) was skipped, 4 = a group's members share fewer
- * leading blocks than shared_blocks declared. 0 when clean; negative on error. */
+ * leading blocks than shared_blocks declared, 8 = prefill q_offsets were not
+ * non-decreasing within [0, T]. 0 when clean; negative on error. */
 int pda_read_device_status(hipStream_t stream);
 
 /* Free every workspace the library holds (waits for the owning streams). */

@@ -1,7 +1,7 @@
 """ctypes binding of the C interface in include/pda.h.
 
-Argument marshalling only: every step of the decode-attention computation runs
-in the HIP library ``libpda.so``. Importing this module fails loudly when the
+Argument marshalling only: every step of the decode attention, KV append and
+prefill runs in the HIP library ``libpda.so``. Importing this module fails loudly when the
 library has not been built; there is no fallback.
 
 torch is used for device memory and streams: tensors provide device pointers
@@ -40,7 +40,7 @@ F32, BF16, FP8_E4M3 = 0, 1, 2
 OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM = 0, -1, -2, -3, -4
 VARIANT_AUTO, VARIANT_VECTOR, VARIANT_MFMA = 0, 1, 2
 _VARIANTS = {"auto": VARIANT_AUTO, "vector": VARIANT_VECTOR, "mfma": VARIANT_MFMA}
-STATUS_LEN_CLAMPED, STATUS_BAD_BLOCK = 1, 2
+STATUS_LEN_CLAMPED, STATUS_BAD_BLOCK, STATUS_PREFIX_SHORTENED, STATUS_BAD_OFFSETS = 1, 2, 4, 8
 
 
 class Problem(ctypes.Structure):
@@ -93,6 +93,23 @@ class AppendProblem(ctypes.Structure):
     ]
 
 
+class PrefillProblem(ctypes.Structure):
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32),
+        ("num_tokens", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("max_blocks_per_seq", ctypes.c_int32),
+        ("num_blocks", ctypes.c_int64),
+        ("max_seq_len", ctypes.c_int32),
+        ("q_dtype", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+        ("out_dtype", ctypes.c_int32),
+    ]
+
+
 _vp = ctypes.c_void_p
 _lib.pda_paged_decode_attention.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_float,
                                             ctypes.POINTER(Problem), ctypes.POINTER(Options), _vp]
@@ -109,6 +126,9 @@ _lib.pda_query_plan_shared_prefix.argtypes = [ctypes.POINTER(Problem), ctypes.PO
 _lib.pda_query_plan_shared_prefix.restype = ctypes.c_int
 _lib.pda_paged_kv_append.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.POINTER(AppendProblem), _vp]
 _lib.pda_paged_kv_append.restype = ctypes.c_int
+_lib.pda_paged_prefill_attention.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_float,
+                                             ctypes.POINTER(PrefillProblem), _vp]
+_lib.pda_paged_prefill_attention.restype = ctypes.c_int
 _lib.pda_read_device_status.argtypes = [_vp]
 _lib.pda_read_device_status.restype = ctypes.c_int
 _lib.pda_release_workspaces.argtypes = []
@@ -175,6 +195,13 @@ def raw_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, positi
     """pda_paged_kv_append with integer pointers; returns the status code."""
     return _lib.pda_paged_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, positions,
                                     ctypes.byref(problem), stream)
+
+
+def raw_prefill(q, q_offsets, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale,
+                problem: PrefillProblem, stream=None) -> int:
+    """pda_paged_prefill_attention with integer pointers; returns the status code."""
+    return _lib.pda_paged_prefill_attention(q, q_offsets, k_cache, v_cache, block_table, seq_lens, kv_scales, out,
+                                            ctypes.c_float(softmax_scale), ctypes.byref(problem), stream)
 
 
 def query_plan_shared_prefix(problem: Problem, group_size: int, options: Options | None = None,
@@ -355,6 +382,59 @@ def paged_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, posi
                            kv_scales.data_ptr() if kv_scales is not None else None, block_table.data_ptr(),
                            positions.data_ptr(), prob, _stream_handle(stream, dev))
     _check(rc)
+
+
+def paged_prefill_attention(q, q_offsets, k_cache, v_cache, block_table, seq_lens, kv_scales, out,
+                            softmax_scale, max_seq_len=0, stream=None):
+    """Enqueue the causal attention of packed query tokens over the paged cache.
+
+    q and out are [T, Hq, D] (q bfloat16; out bfloat16 or float32); rows
+    q_offsets[b] .. q_offsets[b + 1] - 1 (int32 [B + 1]) are the last tokens of
+    sequence b, whose cache holds seq_lens[b] tokens; cache layouts as for
+    paged_decode_attention.
+    """
+    torch = _torch()
+    tensors = {"q": q, "q_offsets": q_offsets, "k_cache": k_cache, "v_cache": v_cache,
+               "block_table": block_table, "seq_lens": seq_lens, "out": out}
+    if kv_scales is not None:
+        tensors["kv_scales"] = kv_scales
+    dev = q.device
+    for name, t in tensors.items():
+        if not t.is_cuda or t.device != dev:
+            raise ValueError(f"{name} must be on {dev}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if q.dim() != 3:
+        raise ValueError("q must be [num_tokens, num_q_heads, head_dim]")
+    T, hq, d = q.shape
+    if k_cache.dim() != 4 or v_cache.dim() != 4:
+        raise ValueError("k_cache must be [NB, Hkv, 16, D] and v_cache [NB, Hkv, D, 16]")
+    nb, hkv, bs, dk = k_cache.shape
+    if tuple(v_cache.shape) != (nb, hkv, dk, bs) or dk != d:
+        raise ValueError("cache shapes must be k [NB, Hkv, 16, D], v [NB, Hkv, D, 16] with q's D")
+    if block_table.dim() != 2 or seq_lens.dim() != 1 or block_table.shape[0] != seq_lens.shape[0]:
+        raise ValueError("block_table must be [num_seqs, max_blocks_per_seq] and seq_lens [num_seqs]")
+    B = seq_lens.shape[0]
+    if q_offsets.shape != (B + 1,):
+        raise ValueError("q_offsets must be [num_seqs + 1]")
+    if any(t.dtype != torch.int32 for t in (q_offsets, block_table, seq_lens)):
+        raise TypeError("q_offsets, block_table and seq_lens must be int32")
+    if out.shape != q.shape:
+        raise ValueError("out must have q's shape")
+    kv_dt = _dtype_code(k_cache, "k_cache")
+    if _dtype_code(v_cache, "v_cache") != kv_dt:
+        raise TypeError("k_cache and v_cache dtypes differ")
+    if kv_scales is not None and (tuple(kv_scales.shape) != (2, nb, hkv) or kv_scales.dtype != torch.float32):
+        raise ValueError("kv_scales must be float32 [2, num_blocks, num_kv_heads]")
+    prob = PrefillProblem(B, T, hq, hkv, d, bs, block_table.shape[1], nb, int(max_seq_len),
+                          _dtype_code(q, "q"), kv_dt, _dtype_code(out, "out"))
+    with torch.cuda.device(dev):
+        rc = raw_prefill(q.data_ptr(), q_offsets.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                         block_table.data_ptr(), seq_lens.data_ptr(),
+                         kv_scales.data_ptr() if kv_scales is not None else None, out.data_ptr(),
+                         float(softmax_scale), prob, _stream_handle(stream, dev))
+    _check(rc)
+    return out
 
 
 def read_device_status(stream=None, device=None) -> int:

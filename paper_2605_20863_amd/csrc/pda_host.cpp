@@ -1,6 +1,7 @@
 // Host side of the C interface in include/pda.h: argument validation (pure
 // host code, no HIP call), the launch plan, the per-(device, stream)
-// workspace and the two kernel launches of one decode step.
+// workspace and the kernel launches of a decode step, a KV append and a
+// prefill.
 
 #include "pda.h"
 #include "pda_internal.h"
@@ -485,6 +486,103 @@ int append_run(const void* k_new, const void* v_new, void* k_cache, void* v_cach
   return PDA_OK;
 }
 
+int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, const void* v_cache,
+                const int32_t* block_table, const int32_t* seq_lens, const float* kv_scales, void* out,
+                float softmax_scale, const pda_prefill_problem* pr, hipStream_t stream) {
+  g_error.clear();
+  if (!pr) return fail(PDA_EINVAL, "problem is NULL");
+  if (pr->num_seqs < 0) return fail(PDA_EINVAL, "num_seqs = %d < 0", pr->num_seqs);
+  if (pr->num_tokens < 0) return fail(PDA_EINVAL, "num_tokens = %d < 0", pr->num_tokens);
+  if (pr->num_q_heads < 1 || pr->num_kv_heads < 1)
+    return fail(PDA_EINVAL, "num_q_heads = %d and num_kv_heads = %d must be >= 1", pr->num_q_heads,
+                pr->num_kv_heads);
+  if (pr->num_q_heads % pr->num_kv_heads)
+    return fail(PDA_EINVAL, "num_q_heads = %d is not a multiple of num_kv_heads = %d", pr->num_q_heads,
+                pr->num_kv_heads);
+  const int G = pr->num_q_heads / pr->num_kv_heads;
+  if (G > pda::kMaxGroup)
+    return fail(PDA_EUNSUPPORTED, "GQA group of %d query heads per KV head (max %d)", G, pda::kMaxGroup);
+  if (pr->head_dim != 64 && pr->head_dim != 128)
+    return fail(PDA_EUNSUPPORTED, "head_dim = %d (supported: 64, 128)", pr->head_dim);
+  if (pr->block_size != pda::kBlockSize)
+    return fail(PDA_EUNSUPPORTED, "block_size = %d (supported: 16)", pr->block_size);
+  if (pr->max_blocks_per_seq < 1) return fail(PDA_EINVAL, "max_blocks_per_seq = %d < 1", pr->max_blocks_per_seq);
+  if (pr->num_blocks < 1) return fail(PDA_EINVAL, "num_blocks = %lld < 1", (long long)pr->num_blocks);
+  const int64_t table_tokens = (int64_t)pr->max_blocks_per_seq * pda::kBlockSize;
+  if (table_tokens > INT32_MAX) return fail(PDA_EINVAL, "max_blocks_per_seq * 16 overflows int32");
+  if ((int64_t)pr->num_seqs * pr->max_blocks_per_seq > INT32_MAX)
+    return fail(PDA_EINVAL, "num_seqs * max_blocks_per_seq overflows int32");
+  if ((int64_t)pr->num_tokens * pr->num_q_heads > INT32_MAX)
+    return fail(PDA_EINVAL, "num_tokens * num_q_heads overflows int32");
+  if (pr->max_seq_len < 0) return fail(PDA_EINVAL, "max_seq_len = %d < 0", pr->max_seq_len);
+  if (pr->max_seq_len > table_tokens)
+    return fail(PDA_EINVAL, "max_seq_len = %d exceeds max_blocks_per_seq * 16 = %lld", pr->max_seq_len,
+                (long long)table_tokens);
+  const int64_t tile = (int64_t)pda::kBlockSize * pr->head_dim * 4;
+  if (pr->num_blocks > INT64_MAX / pr->num_kv_heads / tile) return fail(PDA_EINVAL, "num_blocks too large");
+  if (pr->q_dtype != PDA_DTYPE_BF16)
+    return fail(pr->q_dtype == PDA_DTYPE_F32 ? PDA_EUNSUPPORTED : PDA_EINVAL, "q_dtype = %d (supported: BF16)",
+                pr->q_dtype);
+  const int kd = pr->kv_dtype;
+  if (kd == PDA_DTYPE_F32) return fail(PDA_EUNSUPPORTED, "prefill runs on the matrix cores: it needs a bf16 or fp8 cache");
+  if (kd != PDA_DTYPE_BF16 && kd != PDA_DTYPE_FP8_E4M3) return fail(PDA_EINVAL, "kv_dtype = %d is not a pda_dtype", kd);
+  if (pr->out_dtype != PDA_DTYPE_BF16 && pr->out_dtype != PDA_DTYPE_F32)
+    return fail(PDA_EINVAL, "out_dtype = %d (must be BF16 or F32)", pr->out_dtype);
+  if (!std::isfinite(softmax_scale)) return fail(PDA_EINVAL, "softmax_scale is not finite");
+  const int TQ = pda::kPfColumns / G;
+  // every sequence's tiles: sum of ceil(n_b / TQ) <= (T + B (TQ - 1)) / TQ
+  const int64_t items_max = ((int64_t)pr->num_tokens + (int64_t)pr->num_seqs * (TQ - 1)) / TQ;
+  if (items_max * pr->num_kv_heads > INT32_MAX) return fail(PDA_EINVAL, "too many work items for one grid");
+  if (pr->num_seqs == 0 || pr->num_tokens == 0) return PDA_OK;
+  if (!q || !q_offsets || !k_cache || !v_cache || !block_table || !seq_lens || !out)
+    return fail(PDA_EINVAL, "a required pointer (q, q_offsets, k_cache, v_cache, block_table, seq_lens, out) is NULL");
+  if (kd == PDA_DTYPE_FP8_E4M3 && !kv_scales) return fail(PDA_EINVAL, "an fp8 KV cache needs kv_scales");
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+  DeviceInfo di;
+  int rc;
+  if ((rc = device_info(dev, &di)) != PDA_OK) return rc;
+  if (!di.ok) return fail(PDA_EUNSUPPORTED, "device %d is %s; this library is built for gfx950", dev, di.arch.c_str());
+  Workspace* ws = workspace_for(dev, stream);
+  std::lock_guard<std::mutex> lk(ws->mu);
+  const int64_t items_off = align_up(pda::kHdrWords * 4);
+  if ((rc = ensure_workspace(ws, items_off + items_max * 16, stream)) != PDA_OK) return rc;
+  char* base = static_cast<char*>(ws->ptr);
+
+  pda::PrefillArgs a;
+  a.q = q;
+  a.q_offsets = q_offsets;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.block_table = block_table;
+  a.seq_lens = seq_lens;
+  a.kv_scales = kv_scales;
+  a.out = out;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.B = pr->num_seqs;
+  a.T = pr->num_tokens;
+  a.Hq = pr->num_q_heads;
+  a.Hkv = pr->num_kv_heads;
+  a.G = G;
+  a.D = pr->head_dim;
+  a.TQ = TQ;
+  a.max_blocks = pr->max_blocks_per_seq;
+  a.num_blocks = pr->num_blocks;
+  a.len_cap = pr->max_seq_len > 0 ? pr->max_seq_len : (int)table_tokens;
+  int shift = 0;
+  while ((a.len_cap >> shift) >= pda::kPfBuckets) ++shift;
+  a.len_shift = shift;
+  a.items_max = (int32_t)items_max;
+  a.out_bf16 = pr->out_dtype == PDA_DTYPE_BF16;
+  a.hdr = reinterpret_cast<int32_t*>(base);
+  a.items = reinterpret_cast<int4*>(base + items_off);
+  const pda::KvType kv = kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8;
+  if ((e = pda::launch_prefill(a, kv, stream)) != hipSuccess) return fail_hip(e, "prefill kernel launch");
+  return PDA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -521,6 +619,14 @@ int pda_paged_decode_attention_shared_prefix(const void* q, const void* k_cache,
                                              hipStream_t stream) {
   return run(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale, &group_size,
              shared_blocks, problem, options, stream);
+}
+
+int pda_paged_prefill_attention(const void* q, const int32_t* q_offsets, const void* k_cache, const void* v_cache,
+                                const int32_t* block_table, const int32_t* seq_lens, const float* kv_scales,
+                                void* out, float softmax_scale, const pda_prefill_problem* problem,
+                                hipStream_t stream) {
+  return prefill_run(q, q_offsets, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale, problem,
+                     stream);
 }
 
 int pda_read_device_status(hipStream_t stream) {

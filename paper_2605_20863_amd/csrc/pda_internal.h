@@ -19,11 +19,13 @@ enum class Variant : int { Vector = 1, Mfma = 2 };
 constexpr int kStatusLenClamped = 1;
 constexpr int kStatusBadBlock = 2;
 constexpr int kStatusPrefixShortened = 4;  // a group's members share fewer leading blocks than declared
+constexpr int kStatusBadOffsets = 8;       // prefill: q_offsets not non-decreasing within [0, T]
 
 // Workspace header words.
 constexpr int kHdrStatus = 0;
 constexpr int kHdrShare = 1;  // block-heads per chunk (decode writes, combine reads)
 constexpr int kHdrNext = 2;   // chunk counter of a dynamic split; zero between calls
+constexpr int kHdrItems = 3;  // prefill: work items the plan kernel listed
 constexpr int kHdrWords = 16;
 
 // Everything one decode step's kernels need. Plain data; passed by value.
@@ -91,6 +93,34 @@ struct AppendArgs {
 };
 
 hipError_t launch_append(const AppendArgs& a, KvType kv, hipStream_t s);
+
+// Variable-length causal prefill (pda_prefill.hip).
+constexpr int kPfColumns = 256;  // query (token, head) columns per workgroup
+constexpr int kPfBuckets = 2048; // length classes of the plan's counting sort
+
+struct PrefillArgs {
+  const void* q;        // [T, Hq, D] bf16
+  const int32_t* q_offsets;  // [B + 1]
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  const float* kv_scales;
+  void* out;            // [T, Hq, D] bf16 or f32
+  float scale_log2;     // softmax_scale * log2(e)
+  int32_t B, T, Hq, Hkv, G, D;
+  int32_t TQ;           // query tokens per tile: kPfColumns / G
+  int32_t max_blocks;
+  int64_t num_blocks;
+  int32_t len_cap;
+  int32_t len_shift;    // sort key: length >> len_shift, below kPfBuckets
+  int32_t items_max;    // bound on the work items: the grid is items_max * Hkv
+  int32_t out_bf16;
+  int32_t* hdr;         // workspace header (status, item count)
+  int4* items;          // [items_max] {sequence, first q row, tokens, first position}
+};
+
+hipError_t launch_prefill(const PrefillArgs& a, KvType kv, hipStream_t s);
 
 // Launchers (pda_kernels.hip). Return hipSuccess or the launch error.
 hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t s);

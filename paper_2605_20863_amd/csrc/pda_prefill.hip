@@ -1,0 +1,506 @@
+// HIP kernels for variable-length causal prefill over the paged KV cache on
+// MI355X (gfx950, CDNA4).
+//
+// The log-prob forward of RLVR training (the compute_log_prob phase of the
+// paper's Sec. 6.2 breakdown; a forward call of its Sec. 3 interface) and
+// chunked prefill attend many query tokens per sequence at once: packed q rows
+// q_offsets[b] .. q_offsets[b+1]-1 are the last n_b of sequence b's L_b cached
+// tokens, and token i (position L_b - n_b + i) sees tokens 0 .. L_b - n_b + i.
+// This is compute-bound: every K and V element is reused by all query columns
+// of a tile, so K and V go through LDS once per workgroup and the products run
+// on the matrix cores.
+//
+// * Plan kernel (one workgroup): per sequence, its tiles of 256 / G query
+//   tokens; sequences sorted by length, longest first (counting sort on the
+//   length), and a work list of (sequence, tile) items, each sequence's last
+//   (heaviest) tile first. Workgroup i of the attention kernel takes item
+//   i / Hkv for KV head i % Hkv: the KV heads of one tile go to consecutive
+//   workgroups, which the dispatcher deals round-robin over the 8 XCDs, so with
+//   8 KV heads each XCD serves one KV head and its L2 holds only that head's
+//   keys and values, read by every tile of the sequence at nearly the same time.
+// * Attention kernel: one workgroup (4 waves) per (item, KV head). Its query
+//   columns are (token, head) pairs, 256 / G tokens times the G query heads of
+//   the KV head; each wave owns 64 columns (4 MFMA N-tiles), so every K or V
+//   operand read from LDS feeds 4 matrix products.
+// * The KV prefix up to the tile's last position is walked two 16-token blocks
+//   (32 keys) at a time. The workgroup loads a pair's K and V tiles and writes
+//   them to one of two LDS buffers while the previous pair is computed from the
+//   other, one barrier per pair. K rows are padded so 16 rows hit distinct
+//   banks; V rows are stored with the two blocks' tokens interleaved in the
+//   order the P^T operand holds them, so each lane reads its 8 keys at once.
+// * Per wave and pair: S^T[32 keys x 64 columns] = K . Q^T on
+//   v_mfma_f32_16x16x32_bf16, online softmax on the accumulators (lazy
+//   rescale), O^T += V^T . P^T with P split into bf16 hi + lo (a bf16 weight
+//   alone is off by up to 2^-8 of itself, which rows with a few keys carry
+//   into the output; hi + lo keeps 16 bits). fp8 tiles are converted to bf16
+//   after the LDS read, the K scale goes on the logits and the V scale on the
+//   weights.
+// * Causal masking selects per column (a key is seen iff it is at or before the
+//   column's position); V rows of keys past the tile's last position are zeroed,
+//   so NaN poison in unused slots never reaches the products. Only pairs that
+//   reach past a wave's first position take the masked path, and a wave skips
+//   the pairs past its last position.
+
+#include "pda_internal.h"
+
+#include <stdint.h>
+
+namespace pda {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kPfWaves = 4;
+constexpr int kPfNT = 4;  // 16-column N-tiles per wave
+constexpr float kNegInf = -__builtin_inff();
+constexpr float kSlack = 8.f;  // lazy-rescale slack (log2 units): weights stay below 2^8
+constexpr int kPlanThreads = 1024;
+static_assert(kPfWaves * kPfNT * 16 == kPfColumns, "columns per workgroup");
+static_assert(kPfBuckets % kPlanThreads == 0, "buckets per plan thread");
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ u32x2 fp8x4_to_bf16x4(uint32_t w) {
+  u32x2 r;
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, false));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, true));
+  return r;
+}
+
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// ------------------------------------------------------------------ plan
+
+struct PfSeq {
+  int q0, n, L, tiles, key;
+};
+
+// Sequence b as the plan sees it: lengths are clamped into [0, len_cap]
+// (status bit 1); `bad` is set when its offsets leave [0, T] or decrease. key
+// orders sequences longest first.
+__device__ PfSeq pf_seq(const PrefillArgs& a, int b, int& status, bool& bad) {
+  PfSeq s;
+  const int o0 = a.q_offsets[b], o1 = a.q_offsets[b + 1];
+  s.q0 = o0;
+  s.n = o1 - o0;
+  if (o0 < 0 || o1 > a.T || o1 < o0) {
+    bad = true;
+    s.n = 0;
+  }
+  int L = a.seq_lens[b];
+  if (L > a.len_cap || L < 0) {
+    status |= kStatusLenClamped;
+    L = L < 0 ? 0 : a.len_cap;
+  }
+  s.L = L;
+  s.tiles = (s.n + a.TQ - 1) / a.TQ;
+  const int k = L >> a.len_shift;
+  s.key = kPfBuckets - 1 - (k < kPfBuckets - 1 ? k : kPfBuckets - 1);
+  return s;
+}
+
+// Offsets that are not non-decreasing within [0, T] list no item at all (status
+// bit 8): with them the sequences could overlap and overrun the list. Otherwise
+// the tiles add up to at most (T + B (TQ - 1)) / TQ = items_max.
+__global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PrefillArgs a) {
+  __shared__ int cursor[kPfBuckets];
+  __shared__ int wave_sum[kPlanThreads / 64];
+  const int tid = (int)threadIdx.x;
+  for (int i = tid; i < kPfBuckets; i += kPlanThreads) cursor[i] = 0;
+  __syncthreads();
+  int status = 0;
+  bool bad = false;
+  for (int b = tid; b < a.B; b += kPlanThreads) {
+    const PfSeq s = pf_seq(a, b, status, bad);
+    if (s.tiles) atomicAdd(&cursor[s.key], s.tiles);
+  }
+  if (__syncthreads_or(bad)) {
+    if (tid == 0) {
+      a.hdr[kHdrItems] = 0;
+      atomicOr(a.hdr + kHdrStatus, kStatusBadOffsets);
+    }
+    return;
+  }
+  // exclusive scan of the per-bucket tile counts: bucket starts in the list
+  constexpr int PER = kPfBuckets / kPlanThreads;
+  int v[PER], run = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    v[i] = cursor[tid * PER + i];
+    run += v[i];
+  }
+  int x = run;
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (l >= o) x += y;
+  }
+  if (l == 63) wave_sum[tid >> 6] = x;
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < (tid >> 6); ++w) before += wave_sum[w];
+  int start = before + x - run;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    cursor[tid * PER + i] = start;
+    start += v[i];
+  }
+  if (tid == kPlanThreads - 1) a.hdr[kHdrItems] = start;  // total items
+  __syncthreads();
+  for (int b = tid; b < a.B; b += kPlanThreads) {
+    const PfSeq s = pf_seq(a, b, status, bad);
+    if (!s.tiles) continue;
+    int pos = atomicAdd(&cursor[s.key], s.tiles);
+    for (int t = s.tiles - 1; t >= 0; --t) {  // the last (heaviest) tile first
+      const int t0 = t * a.TQ;
+      const int nt = s.n - t0 < a.TQ ? s.n - t0 : a.TQ;
+      a.items[pos++] = make_int4(b, s.q0 + t0, nt, s.L - s.n + t0);
+    }
+  }
+  if (status) atomicOr(a.hdr + kHdrStatus, status);
+}
+
+// ------------------------------------------------------------- attention
+
+template <KvType KV, int D>
+struct PfCfg {
+  static constexpr int ESZ = KV == KvType::FP8 ? 1 : 2;
+  static constexpr int KSTEPS = D / 32;         // 16x16x32 k-steps over head_dim
+  static constexpr int MT = D / 16;             // 16-row tiles of O^T
+  static constexpr int ROWB = D * ESZ;          // bytes of a K token row (global)
+  static constexpr int KROW = ROWB + 16;        // LDS K row stride: 16 rows on distinct banks
+  static constexpr int VSEG = 4 * ESZ;          // bytes of 4 tokens of one V dim row
+  static constexpr int VROWB = 16 * ESZ;        // bytes of a global V dim row (16 tokens)
+  static constexpr int VROW = 2 * VROWB + 16;   // LDS V row: both blocks' 32 tokens, padded
+  static constexpr int TILEB = 16 * ROWB;       // bytes of one (block, KV head) tile
+  static constexpr int UNITS = 2 * TILEB / 16;  // 16-byte units of a pair's K (or V) tiles
+  static constexpr int UPT = (UNITS + 255) / 256;
+  static constexpr int KBUF = 32 * KROW;
+  static constexpr int BUF = KBUF + D * VROW;
+};
+
+// One pair's global data on its way to LDS (each thread's 16-byte units), and
+// the pair's per-block flags and fp8 scales (workgroup-uniform).
+template <KvType KV, int D>
+struct PfStage {
+  u32x4 k[PfCfg<KV, D>::UPT], v[PfCfg<KV, D>::UPT];
+  int ok[2];  // block holds keys of the tile and its id is in range
+  float ks[2], vs[2];
+};
+
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, const int32_t* row, int j0,
+                                        int nblk, int kvh, int& status) {
+  using C = PfCfg<KV, D>;
+  int64_t tile[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int j = j0 + s;
+    const int p = j < nblk ? row[j] : 0;
+    int ok = j < nblk;
+    if (ok && (unsigned)p >= (uint64_t)a.num_blocks) {
+      status |= kStatusBadBlock;
+      ok = 0;
+    }
+    st.ok[s] = uni(ok);
+    tile[s] = (int64_t)uni(ok ? p : 0) * a.Hkv + kvh;
+    if constexpr (KV == KvType::FP8) {
+      st.ks[s] = ok ? a.kv_scales[tile[s]] : 0.f;
+      st.vs[s] = ok ? a.kv_scales[a.num_blocks * a.Hkv + tile[s]] : 0.f;
+    } else {
+      st.ks[s] = 1.f;
+      st.vs[s] = 1.f;
+    }
+  }
+  const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
+  const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
+#pragma unroll
+  for (int u = 0; u < C::UPT; ++u) {
+    const int unit = (int)threadIdx.x + 256 * u;
+    const int blk = unit / (C::TILEB / 16);
+    const int off = (unit - blk * (C::TILEB / 16)) * 16;
+    const bool live = unit < C::UNITS && st.ok[blk & 1];
+    const int64_t base = tile[blk & 1] * C::TILEB + off;
+    st.k[u] = live ? *reinterpret_cast<const u32x4*>(kc + base) : u32x4{0, 0, 0, 0};
+    st.v[u] = live ? *reinterpret_cast<const u32x4*>(vc + base) : u32x4{0, 0, 0, 0};
+  }
+}
+
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf) {
+  using C = PfCfg<KV, D>;
+#pragma unroll
+  for (int u = 0; u < C::UPT; ++u) {
+    const int unit = (int)threadIdx.x + 256 * u;
+    if (unit >= C::UNITS) break;
+    const int blk = unit / (C::TILEB / 16);
+    const int off = (unit - blk * (C::TILEB / 16)) * 16;
+    const int krow = off / C::ROWB, kcol = off - krow * C::ROWB;
+    *reinterpret_cast<u32x4*>(buf + (blk * 16 + krow) * C::KROW + kcol) = st.k[u];
+    // V: global dim row d, tokens [tok, tok + 16 / ESZ); LDS dim row d holds
+    // segment c = [block 0 tokens 4c..4c+3][block 1 tokens 4c..4c+3]
+    const int d = off / C::VROWB, tok = (off - d * C::VROWB) / C::ESZ;
+    uint8_t* vrow = buf + C::KBUF + d * C::VROW + blk * C::VSEG;
+    if constexpr (KV == KvType::BF16) {
+      const int c = tok / 4;  // 0 or 2
+      *reinterpret_cast<u32x2*>(vrow + c * 2 * C::VSEG) = u32x2{st.v[u].x, st.v[u].y};
+      *reinterpret_cast<u32x2*>(vrow + (c + 1) * 2 * C::VSEG) = u32x2{st.v[u].z, st.v[u].w};
+    } else {
+      *reinterpret_cast<uint32_t*>(vrow + 0 * 2 * C::VSEG) = st.v[u].x;
+      *reinterpret_cast<uint32_t*>(vrow + 1 * 2 * C::VSEG) = st.v[u].y;
+      *reinterpret_cast<uint32_t*>(vrow + 2 * 2 * C::VSEG) = st.v[u].z;
+      *reinterpret_cast<uint32_t*>(vrow + 3 * 2 * C::VSEG) = st.v[u].w;
+    }
+  }
+}
+
+// One pair from LDS for this wave's 64 columns. MASKED: per-column key limits
+// see[n] (keys of the pair the column sees) and the pair's live keys (V rows
+// at or past `live` are zeroed).
+template <KvType KV, int D, bool MASKED>
+__device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
+                                        float c0, float c1, float vs0, float vs1, const int (&see)[kPfNT], int live,
+                                        f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], float (&m_run)[kPfNT],
+                                        float (&l_run)[kPfNT]) {
+  using C = PfCfg<KV, D>;
+  const int l = lane_id();
+  const int r = l & 15, c = l >> 4;
+  f32x4 s0[kPfNT], s1[kPfNT];
+#pragma unroll
+  for (int n = 0; n < kPfNT; ++n) s0[n] = s1[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < C::KSTEPS; ++j) {
+    bf16x8 k0, k1;
+    if constexpr (KV == KvType::BF16) {
+      k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + r * C::KROW + (32 * j + 8 * c) * 2));
+      k1 = __builtin_bit_cast(bf16x8,
+                              *reinterpret_cast<const u32x4*>(buf + (16 + r) * C::KROW + (32 * j + 8 * c) * 2));
+    } else {
+      const u32x2 w0 = *reinterpret_cast<const u32x2*>(buf + r * C::KROW + 32 * j + 8 * c);
+      const u32x2 w1 = *reinterpret_cast<const u32x2*>(buf + (16 + r) * C::KROW + 32 * j + 8 * c);
+      const u32x2 a0 = fp8x4_to_bf16x4(w0.x), b0 = fp8x4_to_bf16x4(w0.y);
+      const u32x2 a1 = fp8x4_to_bf16x4(w1.x), b1 = fp8x4_to_bf16x4(w1.y);
+      k0 = __builtin_bit_cast(bf16x8, u32x4{a0.x, a0.y, b0.x, b0.y});
+      k1 = __builtin_bit_cast(bf16x8, u32x4{a1.x, a1.y, b1.x, b1.y});
+    }
+#pragma unroll
+    for (int n = 0; n < kPfNT; ++n) {
+      s0[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qb[n][j], s0[n], 0, 0, 0);
+      s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qb[n][j], s1[n], 0, 0, 0);
+    }
+  }
+  bf16x8 phi[kPfNT], plo[kPfNT];
+#pragma unroll
+  for (int n = 0; n < kPfNT; ++n) {
+    float x[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[i] = s0[n][i] * c0;
+      x[4 + i] = s1[n][i] * c1;
+      if constexpr (MASKED) {
+        x[i] = 4 * c + i < see[n] ? x[i] : kNegInf;
+        x[4 + i] = 16 + 4 * c + i < see[n] ? x[4 + i] : kNegInf;
+      }
+    }
+    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (__any(mx > m_run[n] + kSlack)) {
+      const float m_new = fmaxf(m_run[n], mx);
+      const float alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run[n] - m_new);
+      m_run[n] = m_new;
+      l_run[n] *= alpha;
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) acc[m][n] *= alpha;
+    }
+    const float m_ref = m_run[n] == kNegInf ? 0.f : m_run[n];
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float p = fast_exp2(x[i] - m_ref);
+      psum += p;
+      if constexpr (KV == KvType::FP8) p *= i < 4 ? vs0 : vs1;
+      const __bf16 h = (__bf16)p;
+      phi[n][i] = h;
+      plo[n][i] = (__bf16)(p - (float)h);
+    }
+    l_run[n] += psum;
+  }
+  uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
+  if constexpr (MASKED) {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {  // word h: keys 16 * (h / 2) + 4c + 2 * (h % 2) + {0, 1}
+      const int k = 16 * (h >> 1) + 4 * c + 2 * (h & 1);
+      mk[h] = (k < live ? 0xFFFFu : 0u) | (k + 1 < live ? 0xFFFF0000u : 0u);
+    }
+  }
+  const uint8_t* vb = buf + C::KBUF;
+#pragma unroll
+  for (int m = 0; m < C::MT; ++m) {
+    const int d = 16 * m + r;
+    u32x4 w;
+    if constexpr (KV == KvType::BF16) {
+      w = *reinterpret_cast<const u32x4*>(vb + d * C::VROW + 16 * c);
+    } else {
+      const u32x2 v = *reinterpret_cast<const u32x2*>(vb + d * C::VROW + 8 * c);
+      const u32x2 a0 = fp8x4_to_bf16x4(v.x), a1 = fp8x4_to_bf16x4(v.y);
+      w = u32x4{a0.x, a0.y, a1.x, a1.y};
+    }
+    if constexpr (MASKED) w = u32x4{w.x & mk[0], w.y & mk[1], w.z & mk[2], w.w & mk[3]};
+    const bf16x8 va = __builtin_bit_cast(bf16x8, w);
+#pragma unroll
+    for (int n = 0; n < kPfNT; ++n) {
+      acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[n], acc[m][n], 0, 0, 0);
+      acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[n], acc[m][n], 0, 0, 0);
+    }
+  }
+}
+
+template <KvType KV, int D>
+__global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
+  using C = PfCfg<KV, D>;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * C::BUF];
+  const int l = lane_id();
+  const int r = l & 15, c = l >> 4;
+  const int w = (int)(threadIdx.x >> 6);
+  const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
+  const int item = (int)(blockIdx.x / (unsigned)a.Hkv);
+  if (item >= a.hdr[kHdrItems]) return;  // the whole workgroup leaves together
+  const int4 it = a.items[item];
+  const int b = it.x, row0 = it.y, nt = it.z, first = it.w;
+
+  // this wave's columns: column col = 64w + 16n + r is token col / G, head col % G
+  int vis[kPfNT], tokq[kPfNT];
+  bf16x8 qb[kPfNT][C::KSTEPS];
+#pragma unroll
+  for (int n = 0; n < kPfNT; ++n) {
+    const int col = 64 * w + 16 * n + r;
+    const int tok = col / a.G, head = col - tok * a.G;
+    const bool ok = tok < nt;
+    vis[n] = first + tok + 1;  // keys the column sees
+    tokq[n] = ok ? ((row0 + tok) * a.Hq + kvh * a.G + head) : -1;
+    const uint16_t* qp = static_cast<const uint16_t*>(a.q) + (int64_t)(ok ? tokq[n] : 0) * D;
+#pragma unroll
+    for (int j = 0; j < C::KSTEPS; ++j) {
+      u32x4 v = {0, 0, 0, 0};
+      if (ok) v = *reinterpret_cast<const u32x4*>(qp + 32 * j + 8 * c);
+      qb[n][j] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  const int tok_lo = 64 * w / a.G;
+  const int tok_hi_raw = (64 * w + 63) / a.G;
+  const int tok_hi = tok_hi_raw < nt - 1 ? tok_hi_raw : nt - 1;
+  const bool wave_on = tok_lo < nt;
+  const int pos_lo = first + tok_lo;  // this wave's first and last query positions
+  const int pos_hi = first + tok_hi;
+
+  const int nkeys = first + nt > 0 ? first + nt : 0;  // keys up to the tile's last position
+  const int npairs = (nkeys + 31) / 32;
+  const int nblk = (nkeys + 15) / 16;
+  const int32_t* row = a.block_table + (int64_t)b * a.max_blocks;
+  int status = 0;
+
+  f32x4 acc[C::MT][kPfNT];
+#pragma unroll
+  for (int m = 0; m < C::MT; ++m)
+#pragma unroll
+    for (int n = 0; n < kPfNT; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[kPfNT], l_run[kPfNT];
+#pragma unroll
+  for (int n = 0; n < kPfNT; ++n) {
+    m_run[n] = kNegInf;
+    l_run[n] = 0.f;
+  }
+
+  PfStage<KV, D> st;
+  if (npairs > 0) {
+    pf_load<KV, D>(st, a, row, 0, nblk, kvh, status);
+    pf_store<KV, D>(st, lds);
+  }
+  __syncthreads();
+  int cur = 0;
+  for (int j2 = 0; j2 < npairs; ++j2) {
+    const float c0 = a.scale_log2 * st.ks[0], c1 = a.scale_log2 * st.ks[1];
+    const float vs0 = st.vs[0], vs1 = st.vs[1];
+    const int ok0 = st.ok[0], ok1 = st.ok[1];
+    if (j2 + 1 < npairs) pf_load<KV, D>(st, a, row, 2 * (j2 + 1), nblk, kvh, status);
+    const int key0 = 32 * j2;
+    if (wave_on && key0 <= pos_hi) {
+      const uint8_t* buf = lds + cur * C::BUF;
+      // keys of the pair that exist for this tile (a skipped block's are dead)
+      int live = nkeys - key0;
+      if (!ok1) live = live < 16 ? live : 16;
+      if (!ok0) live = 0;
+      if (key0 + 31 <= pos_lo && live >= 32) {
+        const int see[kPfNT] = {32, 32, 32, 32};
+        pf_pair<KV, D, false>(buf, qb, c0, c1, vs0, vs1, see, 32, acc, m_run, l_run);
+      } else {
+        int see[kPfNT];
+#pragma unroll
+        for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < live ? vis[n] - key0 : live;
+        pf_pair<KV, D, true>(buf, qb, c0, c1, vs0, vs1, see, live, acc, m_run, l_run);
+      }
+    }
+    if (j2 + 1 < npairs) pf_store<KV, D>(st, lds + (cur ^ 1) * C::BUF);
+    __syncthreads();
+    cur ^= 1;
+  }
+  if (__any(status) && l == 0) atomicOr(a.hdr + kHdrStatus, status);
+  if (!wave_on) return;
+
+#pragma unroll
+  for (int n = 0; n < kPfNT; ++n) {
+    float lt = l_run[n];
+    lt += __shfl_xor(lt, 16, 64);
+    lt += __shfl_xor(lt, 32, 64);
+    if (tokq[n] < 0) continue;
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    if (a.out_bf16) {
+      uint16_t* o = static_cast<uint16_t*>(a.out) + (int64_t)tokq[n] * D;
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) {
+        u32x2 v;
+        v.x = f32_to_bf16_bits(acc[m][n][0] * inv) | (f32_to_bf16_bits(acc[m][n][1] * inv) << 16);
+        v.y = f32_to_bf16_bits(acc[m][n][2] * inv) | (f32_to_bf16_bits(acc[m][n][3] * inv) << 16);
+        *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) = v;
+      }
+    } else {
+      float* o = static_cast<float*>(a.out) + (int64_t)tokq[n] * D;
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m][n] * inv;
+    }
+  }
+}
+
+template <KvType KV>
+void* prefill_for_d(int D) {
+  return D == 64 ? reinterpret_cast<void*>(&prefill_kernel<KV, 64>)
+                 : reinterpret_cast<void*>(&prefill_kernel<KV, 128>);
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const PrefillArgs& a, KvType kv, hipStream_t s) {
+  if (a.B == 0 || a.items_max == 0) return hipSuccess;
+  PrefillArgs args = a;
+  void* params[] = {&args};
+  hipError_t e = hipLaunchKernel(reinterpret_cast<void*>(&prefill_plan_kernel), dim3(1), dim3(kPlanThreads), params,
+                                 0, s);
+  if (e != hipSuccess) return e;
+  void* fn = kv == KvType::FP8 ? prefill_for_d<KvType::FP8>(a.D) : prefill_for_d<KvType::BF16>(a.D);
+  const int64_t wgs = (int64_t)a.items_max * a.Hkv;
+  return hipLaunchKernel(fn, dim3((unsigned)wgs), dim3(64 * kPfWaves), params, 0, s);
+}
+
+}  // namespace pda

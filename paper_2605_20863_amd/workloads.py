@@ -1,8 +1,8 @@
-"""Seeded synthetic decode-step inputs.
+"""Seeded synthetic decode-step and prefill inputs.
 
 This module draws the inputs of one batched paged-KV decode step: sequence
 lengths, block tables, queries and the paged K/V cache (with fp8 encoding and
-scales where asked). It holds none of the attention arithmetic; both the HIP
+scales where asked), and the packed queries of a prefill over such a cache. It holds none of the attention arithmetic; both the HIP
 path and the CPU oracle consume what it produces.
 
 The paper's workload (a proprietary maths dataset decoded by Qwen2.5-7B,
@@ -63,6 +63,9 @@ class Workload:
     cfg_id: int
     block_size: int = BLOCK_SIZE
     q_tokens: int = 1      # query tokens per sequence (> 1: q is [B, q_tokens, Hq, D])
+    # > 0: a prefill (log-prob forward) whose sequence b has n_b =
+    # clip(rint(prefill_frac * L_b), 1, L_b) packed query tokens, its last n_b
+    prefill_frac: float = 0.0
 
     @property
     def group(self) -> int:
@@ -96,6 +99,11 @@ WORKLOADS = {
     # responses): the shape where reading shared blocks once matters most.
     "grpo_longprompt_bf16": Workload("grpo_longprompt_bf16", 256, 32, 8, 128, "bf16", "bf16",
                                      ("grpo", 32, 8, 3072, 6144, 1024, 0.8, 8192), cfg_id=5),
+    # Log-prob forward (the compute_log_prob phase) over the 7B GQA step's 64
+    # sequences: every token of every sequence is a query, causal over its
+    # sequence (~180k packed tokens).
+    "logprob_gqa7b_bf16": Workload("logprob_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
+                                   ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, prefill_frac=1.0),
     # Speculative verification on the 7B GQA step: 2 query tokens per sequence
     # (the drafted one and the next), 14 of the 16 MFMA columns.
     "spec2_gqa7b_bf16": Workload("spec2_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
@@ -236,6 +244,13 @@ def group_prefix(w: Workload, layout: Layout):
     return samples, (layout.prompt_lens[::samples] // w.block_size).astype(np.int32)
 
 
+def prefill_counts(w: Workload, seq_lens) -> np.ndarray:
+    """Query tokens per sequence of a prefill workload: its last n_b tokens."""
+    L = np.asarray(seq_lens, dtype=np.int64)
+    n = np.clip(np.rint(w.prefill_frac * L), 1, np.maximum(L, 1))
+    return np.where(L > 0, n, 0).astype(np.int32)
+
+
 @dataclasses.dataclass
 class DecodeInputs:
     """Device tensors of one decode step plus its host-side layout."""
@@ -350,3 +365,33 @@ def generate(w: Workload, device="cpu", seq_lens=None, q_scale: float = 1.0) -> 
         kv_scales=kv_scales,
         softmax_scale=w.softmax_scale,
     )
+
+
+@dataclasses.dataclass
+class PrefillInputs:
+    """Packed queries of a prefill over the paged cache of ``cache``."""
+
+    cache: DecodeInputs           # the paged cache, block table and lengths (its q is unused)
+    q: torch.Tensor               # [T, Hq, D] bfloat16
+    q_offsets: torch.Tensor       # [B + 1] int32 on the device
+    offsets: np.ndarray           # the same offsets on the host
+    counts: np.ndarray            # [B] query tokens per sequence
+
+
+def generate_prefill(w: Workload, device="cpu", seq_lens=None, q_counts=None, q_scale: float = 1.0) -> PrefillInputs:
+    """Draw a prefill of workload ``w``: the paged cache as ``generate`` draws
+    it, and for sequence b the queries of its last ``q_counts[b]`` tokens
+    (default ``prefill_counts``), packed in sequence order, i.i.d. N(0, 1)
+    times ``q_scale``, rounded to bf16."""
+    cache = generate(w, device, seq_lens=seq_lens)
+    lens = cache.layout.seq_lens
+    counts = prefill_counts(w, lens) if q_counts is None else np.asarray(q_counts, dtype=np.int32)
+    if counts.shape != lens.shape:
+        raise ValueError("q_counts needs one entry per sequence")
+    offsets = np.concatenate([[0], np.cumsum(counts, dtype=np.int64)]).astype(np.int32)
+    T = int(offsets[-1])
+    device = torch.device(device)
+    g = torch.Generator(device=device).manual_seed(_torch_seed(w, _STREAM_Q, 1))
+    q = (torch.randn((T, w.num_q_heads, w.head_dim), generator=g, device=device, dtype=torch.float32) * q_scale)
+    return PrefillInputs(cache=cache, q=q.to(torch.bfloat16), q_offsets=torch.from_numpy(offsets).to(device),
+                         offsets=offsets, counts=counts)

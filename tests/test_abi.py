@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     assert set(declared) == {"pda_paged_decode_attention", "pda_query_plan", "pda_read_device_status",
                              "pda_release_workspaces", "pda_last_error", "pda_version",
                              "pda_paged_decode_attention_shared_prefix", "pda_query_plan_shared_prefix",
-                             "pda_paged_kv_append"}
+                             "pda_paged_kv_append", "pda_paged_prefill_attention"}
     for name in declared:
         assert hasattr(L._lib, name), name
     nm = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True).stdout
@@ -51,6 +51,8 @@ def test_struct_layout_matches_header(tmp_path):
 int main(void) {
   printf("pda_problem %zu\npda_options %zu\npda_plan_info %zu\npda_append_problem %zu\n",
          sizeof(pda_problem), sizeof(pda_options), sizeof(pda_plan_info), sizeof(pda_append_problem));
+  printf("pda_prefill_problem %zu\n", sizeof(pda_prefill_problem));
+  F(pda_prefill_problem, num_blocks); F(pda_prefill_problem, max_seq_len); F(pda_prefill_problem, out_dtype);
   F(pda_append_problem, num_blocks); F(pda_append_problem, kv_dtype);
   F(pda_problem, num_blocks); F(pda_problem, max_seq_len); F(pda_problem, out_dtype);
   F(pda_options, min_blocks_per_wave); F(pda_options, chunks_per_wave); F(pda_options, min_blocks_per_chunk);
@@ -69,6 +71,9 @@ int main(void) {
     assert int(got["pda_options"]) == ctypes.sizeof(L.Options)
     assert int(got["pda_plan_info"]) == ctypes.sizeof(L.PlanInfo)
     assert int(got["pda_append_problem"]) == ctypes.sizeof(L.AppendProblem)
+    assert int(got["pda_prefill_problem"]) == ctypes.sizeof(L.PrefillProblem)
+    for m in ("num_blocks", "max_seq_len", "out_dtype"):
+        assert int(got[f"pda_prefill_problem.{m}"]) == getattr(L.PrefillProblem, m).offset, m
     assert int(got["pda_append_problem.num_blocks"]) == L.AppendProblem.num_blocks.offset
     assert int(got["pda_append_problem.kv_dtype"]) == L.AppendProblem.kv_dtype.offset
     assert int(got["pda_problem.num_blocks"]) == L.Problem.num_blocks.offset
@@ -251,3 +256,43 @@ def test_multi_token_checks_and_plan():
     slots = 64 * 4 + info.chunks_max
     up = lambda x: (x + 255) // 256 * 256
     assert info.workspace_bytes == up(64) + up(64 * 4) + 2 * up(slots * 8 * 4) + up(slots * 8 * 128 * 4)
+
+
+def pprob(**kw):
+    base = dict(num_seqs=4, num_tokens=100, num_q_heads=8, num_kv_heads=2, head_dim=128, block_size=16,
+                max_blocks_per_seq=8, num_blocks=64, max_seq_len=0, q_dtype=L.BF16, kv_dtype=L.BF16,
+                out_dtype=L.BF16)
+    base.update(kw)
+    return L.PrefillProblem(**base)
+
+
+def test_prefill_argument_checks():
+    ok_ptrs = [16] * 8
+    call = lambda pr, ptrs=ok_ptrs, scale=0.1: L.raw_prefill(*ptrs[:7], ptrs[7], scale, pr)
+    assert call(pprob(num_seqs=-1)) == L.EINVAL
+    assert call(pprob(num_tokens=-1)) == L.EINVAL
+    assert call(pprob(num_kv_heads=3)) == L.EINVAL              # 8 % 3
+    assert call(pprob(num_q_heads=34, num_kv_heads=2)) == L.EUNSUPPORTED   # G = 17
+    assert call(pprob(head_dim=96)) == L.EUNSUPPORTED
+    assert call(pprob(block_size=32)) == L.EUNSUPPORTED
+    assert call(pprob(max_blocks_per_seq=0)) == L.EINVAL
+    assert call(pprob(num_blocks=0)) == L.EINVAL
+    assert call(pprob(max_seq_len=8 * 16 + 1)) == L.EINVAL
+    assert call(pprob(q_dtype=L.F32)) == L.EUNSUPPORTED
+    assert call(pprob(q_dtype=L.FP8_E4M3)) == L.EINVAL
+    assert call(pprob(kv_dtype=L.F32)) == L.EUNSUPPORTED
+    assert call(pprob(kv_dtype=5)) == L.EINVAL
+    assert call(pprob(out_dtype=L.FP8_E4M3)) == L.EINVAL
+    assert call(pprob(), scale=math.inf) == L.EINVAL
+    assert call(pprob(num_tokens=2 ** 30, num_q_heads=8)) == L.EINVAL   # T * Hq overflows int32
+    for i in range(8):
+        ptrs = list(ok_ptrs)
+        ptrs[i] = None
+        # kv_scales (index 6) is optional for a bf16 cache, required for fp8
+        want = L.OK if i == 6 else L.EINVAL
+        if want == L.OK:
+            assert call(pprob(kv_dtype=L.FP8_E4M3), ptrs) == L.EINVAL
+        else:
+            assert call(pprob(), ptrs) == L.EINVAL, i
+    assert call(pprob(num_seqs=0), [None] * 8) == L.OK      # empty batch: no-op
+    assert call(pprob(num_tokens=0), [None] * 8) == L.OK    # no query rows: no-op
