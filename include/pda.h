@@ -305,6 +305,11 @@ typedef struct pda_prefill_problem {
  * output row is computed by one workgroup with no split of the keys, so the
  * result does not depend on the launch order.
  *
+ * Precision: q . k in bf16 products with fp32 sums; the softmax weights (at
+ * most 2^8 after the running-max shift) and V (fp8: code times V scale) enter
+ * the P . V product as fp16 (11 significant bits; bf16 V converts exactly),
+ * accumulated in fp32. A live V value beyond +-65504 saturates (status bit 16).
+ *
  * Device-checked: lengths are clamped as in decode (status bit 1), block-table
  * entries outside [0, num_blocks) are skipped (bit 2), and offsets that are not
  * non-decreasing within [0, T] make the call write nothing (bit 8).
@@ -330,7 +335,8 @@ int pda_paged_prefill_attention(const void* q,
  * calls on it recorded: 1 = a sequence length was clamped, 2 = a block-table
  * entry outside [0, num_blocks) was skipped, 4 = a group's members share fewer
  * leading blocks than shared_blocks declared, 8 = prefill q_offsets were not
- * non-decreasing within [0, T]. 0 when clean; negative on error. */
+ * non-decreasing within [0, T], 16 = a prefill V value outside the fp16 range
+ * saturated. 0 when clean; negative on error. */
 int pda_read_device_status(hipStream_t stream);
 
 /* Free every workspace the library holds (waits for the owning streams). */

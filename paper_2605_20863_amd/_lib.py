@@ -41,6 +41,7 @@ OK, EINVAL, EUNSUPPORTED, EHIP, ENOMEM = 0, -1, -2, -3, -4
 VARIANT_AUTO, VARIANT_VECTOR, VARIANT_MFMA = 0, 1, 2
 _VARIANTS = {"auto": VARIANT_AUTO, "vector": VARIANT_VECTOR, "mfma": VARIANT_MFMA}
 STATUS_LEN_CLAMPED, STATUS_BAD_BLOCK, STATUS_PREFIX_SHORTENED, STATUS_BAD_OFFSETS = 1, 2, 4, 8
+STATUS_HALF_RANGE = 16
 
 
 class Problem(ctypes.Structure):

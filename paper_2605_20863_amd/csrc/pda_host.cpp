@@ -560,7 +560,8 @@ int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, co
   a.seq_lens = seq_lens;
   a.kv_scales = kv_scales;
   a.out = out;
-  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.scale_log2 = std::fabs(softmax_scale) * 1.4426950408889634f;
+  a.neg_scale = softmax_scale < 0.f;
   a.B = pr->num_seqs;
   a.T = pr->num_tokens;
   a.Hq = pr->num_q_heads;

@@ -20,6 +20,7 @@ constexpr int kStatusLenClamped = 1;
 constexpr int kStatusBadBlock = 2;
 constexpr int kStatusPrefixShortened = 4;  // a group's members share fewer leading blocks than declared
 constexpr int kStatusBadOffsets = 8;       // prefill: q_offsets not non-decreasing within [0, T]
+constexpr int kStatusHalfRange = 16;       // prefill: a V value outside the fp16 range was saturated
 
 // Workspace header words.
 constexpr int kHdrStatus = 0;
@@ -107,7 +108,8 @@ struct PrefillArgs {
   const int32_t* seq_lens;
   const float* kv_scales;
   void* out;            // [T, Hq, D] bf16 or f32
-  float scale_log2;     // softmax_scale * log2(e)
+  float scale_log2;     // |softmax_scale| * log2(e)
+  int32_t neg_scale;    // 1: softmax_scale < 0 (q enters with its sign flipped)
   int32_t B, T, Hq, Hkv, G, D;
   int32_t TQ;           // query tokens per tile: kPfColumns / G
   int32_t max_blocks;

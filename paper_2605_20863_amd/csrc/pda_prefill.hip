@@ -52,9 +52,14 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kPfWaves = 4;
-constexpr int kPfNT = 4;  // 16-column N-tiles per wave
+constexpr int kPfWaves = 8;
+constexpr int kPfThreads = 64 * kPfWaves;
+constexpr int kPfNT = 2;                // 16-column N-tiles per wave
+constexpr int kPfWaveCols = 16 * kPfNT; // query columns per wave
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kSlack = 8.f;  // lazy-rescale slack (log2 units): weights stay below 2^8
 constexpr int kPlanThreads = 1024;
@@ -70,6 +75,22 @@ __device__ __forceinline__ u32x2 fp8x4_to_bf16x4(uint32_t w) {
   r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, false));
   r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, true));
   return r;
+}
+
+// codes 0, 1 (HI false) or 2, 3 (HI true) of a word of four E4M3 codes, times
+// scale (the conversion's own scale operand is a power-of-two exponent, so the
+// tile scale is applied in fp32 afterwards)
+template <bool HI>
+__device__ __forceinline__ float2 fp8x2_to_f32x2(uint32_t w, float scale) {
+  const f32x2 v = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8((int)w, 1.0f, HI);
+  return float2{v.x * scale, v.y * scale};
+}
+
+__device__ __forceinline__ uint32_t pk_f16(float x, float y) {
+  f16x2 h;
+  h[0] = (_Float16)x;
+  h[1] = (_Float16)y;
+  return __builtin_bit_cast(uint32_t, h);
 }
 
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
@@ -173,104 +194,149 @@ __global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PrefillArgs 
 
 // ------------------------------------------------------------- attention
 
+// LDS layout of one pair (two 16-token blocks of one KV head), the same for
+// bf16 and fp8 caches (fp8 tiles are decoded while they are staged, once per
+// workgroup rather than once per wave):
+//   K  [32 keys][D] bf16 (fp8: the codes, exact in bf16), rows padded by 16 B
+//   V  [D][32 keys] fp16 (fp8: code * V scale), per dim row the segments
+//      c = 0..3 hold [block 0 tokens 4c..4c+3][block 1 tokens 4c..4c+3],
+//      the order in which a lane's P^T operand holds its 8 keys
 template <KvType KV, int D>
 struct PfCfg {
-  static constexpr int ESZ = KV == KvType::FP8 ? 1 : 2;
-  static constexpr int KSTEPS = D / 32;         // 16x16x32 k-steps over head_dim
-  static constexpr int MT = D / 16;             // 16-row tiles of O^T
-  static constexpr int ROWB = D * ESZ;          // bytes of a K token row (global)
-  static constexpr int KROW = ROWB + 16;        // LDS K row stride: 16 rows on distinct banks
-  static constexpr int VSEG = 4 * ESZ;          // bytes of 4 tokens of one V dim row
-  static constexpr int VROWB = 16 * ESZ;        // bytes of a global V dim row (16 tokens)
-  static constexpr int VROW = 2 * VROWB + 16;   // LDS V row: both blocks' 32 tokens, padded
-  static constexpr int TILEB = 16 * ROWB;       // bytes of one (block, KV head) tile
-  static constexpr int UNITS = 2 * TILEB / 16;  // 16-byte units of a pair's K (or V) tiles
-  static constexpr int UPT = (UNITS + 255) / 256;
+  static constexpr int GSZ = KV == KvType::FP8 ? 1 : 2;  // bytes per cached element
+  static constexpr int KSTEPS = D / 32;                 // 16x16x32 k-steps over head_dim
+  static constexpr int MT = D / 16;                     // 16-row tiles of O^T
+  static constexpr int GROW = D * GSZ;                  // bytes of a cached K token row
+  static constexpr int GVROW = 16 * GSZ;                // bytes of a cached V dim row (16 tokens)
+  static constexpr int TILEB = 16 * GROW;               // bytes of one cached (block, KV head) tile
+  static constexpr int UNITS = 2 * TILEB / 16;          // 16-byte units of a pair's K (or V) tiles
+  static constexpr int UPT = (UNITS + kPfThreads - 1) / kPfThreads;
+  static constexpr int KROW = 2 * D + 16;               // LDS K row stride: 16 rows on distinct banks
+  static constexpr int VROW = 64 + 16;                  // LDS V row stride (32 fp16 keys + pad)
   static constexpr int KBUF = 32 * KROW;
   static constexpr int BUF = KBUF + D * VROW;
 };
 
-// One pair's global data on its way to LDS (each thread's 16-byte units), and
-// the pair's per-block flags and fp8 scales (workgroup-uniform).
+// One pair on its way to LDS: each thread's 16-byte units of the cached K and
+// V tiles, and the pair's workgroup-uniform block flags, scales and live keys.
 template <KvType KV, int D>
 struct PfStage {
   u32x4 k[PfCfg<KV, D>::UPT], v[PfCfg<KV, D>::UPT];
-  int ok[2];  // block holds keys of the tile and its id is in range
+  int ok0, ok1;   // block holds keys of the tile and its id is in range
+  int live;       // keys of the pair that exist (from the pair's first key)
   float ks[2], vs[2];
 };
 
 template <KvType KV, int D>
 __device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, const int32_t* row, int j0,
-                                        int nblk, int kvh, int& status) {
+                                        int nblk, int nkeys, int kvh, int& status) {
   using C = PfCfg<KV, D>;
   int64_t tile[2];
+  int ok[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int j = j0 + s;
     const int p = j < nblk ? row[j] : 0;
-    int ok = j < nblk;
-    if (ok && (unsigned)p >= (uint64_t)a.num_blocks) {
+    ok[s] = j < nblk;
+    if (ok[s] && (unsigned)p >= (uint64_t)a.num_blocks) {
       status |= kStatusBadBlock;
-      ok = 0;
+      ok[s] = 0;
     }
-    st.ok[s] = uni(ok);
-    tile[s] = (int64_t)uni(ok ? p : 0) * a.Hkv + kvh;
+    ok[s] = uni(ok[s]);
+    tile[s] = (int64_t)uni(ok[s] ? p : 0) * a.Hkv + kvh;
+    st.ks[s] = 1.f;
+    st.vs[s] = 1.f;
     if constexpr (KV == KvType::FP8) {
-      st.ks[s] = ok ? a.kv_scales[tile[s]] : 0.f;
-      st.vs[s] = ok ? a.kv_scales[a.num_blocks * a.Hkv + tile[s]] : 0.f;
-    } else {
-      st.ks[s] = 1.f;
-      st.vs[s] = 1.f;
+      if (ok[s]) {
+        st.ks[s] = a.kv_scales[tile[s]];
+        st.vs[s] = a.kv_scales[a.num_blocks * a.Hkv + tile[s]];
+      }
     }
   }
+  st.ok0 = ok[0];
+  st.ok1 = ok[1];
+  int live = nkeys - 16 * j0;
+  if (!ok[1]) live = live < 16 ? live : 16;
+  if (!ok[0]) live = 0;
+  st.live = live;
   const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
   const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
 #pragma unroll
   for (int u = 0; u < C::UPT; ++u) {
-    const int unit = (int)threadIdx.x + 256 * u;
+    const int unit = (int)threadIdx.x + kPfThreads * u;
     const int blk = unit / (C::TILEB / 16);
     const int off = (unit - blk * (C::TILEB / 16)) * 16;
-    const bool live = unit < C::UNITS && st.ok[blk & 1];
+    const bool on = unit < C::UNITS && ok[blk & 1];
     const int64_t base = tile[blk & 1] * C::TILEB + off;
-    st.k[u] = live ? *reinterpret_cast<const u32x4*>(kc + base) : u32x4{0, 0, 0, 0};
-    st.v[u] = live ? *reinterpret_cast<const u32x4*>(vc + base) : u32x4{0, 0, 0, 0};
+    st.k[u] = on ? *reinterpret_cast<const u32x4*>(kc + base) : u32x4{0, 0, 0, 0};
+    st.v[u] = on ? *reinterpret_cast<const u32x4*>(vc + base) : u32x4{0, 0, 0, 0};
   }
+}
+
+// Two V values (f32) of keys k and k + 1 -> packed fp16, saturated to the fp16
+// range; `ovf` records a live key whose value did not fit.
+__device__ __forceinline__ uint32_t v_pack(float x, float y, int k, int live, int& ovf) {
+  constexpr float kHalfMax = 65504.f;
+  ovf |= (k < live && !(fabsf(x) <= kHalfMax)) | (k + 1 < live && !(fabsf(y) <= kHalfMax));
+  return pk_f16(__builtin_amdgcn_fmed3f(x, -kHalfMax, kHalfMax), __builtin_amdgcn_fmed3f(y, -kHalfMax, kHalfMax));
 }
 
 template <KvType KV, int D>
-__device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf) {
+__device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf, int& status) {
   using C = PfCfg<KV, D>;
+  int ovf = 0;
 #pragma unroll
   for (int u = 0; u < C::UPT; ++u) {
-    const int unit = (int)threadIdx.x + 256 * u;
+    const int unit = (int)threadIdx.x + kPfThreads * u;
     if (unit >= C::UNITS) break;
     const int blk = unit / (C::TILEB / 16);
     const int off = (unit - blk * (C::TILEB / 16)) * 16;
-    const int krow = off / C::ROWB, kcol = off - krow * C::ROWB;
-    *reinterpret_cast<u32x4*>(buf + (blk * 16 + krow) * C::KROW + kcol) = st.k[u];
-    // V: global dim row d, tokens [tok, tok + 16 / ESZ); LDS dim row d holds
-    // segment c = [block 0 tokens 4c..4c+3][block 1 tokens 4c..4c+3]
-    const int d = off / C::VROWB, tok = (off - d * C::VROWB) / C::ESZ;
-    uint8_t* vrow = buf + C::KBUF + d * C::VROW + blk * C::VSEG;
+    const int krow = off / C::GROW, e0 = (off - krow * C::GROW) / C::GSZ;  // token row, first element
+    uint8_t* kdst = buf + (blk * 16 + krow) * C::KROW + 2 * e0;
+    const int d = off / C::GVROW, t0 = (off - d * C::GVROW) / C::GSZ;     // dim row, first token
+    uint8_t* vrow = buf + C::KBUF + d * C::VROW + 8 * blk;               // segment c at + 16 c
+    const int k0 = 16 * blk + t0;                                         // pair-relative key of t0
     if constexpr (KV == KvType::BF16) {
-      const int c = tok / 4;  // 0 or 2
-      *reinterpret_cast<u32x2*>(vrow + c * 2 * C::VSEG) = u32x2{st.v[u].x, st.v[u].y};
-      *reinterpret_cast<u32x2*>(vrow + (c + 1) * 2 * C::VSEG) = u32x2{st.v[u].z, st.v[u].w};
+      *reinterpret_cast<u32x4*>(kdst) = st.k[u];
+      float f[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __builtin_bit_cast(float, st.v[u][i] << 16);
+        f[2 * i + 1] = __builtin_bit_cast(float, st.v[u][i] & 0xFFFF0000u);
+      }
+      const int c = t0 / 4;  // 0 or 2
+      *reinterpret_cast<u32x2*>(vrow + 16 * c) =
+          u32x2{v_pack(f[0], f[1], k0, st.live, ovf), v_pack(f[2], f[3], k0 + 2, st.live, ovf)};
+      *reinterpret_cast<u32x2*>(vrow + 16 * (c + 1)) =
+          u32x2{v_pack(f[4], f[5], k0 + 4, st.live, ovf), v_pack(f[6], f[7], k0 + 6, st.live, ovf)};
     } else {
-      *reinterpret_cast<uint32_t*>(vrow + 0 * 2 * C::VSEG) = st.v[u].x;
-      *reinterpret_cast<uint32_t*>(vrow + 1 * 2 * C::VSEG) = st.v[u].y;
-      *reinterpret_cast<uint32_t*>(vrow + 2 * 2 * C::VSEG) = st.v[u].z;
-      *reinterpret_cast<uint32_t*>(vrow + 3 * 2 * C::VSEG) = st.v[u].w;
+      u32x4 lo, hi;  // 16 codes -> 16 bf16 (exact)
+      const u32x2 a0 = fp8x4_to_bf16x4(st.k[u].x), a1 = fp8x4_to_bf16x4(st.k[u].y);
+      const u32x2 a2 = fp8x4_to_bf16x4(st.k[u].z), a3 = fp8x4_to_bf16x4(st.k[u].w);
+      lo = u32x4{a0.x, a0.y, a1.x, a1.y};
+      hi = u32x4{a2.x, a2.y, a3.x, a3.y};
+      *reinterpret_cast<u32x4*>(kdst) = lo;
+      *reinterpret_cast<u32x4*>(kdst + 16) = hi;
+      const float vs = st.vs[blk & 1];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {  // word c: tokens 4c..4c+3 of dim row d
+        const uint32_t wv = st.v[u][c];
+        const float2 x01 = fp8x2_to_f32x2<false>(wv, vs), x23 = fp8x2_to_f32x2<true>(wv, vs);
+        *reinterpret_cast<u32x2*>(vrow + 16 * c) =
+            u32x2{v_pack(x01.x, x01.y, k0 + 4 * c, st.live, ovf), v_pack(x23.x, x23.y, k0 + 4 * c + 2, st.live, ovf)};
+      }
     }
   }
+  if (ovf) status |= kStatusHalfRange;
 }
 
-// One pair from LDS for this wave's 64 columns. MASKED: per-column key limits
+// One pair from LDS for this wave's columns. MASKED: per-column key limits
 // see[n] (keys of the pair the column sees) and the pair's live keys (V rows
-// at or past `live` are zeroed).
+// at or past `live` are zeroed). c0 / c1: softmax scale (log2 units) times the
+// blocks' K scales, > 0.
 template <KvType KV, int D, bool MASKED>
 __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
-                                        float c0, float c1, float vs0, float vs1, const int (&see)[kPfNT], int live,
+                                        float c0, float c1, const int (&see)[kPfNT], int live,
                                         f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], float (&m_run)[kPfNT],
                                         float (&l_run)[kPfNT]) {
   using C = PfCfg<KV, D>;
@@ -281,39 +347,31 @@ __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[k
   for (int n = 0; n < kPfNT; ++n) s0[n] = s1[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < C::KSTEPS; ++j) {
-    bf16x8 k0, k1;
-    if constexpr (KV == KvType::BF16) {
-      k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + r * C::KROW + (32 * j + 8 * c) * 2));
-      k1 = __builtin_bit_cast(bf16x8,
-                              *reinterpret_cast<const u32x4*>(buf + (16 + r) * C::KROW + (32 * j + 8 * c) * 2));
-    } else {
-      const u32x2 w0 = *reinterpret_cast<const u32x2*>(buf + r * C::KROW + 32 * j + 8 * c);
-      const u32x2 w1 = *reinterpret_cast<const u32x2*>(buf + (16 + r) * C::KROW + 32 * j + 8 * c);
-      const u32x2 a0 = fp8x4_to_bf16x4(w0.x), b0 = fp8x4_to_bf16x4(w0.y);
-      const u32x2 a1 = fp8x4_to_bf16x4(w1.x), b1 = fp8x4_to_bf16x4(w1.y);
-      k0 = __builtin_bit_cast(bf16x8, u32x4{a0.x, a0.y, b0.x, b0.y});
-      k1 = __builtin_bit_cast(bf16x8, u32x4{a1.x, a1.y, b1.x, b1.y});
-    }
+    const bf16x8 k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + r * C::KROW + 64 * j + 16 * c));
+    const bf16x8 k1 =
+        __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + (16 + r) * C::KROW + 64 * j + 16 * c));
 #pragma unroll
     for (int n = 0; n < kPfNT; ++n) {
       s0[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qb[n][j], s0[n], 0, 0, 0);
       s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qb[n][j], s1[n], 0, 0, 0);
     }
   }
-  bf16x8 phi[kPfNT], plo[kPfNT];
+  f16x8 ph[kPfNT];
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) {
-    float x[8];
+    float y[8];  // raw scores of keys 4c+i (block 0) and 16+4c+i (block 1)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      x[i] = s0[n][i] * c0;
-      x[4 + i] = s1[n][i] * c1;
+      y[i] = s0[n][i];
+      y[4 + i] = s1[n][i];
       if constexpr (MASKED) {
-        x[i] = 4 * c + i < see[n] ? x[i] : kNegInf;
-        x[4 + i] = 16 + 4 * c + i < see[n] ? x[4 + i] : kNegInf;
+        y[i] = 4 * c + i < see[n] ? y[i] : kNegInf;
+        y[4 + i] = 16 + 4 * c + i < see[n] ? y[4 + i] : kNegInf;
       }
     }
-    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    const float m0 = fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3]));
+    const float m1 = fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]));
+    float mx = fmaxf(m0 * c0, m1 * c1);
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     if (__any(mx > m_run[n] + kSlack)) {
@@ -324,18 +382,18 @@ __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[k
 #pragma unroll
       for (int m = 0; m < C::MT; ++m) acc[m][n] *= alpha;
     }
-    const float m_ref = m_run[n] == kNegInf ? 0.f : m_run[n];
-    float psum = 0.f;
+    const float nm = m_run[n] == kNegInf ? 0.f : -m_run[n];
+    float p[8], psum = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      float p = fast_exp2(x[i] - m_ref);
-      psum += p;
-      if constexpr (KV == KvType::FP8) p *= i < 4 ? vs0 : vs1;
-      const __bf16 h = (__bf16)p;
-      phi[n][i] = h;
-      plo[n][i] = (__bf16)(p - (float)h);
+      p[i] = fast_exp2(__builtin_fmaf(y[i], i < 4 ? c0 : c1, nm));
+      psum += p[i];
     }
     l_run[n] += psum;
+    u32x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = pk_f16(p[2 * i], p[2 * i + 1]);
+    ph[n] = __builtin_bit_cast(f16x8, w);
   }
   uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
   if constexpr (MASKED) {
@@ -348,27 +406,16 @@ __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[k
   const uint8_t* vb = buf + C::KBUF;
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
-    const int d = 16 * m + r;
-    u32x4 w;
-    if constexpr (KV == KvType::BF16) {
-      w = *reinterpret_cast<const u32x4*>(vb + d * C::VROW + 16 * c);
-    } else {
-      const u32x2 v = *reinterpret_cast<const u32x2*>(vb + d * C::VROW + 8 * c);
-      const u32x2 a0 = fp8x4_to_bf16x4(v.x), a1 = fp8x4_to_bf16x4(v.y);
-      w = u32x4{a0.x, a0.y, a1.x, a1.y};
-    }
+    u32x4 w = *reinterpret_cast<const u32x4*>(vb + (16 * m + r) * C::VROW + 16 * c);
     if constexpr (MASKED) w = u32x4{w.x & mk[0], w.y & mk[1], w.z & mk[2], w.w & mk[3]};
-    const bf16x8 va = __builtin_bit_cast(bf16x8, w);
+    const f16x8 va = __builtin_bit_cast(f16x8, w);
 #pragma unroll
-    for (int n = 0; n < kPfNT; ++n) {
-      acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[n], acc[m][n], 0, 0, 0);
-      acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[n], acc[m][n], 0, 0, 0);
-    }
+    for (int n = 0; n < kPfNT; ++n) acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, ph[n], acc[m][n], 0, 0, 0);
   }
 }
 
 template <KvType KV, int D>
-__global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   using C = PfCfg<KV, D>;
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * C::BUF];
   const int l = lane_id();
@@ -380,12 +427,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
   const int4 it = a.items[item];
   const int b = it.x, row0 = it.y, nt = it.z, first = it.w;
 
-  // this wave's columns: column col = 64w + 16n + r is token col / G, head col % G
+  // this wave's columns: column col = 32w + 16n + r is token col / G, head col % G
   int vis[kPfNT], tokq[kPfNT];
   bf16x8 qb[kPfNT][C::KSTEPS];
+  const uint32_t qflip = a.neg_scale ? 0x80008000u : 0u;  // a negative scale goes into q's sign
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) {
-    const int col = 64 * w + 16 * n + r;
+    const int col = kPfWaveCols * w + 16 * n + r;
     const int tok = col / a.G, head = col - tok * a.G;
     const bool ok = tok < nt;
     vis[n] = first + tok + 1;  // keys the column sees
@@ -395,11 +443,11 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
     for (int j = 0; j < C::KSTEPS; ++j) {
       u32x4 v = {0, 0, 0, 0};
       if (ok) v = *reinterpret_cast<const u32x4*>(qp + 32 * j + 8 * c);
-      qb[n][j] = __builtin_bit_cast(bf16x8, v);
+      qb[n][j] = __builtin_bit_cast(bf16x8, v ^ qflip);
     }
   }
-  const int tok_lo = 64 * w / a.G;
-  const int tok_hi_raw = (64 * w + 63) / a.G;
+  const int tok_lo = kPfWaveCols * w / a.G;
+  const int tok_hi_raw = (kPfWaveCols * w + kPfWaveCols - 1) / a.G;
   const int tok_hi = tok_hi_raw < nt - 1 ? tok_hi_raw : nt - 1;
   const bool wave_on = tok_lo < nt;
   const int pos_lo = first + tok_lo;  // this wave's first and last query positions
@@ -425,38 +473,35 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
 
   PfStage<KV, D> st;
   if (npairs > 0) {
-    pf_load<KV, D>(st, a, row, 0, nblk, kvh, status);
-    pf_store<KV, D>(st, lds);
+    pf_load<KV, D>(st, a, row, 0, nblk, nkeys, kvh, status);
+    pf_store<KV, D>(st, lds, status);
   }
   __syncthreads();
   int cur = 0;
   for (int j2 = 0; j2 < npairs; ++j2) {
-    const float c0 = a.scale_log2 * st.ks[0], c1 = a.scale_log2 * st.ks[1];
-    const float vs0 = st.vs[0], vs1 = st.vs[1];
-    const int ok0 = st.ok[0], ok1 = st.ok[1];
-    if (j2 + 1 < npairs) pf_load<KV, D>(st, a, row, 2 * (j2 + 1), nblk, kvh, status);
+    // c > 0: a zero or tiny scale leaves every weight at 1 either way
+    const float c0 = fmaxf(a.scale_log2 * st.ks[0], 1e-30f), c1 = fmaxf(a.scale_log2 * st.ks[1], 1e-30f);
+    const int live = st.live;
+    if (j2 + 1 < npairs) pf_load<KV, D>(st, a, row, 2 * (j2 + 1), nblk, nkeys, kvh, status);
     const int key0 = 32 * j2;
     if (wave_on && key0 <= pos_hi) {
       const uint8_t* buf = lds + cur * C::BUF;
-      // keys of the pair that exist for this tile (a skipped block's are dead)
-      int live = nkeys - key0;
-      if (!ok1) live = live < 16 ? live : 16;
-      if (!ok0) live = 0;
+      int see[kPfNT];
       if (key0 + 31 <= pos_lo && live >= 32) {
-        const int see[kPfNT] = {32, 32, 32, 32};
-        pf_pair<KV, D, false>(buf, qb, c0, c1, vs0, vs1, see, 32, acc, m_run, l_run);
+#pragma unroll
+        for (int n = 0; n < kPfNT; ++n) see[n] = 32;
+        pf_pair<KV, D, false>(buf, qb, c0, c1, see, 32, acc, m_run, l_run);
       } else {
-        int see[kPfNT];
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < live ? vis[n] - key0 : live;
-        pf_pair<KV, D, true>(buf, qb, c0, c1, vs0, vs1, see, live, acc, m_run, l_run);
+        pf_pair<KV, D, true>(buf, qb, c0, c1, see, live, acc, m_run, l_run);
       }
     }
-    if (j2 + 1 < npairs) pf_store<KV, D>(st, lds + (cur ^ 1) * C::BUF);
+    if (j2 + 1 < npairs) pf_store<KV, D>(st, lds + (cur ^ 1) * C::BUF, status);
     __syncthreads();
     cur ^= 1;
   }
-  if (__any(status) && l == 0) atomicOr(a.hdr + kHdrStatus, status);
+  if (status) atomicOr(a.hdr + kHdrStatus, status);  // error paths only
   if (!wave_on) return;
 
 #pragma unroll
@@ -500,7 +545,7 @@ hipError_t launch_prefill(const PrefillArgs& a, KvType kv, hipStream_t s) {
   if (e != hipSuccess) return e;
   void* fn = kv == KvType::FP8 ? prefill_for_d<KvType::FP8>(a.D) : prefill_for_d<KvType::BF16>(a.D);
   const int64_t wgs = (int64_t)a.items_max * a.Hkv;
-  return hipLaunchKernel(fn, dim3((unsigned)wgs), dim3(64 * kPfWaves), params, 0, s);
+  return hipLaunchKernel(fn, dim3((unsigned)wgs), dim3(kPfThreads), params, 0, s);
 }
 
 }  // namespace pda

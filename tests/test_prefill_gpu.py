@@ -158,6 +158,43 @@ def test_prefill_status_bits(lib):
     U.assert_close(U.out_to_f64(out)[:40], reference(pin)[:40], "bf16", "sequence without bad blocks")
 
 
+@pytest.mark.parametrize("scale", [-0.2, 0.0, 1e-3, 0.7])
+def test_prefill_softmax_scales(lib, scale):
+    """Any finite softmax scale: a negative one enters through q's sign, zero
+    averages the visible values."""
+    pin = W.generate_prefill(wl(8, 2, 64, "fp8_e4m3"), DEV, seq_lens=[3, 70, 200], q_counts=[3, 70, 120])
+    c = pin.cache
+    out = torch.empty(pin.q.shape, dtype=torch.float32, device=DEV)
+    lib.paged_prefill_attention(pin.q, pin.q_offsets, c.k_cache, c.v_cache, c.block_table, c.seq_lens, c.kv_scales,
+                                out, scale)
+    torch.cuda.synchronize()
+    ref = oracle.paged_prefill_attention(
+        q=U.raw(pin.q), q_offsets=pin.offsets, k_cache=U.raw(c.k_cache), v_cache=U.raw(c.v_cache),
+        block_table=c.layout.block_table, seq_lens=c.layout.seq_lens, softmax_scale=scale, q_dtype="bf16",
+        kv_dtype="fp8_e4m3", kv_scales=U.raw(c.kv_scales))
+    U.assert_close(U.out_to_f64(out), ref, "fp8_e4m3", f"scale {scale}")
+    assert lib.read_device_status() == 0
+
+
+def test_prefill_value_range_flag(lib):
+    """P . V runs in fp16: a live V value beyond +-65504 saturates and sets
+    status bit 16; values in range, and poison in dead slots, do not."""
+    pin = W.generate_prefill(wl(8, 2, 128, "bf16"), DEV, seq_lens=[40, 70], q_counts=[40, 70])
+    c = pin.cache
+    out = torch.empty(pin.q.shape, dtype=torch.float32, device=DEV)
+    v = c.v_cache.clone()
+    p = int(c.layout.block_table[1, 1])
+    v[p, 0, 5, 3] = 60000.0            # in range: no flag (token 19 of sequence 1)
+    lib.paged_prefill_attention(pin.q, pin.q_offsets, c.k_cache, v, c.block_table, c.seq_lens, None, out,
+                                c.softmax_scale)
+    assert lib.read_device_status() == 0
+    v[p, 0, 5, 3] = 1.0e6
+    lib.paged_prefill_attention(pin.q, pin.q_offsets, c.k_cache, v, c.block_table, c.seq_lens, None, out,
+                                c.softmax_scale)
+    assert lib.read_device_status() == lib.STATUS_HALF_RANGE
+    assert torch.isfinite(out).all()
+
+
 def test_prefill_after_appends(lib):
     """A cache written token by token by the append kernel, then read by the
     prefill (the log-prob forward after rollout), against the oracle."""
