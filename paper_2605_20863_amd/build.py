@@ -2,9 +2,9 @@
 
     python -m paper_2605_20863_amd.build
 
-compiles every source under ``csrc/`` with hipcc into
-``paper_2605_20863_amd/libpda.so`` (written to a temporary name, then renamed,
-so a concurrent loader never sees a half-written file).
+compiles every source under ``csrc/`` with hipcc (one object per source, in
+parallel) and links ``paper_2605_20863_amd/libpda.so`` (written to a temporary
+name, then renamed, so a concurrent loader never sees a half-written file).
 """
 
 import os
@@ -50,15 +50,15 @@ def hip_runtime_dir():
     return None
 
 
-def build(verbose: bool = False) -> str:
-    out_tmp = LIB + f".tmp{os.getpid()}"
-    link = []
-    rt = hip_runtime_dir()
-    if rt:
-        link = ["-L", rt, f"-Wl,-rpath,{rt}"]
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-shared", "-fPIC",
-           "-I", os.path.join(ROOT, "include"), "-I", CSRC, *HIP_FLAGS,
-           *[os.path.join(CSRC, s) for s in SOURCES], *link, "-o", out_tmp]
+# Per-source device flags. The prefill kernels never rely on NaN semantics
+# (dead cache slots are masked bitwise, masked logits are -inf), so they run
+# with IEEE mode off: max and min then need no NaN-quieting copies.
+SOURCE_FLAGS = {
+    "pda_prefill.hip": ["-Xarch_device", "-fno-honor-nans", "-Xarch_device", "-mno-amdgpu-ieee"],
+}
+
+
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -66,11 +66,36 @@ def build(verbose: bool = False) -> str:
     noise = "is not a recognized feature for this target"
     log = "\n".join(l for l in (res.stdout + res.stderr).splitlines() if noise not in l)
     if res.returncode != 0:
-        if os.path.exists(out_tmp):
-            os.unlink(out_tmp)
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{log}")
     if verbose and log.strip():
         print(log)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source to an object (in parallel), then link libpda.so."""
+    import tempfile
+    from concurrent.futures import ThreadPoolExecutor
+
+    out_tmp = LIB + f".tmp{os.getpid()}"
+    link = []
+    rt = hip_runtime_dir()
+    if rt:
+        link = ["-L", rt, f"-Wl,-rpath,{rt}"]
+    common = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+              "-I", os.path.join(ROOT, "include"), "-I", CSRC, *HIP_FLAGS]
+    with tempfile.TemporaryDirectory(prefix="pda_build_") as tmp:
+        objs = [os.path.join(tmp, s + ".o") for s in SOURCES]
+        cmds = [[*common, *SOURCE_FLAGS.get(s, []), "-c", os.path.join(CSRC, s), "-o", o]
+                for s, o in zip(SOURCES, objs)]
+        with ThreadPoolExecutor(max_workers=len(cmds)) as pool:
+            for f in [pool.submit(_run, c, verbose) for c in cmds]:
+                f.result()
+        try:
+            _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, *link, "-o", out_tmp], verbose)
+        except Exception:
+            if os.path.exists(out_tmp):
+                os.unlink(out_tmp)
+            raise
     os.replace(out_tmp, LIB)
     return LIB
 

@@ -28,7 +28,7 @@
 //   other, one barrier per pair. K rows are padded so 16 rows hit distinct
 //   banks; V rows are stored with the two blocks' tokens interleaved in the
 //   order the P^T operand holds them, so each lane reads its 8 keys at once.
-// * Per wave and pair: S^T[32 keys x 64 columns] = K . Q^T on
+// * Per wave and pair: S^T[32 keys x 32 columns] = K . Q^T on
 //   v_mfma_f32_16x16x32_bf16, online softmax on the accumulators (lazy
 //   rescale), O^T += V^T . P^T with P split into bf16 hi + lo (a bf16 weight
 //   alone is off by up to 2^-8 of itself, which rows with a few keys carry
@@ -54,6 +54,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kPfWaves = 8;
@@ -93,11 +94,12 @@ __device__ __forceinline__ uint32_t pk_f16(float x, float y) {
   return __builtin_bit_cast(uint32_t, h);
 }
 
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-  uint32_t u = __builtin_bit_cast(uint32_t, f);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
+// two f32 -> packed bf16, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pk_bf16(float x, float y) {
+  bf16x2 h;
+  h[0] = (__bf16)x;
+  h[1] = (__bf16)y;
+  return __builtin_bit_cast(uint32_t, h);
 }
 
 // ------------------------------------------------------------------ plan
@@ -227,30 +229,57 @@ struct PfStage {
   float ks[2], vs[2];
 };
 
+// The tile's physical block ids, 64 at a time: lane i holds the id of block
+// 64q + i of chunk q (and, for fp8 caches, that block's K and V scales), read
+// with one vector load per chunk, the next chunk's ids one chunk ahead, so a
+// pair's ids come from v_readlane instead of a scalar load per block.
+struct PfIds {
+  int q;          // current chunk
+  int id, nxt;    // ids of chunk q and of chunk q + 1 (-1: past the tile or out of range)
+  float ks, vs;   // fp8 scales of chunk q's blocks
+};
+
+__device__ __forceinline__ int pf_id_load(const PrefillArgs& a, const int32_t* row, int j, int nblk, int& status) {
+  if (j >= nblk) return -1;
+  const int p = row[j];
+  if ((unsigned)p >= (uint64_t)a.num_blocks) {
+    status |= kStatusBadBlock;
+    return -1;
+  }
+  return p;
+}
+
+template <KvType KV>
+__device__ __forceinline__ void pf_ids_enter(PfIds& ids, const PrefillArgs& a, const int32_t* row, int q, int nblk,
+                                             int kvh, int& status) {
+  const int l = lane_id();
+  ids.q = q;
+  ids.id = ids.nxt;
+  ids.nxt = pf_id_load(a, row, 64 * (q + 1) + l, nblk, status);
+  if constexpr (KV == KvType::FP8) {
+    const int64_t tile = (int64_t)(ids.id < 0 ? 0 : ids.id) * a.Hkv + kvh;
+    ids.ks = ids.id < 0 ? 1.f : a.kv_scales[tile];
+    ids.vs = ids.id < 0 ? 1.f : a.kv_scales[a.num_blocks * a.Hkv + tile];
+  }
+}
+
 template <KvType KV, int D>
-__device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, const int32_t* row, int j0,
-                                        int nblk, int nkeys, int kvh, int& status) {
+__device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, PfIds& ids, const int32_t* row,
+                                        int j0, int nblk, int nkeys, int kvh, int& status) {
   using C = PfCfg<KV, D>;
+  if ((j0 >> 6) != ids.q) pf_ids_enter<KV>(ids, a, row, j0 >> 6, nblk, kvh, status);
   int64_t tile[2];
   int ok[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
-    const int j = j0 + s;
-    const int p = j < nblk ? row[j] : 0;
-    ok[s] = j < nblk;
-    if (ok[s] && (unsigned)p >= (uint64_t)a.num_blocks) {
-      status |= kStatusBadBlock;
-      ok[s] = 0;
-    }
-    ok[s] = uni(ok[s]);
-    tile[s] = (int64_t)uni(ok[s] ? p : 0) * a.Hkv + kvh;
+    const int p = __builtin_amdgcn_readlane(ids.id, (j0 + s) & 63);
+    ok[s] = p >= 0;
+    tile[s] = (int64_t)(ok[s] ? p : 0) * a.Hkv + kvh;
     st.ks[s] = 1.f;
     st.vs[s] = 1.f;
     if constexpr (KV == KvType::FP8) {
-      if (ok[s]) {
-        st.ks[s] = a.kv_scales[tile[s]];
-        st.vs[s] = a.kv_scales[a.num_blocks * a.Hkv + tile[s]];
-      }
+      st.ks[s] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ids.ks), (j0 + s) & 63));
+      st.vs[s] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ids.vs), (j0 + s) & 63));
     }
   }
   st.ok0 = ok[0];
@@ -261,24 +290,40 @@ __device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a
   st.live = live;
   const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
   const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
+  static_assert((C::TILEB / 16) % 64 == 0, "a wave's units lie in one block");
 #pragma unroll
   for (int u = 0; u < C::UPT; ++u) {
     const int unit = (int)threadIdx.x + kPfThreads * u;
-    const int blk = unit / (C::TILEB / 16);
+    const int blk = uni(unit / (C::TILEB / 16));  // the same for the whole wave
     const int off = (unit - blk * (C::TILEB / 16)) * 16;
-    const bool on = unit < C::UNITS && ok[blk & 1];
-    const int64_t base = tile[blk & 1] * C::TILEB + off;
-    st.k[u] = on ? *reinterpret_cast<const u32x4*>(kc + base) : u32x4{0, 0, 0, 0};
-    st.v[u] = on ? *reinterpret_cast<const u32x4*>(vc + base) : u32x4{0, 0, 0, 0};
+    const bool on = blk < 2 && ok[blk & 1];
+    const int64_t base = (blk & 1 ? tile[1] : tile[0]) * C::TILEB;  // uniform
+    st.k[u] = on ? *reinterpret_cast<const u32x4*>(kc + base + off) : u32x4{0, 0, 0, 0};
+    st.v[u] = on ? *reinterpret_cast<const u32x4*>(vc + base + off) : u32x4{0, 0, 0, 0};
   }
 }
 
-// Two V values (f32) of keys k and k + 1 -> packed fp16, saturated to the fp16
-// range; `ovf` records a live key whose value did not fit.
-__device__ __forceinline__ uint32_t v_pack(float x, float y, int k, int live, int& ovf) {
-  constexpr float kHalfMax = 65504.f;
-  ovf |= (k < live && !(fabsf(x) <= kHalfMax)) | (k + 1 < live && !(fabsf(y) <= kHalfMax));
-  return pk_f16(__builtin_amdgcn_fmed3f(x, -kHalfMax, kHalfMax), __builtin_amdgcn_fmed3f(y, -kHalfMax, kHalfMax));
+constexpr float kHalfMax = 65504.f;  // largest finite fp16
+
+// V values (f32) -> packed fp16 pairs. Values within the fp16 range convert
+// as they are; larger ones saturate, and `ovf` records one whose key is live
+// (poison in a dead slot does not count).
+template <int N>
+__device__ __forceinline__ void v_pack(const float (&f)[N], uint32_t (&out)[N / 2], int k0, int live, int& ovf) {
+  float amax = 0.f;
+#pragma unroll
+  for (int i = 0; i < N; ++i) amax = fmaxf(amax, fabsf(f[i]));
+  if (amax > kHalfMax) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) ovf |= k0 + i < live && fabsf(f[i]) > kHalfMax;
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i)
+      out[i] = pk_f16(__builtin_amdgcn_fmed3f(f[2 * i], -kHalfMax, kHalfMax),
+                      __builtin_amdgcn_fmed3f(f[2 * i + 1], -kHalfMax, kHalfMax));
+  } else {
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) out[i] = pk_f16(f[2 * i], f[2 * i + 1]);
+  }
 }
 
 template <KvType KV, int D>
@@ -304,41 +349,63 @@ __device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf,
         f[2 * i] = __builtin_bit_cast(float, st.v[u][i] << 16);
         f[2 * i + 1] = __builtin_bit_cast(float, st.v[u][i] & 0xFFFF0000u);
       }
+      uint32_t h[4];
+      v_pack<8>(f, h, k0, st.live, ovf);
       const int c = t0 / 4;  // 0 or 2
-      *reinterpret_cast<u32x2*>(vrow + 16 * c) =
-          u32x2{v_pack(f[0], f[1], k0, st.live, ovf), v_pack(f[2], f[3], k0 + 2, st.live, ovf)};
-      *reinterpret_cast<u32x2*>(vrow + 16 * (c + 1)) =
-          u32x2{v_pack(f[4], f[5], k0 + 4, st.live, ovf), v_pack(f[6], f[7], k0 + 6, st.live, ovf)};
+      *reinterpret_cast<u32x2*>(vrow + 16 * c) = u32x2{h[0], h[1]};
+      *reinterpret_cast<u32x2*>(vrow + 16 * (c + 1)) = u32x2{h[2], h[3]};
     } else {
-      u32x4 lo, hi;  // 16 codes -> 16 bf16 (exact)
+      // K: 16 codes -> 16 bf16 (exact, unscaled: the K scale goes on the logits)
       const u32x2 a0 = fp8x4_to_bf16x4(st.k[u].x), a1 = fp8x4_to_bf16x4(st.k[u].y);
       const u32x2 a2 = fp8x4_to_bf16x4(st.k[u].z), a3 = fp8x4_to_bf16x4(st.k[u].w);
-      lo = u32x4{a0.x, a0.y, a1.x, a1.y};
-      hi = u32x4{a2.x, a2.y, a3.x, a3.y};
-      *reinterpret_cast<u32x4*>(kdst) = lo;
-      *reinterpret_cast<u32x4*>(kdst + 16) = hi;
+      *reinterpret_cast<u32x4*>(kdst) = u32x4{a0.x, a0.y, a1.x, a1.y};
+      *reinterpret_cast<u32x4*>(kdst + 16) = u32x4{a2.x, a2.y, a3.x, a3.y};
+      // V: code * scale in fp32, one rounding to fp16
       const float vs = st.vs[blk & 1];
+      float f[16];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {  // word c: tokens 4c..4c+3 of dim row d
-        const uint32_t wv = st.v[u][c];
-        const float2 x01 = fp8x2_to_f32x2<false>(wv, vs), x23 = fp8x2_to_f32x2<true>(wv, vs);
-        *reinterpret_cast<u32x2*>(vrow + 16 * c) =
-            u32x2{v_pack(x01.x, x01.y, k0 + 4 * c, st.live, ovf), v_pack(x23.x, x23.y, k0 + 4 * c + 2, st.live, ovf)};
+      for (int c = 0; c < 4; ++c) {
+        const float2 x01 = fp8x2_to_f32x2<false>(st.v[u][c], vs), x23 = fp8x2_to_f32x2<true>(st.v[u][c], vs);
+        f[4 * c] = x01.x;
+        f[4 * c + 1] = x01.y;
+        f[4 * c + 2] = x23.x;
+        f[4 * c + 3] = x23.y;
       }
+      uint32_t h[8];
+      if (vs * 448.f <= kHalfMax) {  // no code can leave the fp16 range
+#pragma unroll
+        for (int i = 0; i < 8; ++i) h[i] = pk_f16(f[2 * i], f[2 * i + 1]);
+      } else {
+        v_pack<16>(f, h, k0, st.live, ovf);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) *reinterpret_cast<u32x2*>(vrow + 16 * c) = u32x2{h[2 * c], h[2 * c + 1]};
     }
   }
   if (ovf) status |= kStatusHalfRange;
 }
 
+// Running softmax state of one 16-column N-tile (per lane: column r).
+struct PfRow {
+  float m;    // running max of the scaled logits (base 2); -inf before any key
+  float nm;   // -m, or 0 while m = -inf: the exponent offset of the weights
+  f32x4 l;    // sum of the fp16 weights (every row of a ones . P^T product)
+};
+
 // One pair from LDS for this wave's columns. MASKED: per-column key limits
 // see[n] (keys of the pair the column sees) and the pair's live keys (V rows
 // at or past `live` are zeroed). c0 / c1: softmax scale (log2 units) times the
 // blocks' K scales, > 0.
+//
+// The weights are exp2(logit - m) with a lazily updated running max m: only
+// when a logit exceeds m by more than kSlack (so weights stay below 2^8 and fit
+// fp16) is m raised and the accumulators rescaled. Each lane first checks its
+// own 8 logits; the cross-lane max over the column's 4 lanes runs only when a
+// lane of the wave crosses the threshold.
 template <KvType KV, int D, bool MASKED>
 __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
                                         float c0, float c1, const int (&see)[kPfNT], int live,
-                                        f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], float (&m_run)[kPfNT],
-                                        float (&l_run)[kPfNT]) {
+                                        f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], PfRow (&row)[kPfNT]) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
@@ -357,6 +424,7 @@ __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[k
     }
   }
   f16x8 ph[kPfNT];
+  const f16x8 ones = {1, 1, 1, 1, 1, 1, 1, 1};
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) {
     float y[8];  // raw scores of keys 4c+i (block 0) and 16+4c+i (block 1)
@@ -369,31 +437,31 @@ __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[k
         y[4 + i] = 16 + 4 * c + i < see[n] ? y[4 + i] : kNegInf;
       }
     }
-    const float m0 = fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3]));
-    const float m1 = fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]));
-    float mx = fmaxf(m0 * c0, m1 * c1);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    if (__any(mx > m_run[n] + kSlack)) {
-      const float m_new = fmaxf(m_run[n], mx);
-      const float alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run[n] - m_new);
-      m_run[n] = m_new;
-      l_run[n] *= alpha;
+    float lm;  // this lane's largest scaled logit
+    if constexpr (KV == KvType::FP8) {
+      lm = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])) * c0, fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7])) * c1);
+    } else {
+      lm = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]))) * c0;
+    }
+    if (__any(lm > row[n].m + kSlack)) {
+      float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(row[n].m, mx);
+      const float alpha = m_new == kNegInf ? 1.f : fast_exp2(row[n].m - m_new);
+      row[n].m = m_new;
+      row[n].nm = m_new == kNegInf ? 0.f : -m_new;
+      row[n].l *= alpha;
 #pragma unroll
       for (int m = 0; m < C::MT; ++m) acc[m][n] *= alpha;
     }
-    const float nm = m_run[n] == kNegInf ? 0.f : -m_run[n];
-    float p[8], psum = 0.f;
+    float p[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      p[i] = fast_exp2(__builtin_fmaf(y[i], i < 4 ? c0 : c1, nm));
-      psum += p[i];
-    }
-    l_run[n] += psum;
+    for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(y[i], i < 4 ? c0 : c1, row[n].nm));
     u32x4 w;
 #pragma unroll
     for (int i = 0; i < 4; ++i) w[i] = pk_f16(p[2 * i], p[2 * i + 1]);
     ph[n] = __builtin_bit_cast(f16x8, w);
+    row[n].l = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, ph[n], row[n].l, 0, 0, 0);
   }
   uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
   if constexpr (MASKED) {
@@ -464,16 +532,16 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   for (int m = 0; m < C::MT; ++m)
 #pragma unroll
     for (int n = 0; n < kPfNT; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[kPfNT], l_run[kPfNT];
+  PfRow rows[kPfNT];
 #pragma unroll
-  for (int n = 0; n < kPfNT; ++n) {
-    m_run[n] = kNegInf;
-    l_run[n] = 0.f;
-  }
+  for (int n = 0; n < kPfNT; ++n) rows[n] = PfRow{kNegInf, 0.f, f32x4{0.f, 0.f, 0.f, 0.f}};
 
   PfStage<KV, D> st;
+  PfIds ids;
+  ids.q = -1;
+  ids.nxt = pf_id_load(a, row, l, nblk, status);  // chunk 0, entered by the first load
   if (npairs > 0) {
-    pf_load<KV, D>(st, a, row, 0, nblk, nkeys, kvh, status);
+    pf_load<KV, D>(st, a, ids, row, 0, nblk, nkeys, kvh, status);
     pf_store<KV, D>(st, lds, status);
   }
   __syncthreads();
@@ -482,7 +550,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     // c > 0: a zero or tiny scale leaves every weight at 1 either way
     const float c0 = fmaxf(a.scale_log2 * st.ks[0], 1e-30f), c1 = fmaxf(a.scale_log2 * st.ks[1], 1e-30f);
     const int live = st.live;
-    if (j2 + 1 < npairs) pf_load<KV, D>(st, a, row, 2 * (j2 + 1), nblk, nkeys, kvh, status);
+    if (j2 + 1 < npairs) pf_load<KV, D>(st, a, ids, row, 2 * (j2 + 1), nblk, nkeys, kvh, status);
     const int key0 = 32 * j2;
     if (wave_on && key0 <= pos_hi) {
       const uint8_t* buf = lds + cur * C::BUF;
@@ -490,11 +558,11 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       if (key0 + 31 <= pos_lo && live >= 32) {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = 32;
-        pf_pair<KV, D, false>(buf, qb, c0, c1, see, 32, acc, m_run, l_run);
+        pf_pair<KV, D, false>(buf, qb, c0, c1, see, 32, acc, rows);
       } else {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < live ? vis[n] - key0 : live;
-        pf_pair<KV, D, true>(buf, qb, c0, c1, see, live, acc, m_run, l_run);
+        pf_pair<KV, D, true>(buf, qb, c0, c1, see, live, acc, rows);
       }
     }
     if (j2 + 1 < npairs) pf_store<KV, D>(st, lds + (cur ^ 1) * C::BUF, status);
@@ -506,20 +574,15 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
 
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) {
-    float lt = l_run[n];
-    lt += __shfl_xor(lt, 16, 64);
-    lt += __shfl_xor(lt, 32, 64);
+    const float lt = rows[n].l[0];
     if (tokq[n] < 0) continue;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     if (a.out_bf16) {
       uint16_t* o = static_cast<uint16_t*>(a.out) + (int64_t)tokq[n] * D;
 #pragma unroll
-      for (int m = 0; m < C::MT; ++m) {
-        u32x2 v;
-        v.x = f32_to_bf16_bits(acc[m][n][0] * inv) | (f32_to_bf16_bits(acc[m][n][1] * inv) << 16);
-        v.y = f32_to_bf16_bits(acc[m][n][2] * inv) | (f32_to_bf16_bits(acc[m][n][3] * inv) << 16);
-        *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) = v;
-      }
+      for (int m = 0; m < C::MT; ++m)
+        *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) =
+            u32x2{pk_bf16(acc[m][n][0] * inv, acc[m][n][1] * inv), pk_bf16(acc[m][n][2] * inv, acc[m][n][3] * inv)};
     } else {
       float* o = static_cast<float*>(a.out) + (int64_t)tokq[n] * D;
 #pragma unroll
