@@ -34,6 +34,7 @@ MFMA_BF16_PEAK_TFS = 2500.0   # dense bf16 matrix-core peak of MI355X
 LLC_BYTES = 256 << 20
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2605_20863_amd", "csrc", "pda_kernels.hip")
+PREFILL_SOURCE = os.path.join(ROOT, "paper_2605_20863_amd", "csrc", "pda_prefill.hip")
 
 
 def algorithmic_bytes(workload, seq_lens, shared=None):
@@ -261,14 +262,14 @@ def cpu_baseline(inp, budget_s):
 
 # ----------------------------------------------------------------- traffic
 
-def measured_traffic(workload_name, per_launch_bytes):
+def measured_traffic(workload_name, per_launch_bytes, source=KERNEL_SOURCE):
     """HBM bytes per call from committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs,
     or None when absent or taken on a different kernel source."""
     path = os.path.join(PROFILES, f"traffic_{workload_name}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    src = hashlib.sha256(open(source, "rb").read()).hexdigest()
     if rec.get("kernel_source_sha256") != src:
         return None
     return rec.get("hbm_bytes_per_call")
@@ -567,7 +568,7 @@ def prefill_main(args, w, dev):
             "peak": MFMA_BF16_PEAK_TFS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(w.name, flops, PREFILL_SOURCE),
             "algorithmic_flops_per_call": flops,
             "call_us": round(call_ms * 1e3, 2),
         },

@@ -45,6 +45,8 @@
 
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace pda {
 namespace {
 
@@ -211,7 +213,9 @@ struct PfCfg {
   static constexpr int GROW = D * GSZ;                  // bytes of a cached K token row
   static constexpr int GVROW = 16 * GSZ;                // bytes of a cached V dim row (16 tokens)
   static constexpr int TILEB = 16 * GROW;               // bytes of one cached (block, KV head) tile
-  static constexpr int UNITS = 2 * TILEB / 16;          // 16-byte units of a pair's K (or V) tiles
+  // staging unit: 8 elements (16 bytes of bf16, 8 bytes of fp8), so fp8 pairs keep every thread busy
+  static constexpr int UB = 8 * GSZ;
+  static constexpr int UNITS = 2 * TILEB / UB;          // units of a pair's K (or V) tiles
   static constexpr int UPT = (UNITS + kPfThreads - 1) / kPfThreads;
   static constexpr int KROW = 2 * D + 16;               // LDS K row stride: 16 rows on distinct banks
   static constexpr int VROW = 64 + 16;                  // LDS V row stride (32 fp16 keys + pad)
@@ -223,7 +227,8 @@ struct PfCfg {
 // V tiles, and the pair's workgroup-uniform block flags, scales and live keys.
 template <KvType KV, int D>
 struct PfStage {
-  u32x4 k[PfCfg<KV, D>::UPT], v[PfCfg<KV, D>::UPT];
+  using Unit = typename std::conditional<KV == KvType::FP8, u32x2, u32x4>::type;
+  Unit k[PfCfg<KV, D>::UPT], v[PfCfg<KV, D>::UPT];
   int ok0, ok1;   // block holds keys of the tile and its id is in range
   int live;       // keys of the pair that exist (from the pair's first key)
   float ks[2], vs[2];
@@ -290,16 +295,17 @@ __device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a
   st.live = live;
   const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
   const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
-  static_assert((C::TILEB / 16) % 64 == 0, "a wave's units lie in one block");
+  using Unit = typename PfStage<KV, D>::Unit;
+  static_assert((C::TILEB / C::UB) % 64 == 0, "a wave's units lie in one block");
 #pragma unroll
   for (int u = 0; u < C::UPT; ++u) {
     const int unit = (int)threadIdx.x + kPfThreads * u;
-    const int blk = uni(unit / (C::TILEB / 16));  // the same for the whole wave
-    const int off = (unit - blk * (C::TILEB / 16)) * 16;
+    const int blk = uni(unit / (C::TILEB / C::UB));  // the same for the whole wave
+    const int off = (unit - blk * (C::TILEB / C::UB)) * C::UB;
     const bool on = blk < 2 && ok[blk & 1];
     const int64_t base = (blk & 1 ? tile[1] : tile[0]) * C::TILEB;  // uniform
-    st.k[u] = on ? *reinterpret_cast<const u32x4*>(kc + base + off) : u32x4{0, 0, 0, 0};
-    st.v[u] = on ? *reinterpret_cast<const u32x4*>(vc + base + off) : u32x4{0, 0, 0, 0};
+    st.k[u] = on ? *reinterpret_cast<const Unit*>(kc + base + off) : Unit{};
+    st.v[u] = on ? *reinterpret_cast<const Unit*>(vc + base + off) : Unit{};
   }
 }
 
@@ -334,8 +340,8 @@ __device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf,
   for (int u = 0; u < C::UPT; ++u) {
     const int unit = (int)threadIdx.x + kPfThreads * u;
     if (unit >= C::UNITS) break;
-    const int blk = unit / (C::TILEB / 16);
-    const int off = (unit - blk * (C::TILEB / 16)) * 16;
+    const int blk = unit / (C::TILEB / C::UB);
+    const int off = (unit - blk * (C::TILEB / C::UB)) * C::UB;
     const int krow = off / C::GROW, e0 = (off - krow * C::GROW) / C::GSZ;  // token row, first element
     uint8_t* kdst = buf + (blk * 16 + krow) * C::KROW + 2 * e0;
     const int d = off / C::GVROW, t0 = (off - d * C::GVROW) / C::GSZ;     // dim row, first token
@@ -355,31 +361,30 @@ __device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf,
       *reinterpret_cast<u32x2*>(vrow + 16 * c) = u32x2{h[0], h[1]};
       *reinterpret_cast<u32x2*>(vrow + 16 * (c + 1)) = u32x2{h[2], h[3]};
     } else {
-      // K: 16 codes -> 16 bf16 (exact, unscaled: the K scale goes on the logits)
+      // K: 8 codes -> 8 bf16 (exact, unscaled: the K scale goes on the logits)
       const u32x2 a0 = fp8x4_to_bf16x4(st.k[u].x), a1 = fp8x4_to_bf16x4(st.k[u].y);
-      const u32x2 a2 = fp8x4_to_bf16x4(st.k[u].z), a3 = fp8x4_to_bf16x4(st.k[u].w);
       *reinterpret_cast<u32x4*>(kdst) = u32x4{a0.x, a0.y, a1.x, a1.y};
-      *reinterpret_cast<u32x4*>(kdst + 16) = u32x4{a2.x, a2.y, a3.x, a3.y};
-      // V: code * scale in fp32, one rounding to fp16
+      // V: tokens t0 .. t0 + 7 of dim row d, code * scale in fp32, one rounding to fp16
       const float vs = st.vs[blk & 1];
-      float f[16];
+      float f[8];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const float2 x01 = fp8x2_to_f32x2<false>(st.v[u][c], vs), x23 = fp8x2_to_f32x2<true>(st.v[u][c], vs);
-        f[4 * c] = x01.x;
-        f[4 * c + 1] = x01.y;
-        f[4 * c + 2] = x23.x;
-        f[4 * c + 3] = x23.y;
+      for (int i = 0; i < 2; ++i) {
+        const float2 x01 = fp8x2_to_f32x2<false>(st.v[u][i], vs), x23 = fp8x2_to_f32x2<true>(st.v[u][i], vs);
+        f[4 * i] = x01.x;
+        f[4 * i + 1] = x01.y;
+        f[4 * i + 2] = x23.x;
+        f[4 * i + 3] = x23.y;
       }
-      uint32_t h[8];
+      uint32_t h[4];
       if (vs * 448.f <= kHalfMax) {  // no code can leave the fp16 range
 #pragma unroll
-        for (int i = 0; i < 8; ++i) h[i] = pk_f16(f[2 * i], f[2 * i + 1]);
+        for (int i = 0; i < 4; ++i) h[i] = pk_f16(f[2 * i], f[2 * i + 1]);
       } else {
-        v_pack<16>(f, h, k0, st.live, ovf);
+        v_pack<8>(f, h, k0, st.live, ovf);
       }
-#pragma unroll
-      for (int c = 0; c < 4; ++c) *reinterpret_cast<u32x2*>(vrow + 16 * c) = u32x2{h[2 * c], h[2 * c + 1]};
+      const int c = t0 / 4;  // 0 or 2
+      *reinterpret_cast<u32x2*>(vrow + 16 * c) = u32x2{h[0], h[1]};
+      *reinterpret_cast<u32x2*>(vrow + 16 * (c + 1)) = u32x2{h[2], h[3]};
     }
   }
   if (ovf) status |= kStatusHalfRange;

@@ -104,6 +104,9 @@ WORKLOADS = {
     # sequence (~180k packed tokens).
     "logprob_gqa7b_bf16": Workload("logprob_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
                                    ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, prefill_frac=1.0),
+    # The same log-prob forward over an fp8 (e4m3) cache with per-tile scales.
+    "logprob_gqa7b_fp8kv": Workload("logprob_gqa7b_fp8kv", 64, 28, 4, 128, "bf16", "fp8_e4m3",
+                                    ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, prefill_frac=1.0),
     # Speculative verification on the 7B GQA step: 2 query tokens per sequence
     # (the drafted one and the next), 14 of the 16 MFMA columns.
     "spec2_gqa7b_bf16": Workload("spec2_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
