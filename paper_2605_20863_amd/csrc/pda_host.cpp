@@ -382,6 +382,8 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   a.kv_scales = kv_scales;
   a.out = out;
   a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.mfma_scale_log2 = std::fabs(softmax_scale) * 1.4426950408889634f;
+  a.neg_scale = softmax_scale < 0.f;
   a.B = problem->num_seqs;
   a.Hq = problem->num_q_heads;
   a.Hkv = problem->num_kv_heads;

@@ -39,6 +39,8 @@ struct DecodeArgs {
   const float* kv_scales;
   void* out;
   float scale_log2;     // softmax_scale * log2(e): logits are kept in base 2
+  float mfma_scale_log2; // |softmax_scale| * log2(e): the MFMA body flips q's sign for a negative scale
+  int32_t neg_scale;    // 1: softmax_scale < 0
   int32_t B, Hq, Hkv, G, D;
   int32_t max_blocks;   // block_table row stride
   int64_t num_blocks;   // physical blocks (for the bounds check of table entries)

@@ -516,28 +516,36 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
     s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[0], j), qb[j], s0, 0, 0, 0);
     s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[1], j), qb[j], s1, 0, 0, 0);
   }
-  const float c0 = scale_log2 * bf.ks[0];
-  const float c1 = scale_log2 * bf.ks[1];
-  float x[8];
+  // scale_log2 > 0 here (a negative softmax scale enters through q's sign); a
+  // zero or tiny scale leaves every weight at 1 either way
+  const float c0 = fmaxf(scale_log2 * bf.ks[0], 1e-30f);
+  const float c1 = fmaxf(scale_log2 * bf.ks[1], 1e-30f);
+  float y[8];  // raw scores; -inf where masked
   // live: the lane's token slot holds a token of the entry (the V rows this
   // lane feeds to PV are these tokens, for every column); the lane's column
   // sees the token only if it is also `hide` or more slots before the end
   bool live[8];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    x[i] = s0[i] * c0;
-    x[4 + i] = s1[i] * c1;
+    y[i] = s0[i];
+    y[4 + i] = s1[i];
     if constexpr (MASKED) {
       live[i] = 4 * c + i < bf.rem[0];
       live[4 + i] = 4 * c + i < bf.rem[1];
-      x[i] = 4 * c + i < bf.rem[0] - hide ? x[i] : kNegInf;
-      x[4 + i] = 4 * c + i < bf.rem[1] - hide ? x[4 + i] : kNegInf;
+      y[i] = 4 * c + i < bf.rem[0] - hide ? y[i] : kNegInf;
+      y[4 + i] = 4 * c + i < bf.rem[1] - hide ? y[4 + i] : kNegInf;
     }
   }
-  float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-  if (__any(mx > m_run + kMaxSlack)) {  // wave-uniform; -inf + slack = -inf starts a segment
+  // Lazy rescale: weights are exp2(logit - m) with the running max m raised
+  // (and the partial rescaled) only when a logit exceeds m by kMaxSlack. Each
+  // lane checks its own 8 logits; the max over the column's 4 lanes is taken
+  // only when some lane of the wave crosses the threshold (wave-uniform).
+  const float m0 = fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3]));
+  const float m1 = fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]));
+  const float lm = KV == KvType::FP8 ? fmaxf(m0 * c0, m1 * c1) : fmaxf(m0, m1) * c0;
+  if (__any(lm > m_run + kMaxSlack)) {  // -inf + slack = -inf starts a segment
+    float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m_run, mx);
     const float alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run - m_new);
     m_run = m_new;
@@ -545,13 +553,13 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
 #pragma unroll
     for (int m = 0; m < C::MT; ++m) acc[m] *= alpha;
   }
-  const float m_ref = m_run == kNegInf ? 0.f : m_run;
+  const float nm = m_run == kNegInf ? 0.f : -m_run;
 
   float p[8];
   float psum = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    p[i] = fast_exp2(x[i] - m_ref);
+    p[i] = fast_exp2(__builtin_fmaf(y[i], i < 4 ? c0 : c1, nm));
     psum += p[i];
   }
   l_run += psum;
@@ -625,12 +633,13 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
   const int full = kBlockSize + a.Qn - 1;
   bf16x8 qb[C::KSTEPS];
   {
+    const uint32_t qflip = a.neg_scale ? 0x80008000u : 0u;  // a negative scale goes into q's sign
     const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + qo_row * D;
 #pragma unroll
     for (int j = 0; j < C::KSTEPS; ++j) {
       u32x4 w = {0, 0, 0, 0};
       if (r < sg.ncols) w = ld<u32x4>(qrow + C::qdim(j, c));
-      qb[j] = __builtin_bit_cast(bf16x8, w);
+      qb[j] = __builtin_bit_cast(bf16x8, w ^ qflip);
     }
   }
 
@@ -648,17 +657,17 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
   if (npairs > 1) mfma_issue<KV, D>(b1, a, ids, j_lo + 2, j_hi, L, kvh, status);
   int i = 0;
   for (; i + 3 < npairs; i += 2) {
-    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run, full, hide);
+    mfma_step<KV, D>(b0, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
     mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
-    mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run, full, hide);
+    mfma_step<KV, D>(b1, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
     mfma_issue<KV, D>(b1, a, ids, j_lo + 2 * (i + 3), j_hi, L, kvh, status);
   }
   if (i < npairs) {
-    mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run, full, hide);
+    mfma_step<KV, D>(b0, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
     if (i + 2 < npairs) mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
   }
-  if (i + 1 < npairs) mfma_step<KV, D>(b1, qb, a.scale_log2, acc, m_run, l_run, full, hide);
-  if (i + 2 < npairs) mfma_step<KV, D>(b0, qb, a.scale_log2, acc, m_run, l_run, full, hide);
+  if (i + 1 < npairs) mfma_step<KV, D>(b1, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
+  if (i + 2 < npairs) mfma_step<KV, D>(b0, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
 
   // Lanes c = 0..3 hold disjoint token subsets of head r: total the denominator.
   l_run += __shfl_xor(l_run, 16, 64);

@@ -79,6 +79,27 @@ def test_edge_lengths(lib, kv, G, D):
             assert np.array_equal(got[7], np.zeros_like(got[7])), "empty sequence must give zeros"
 
 
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+@pytest.mark.parametrize("scale", [-0.15, 0.0, 1e-4, 0.3])
+def test_softmax_scales(lib, kv, scale):
+    """Any finite softmax scale, on both kernel families: a negative scale,
+    zero (the mean of the values) and a tiny one."""
+    lens = [1, 17, 40, 300, 0, 129]
+    w = W.Workload(f"scale_{kv}", len(lens), 8, 2, 128, "bf16", kv, ("uniform", 1, 1), cfg_id=97)
+    inp = W.generate(w, DEV, seq_lens=lens)
+    ref = oracle.paged_decode_attention(
+        q=U.raw(inp.q), k_cache=U.raw(inp.k_cache), v_cache=U.raw(inp.v_cache), block_table=inp.layout.block_table,
+        seq_lens=inp.layout.seq_lens, softmax_scale=scale, q_dtype="bf16", kv_dtype=kv,
+        kv_scales=U.raw(inp.kv_scales) if inp.kv_scales is not None else None)
+    for v in ("vector", "mfma"):
+        out = torch.empty(inp.q.shape, dtype=torch.float32, device=DEV)
+        lib.paged_decode_attention(inp.q, inp.k_cache, inp.v_cache, inp.block_table, inp.seq_lens, inp.kv_scales,
+                                   out, scale, variant=v, min_blocks_per_wave=1, waves_per_cu=16)
+        torch.cuda.synchronize()
+        U.assert_close(U.out_to_f64(out), ref, kv, f"scale {scale} {kv} {v}")
+    assert lib.read_device_status() == 0
+
+
 @pytest.mark.parametrize("name", ["gqa7b_bf16", "fp8kv", "tiny_mha_f32"])
 def test_peaked_softmax(lib, name):
     # q x 8 makes logits ~N(0, 64): a few tokens dominate and the running max
