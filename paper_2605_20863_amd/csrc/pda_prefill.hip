@@ -302,7 +302,7 @@ __device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a
     const int unit = (int)threadIdx.x + kPfThreads * u;
     const int blk = uni(unit / (C::TILEB / C::UB));  // the same for the whole wave
     const int off = (unit - blk * (C::TILEB / C::UB)) * C::UB;
-    const bool on = blk < 2 && ok[blk & 1];
+    const bool on = blk < 2 && ((blk & 1) ? ok[1] : ok[0]);  // selects: no dynamically indexed array
     const int64_t base = (blk & 1 ? tile[1] : tile[0]) * C::TILEB;  // uniform
     st.k[u] = on ? *reinterpret_cast<const Unit*>(kc + base + off) : Unit{};
     st.v[u] = on ? *reinterpret_cast<const Unit*>(vc + base + off) : Unit{};
@@ -365,7 +365,7 @@ __device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf,
       const u32x2 a0 = fp8x4_to_bf16x4(st.k[u].x), a1 = fp8x4_to_bf16x4(st.k[u].y);
       *reinterpret_cast<u32x4*>(kdst) = u32x4{a0.x, a0.y, a1.x, a1.y};
       // V: tokens t0 .. t0 + 7 of dim row d, code * scale in fp32, one rounding to fp16
-      const float vs = st.vs[blk & 1];
+      const float vs = (blk & 1) ? st.vs[1] : st.vs[0];
       float f[8];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -397,24 +397,15 @@ struct PfRow {
   f32x4 l;    // sum of the fp16 weights (every row of a ones . P^T product)
 };
 
-// One pair from LDS for this wave's columns. MASKED: per-column key limits
-// see[n] (keys of the pair the column sees) and the pair's live keys (V rows
-// at or past `live` are zeroed). c0 / c1: softmax scale (log2 units) times the
-// blocks' K scales, > 0.
-//
-// The weights are exp2(logit - m) with a lazily updated running max m: only
-// when a logit exceeds m by more than kSlack (so weights stay below 2^8 and fit
-// fp16) is m raised and the accumulators rescaled. Each lane first checks its
-// own 8 logits; the cross-lane max over the column's 4 lanes runs only when a
-// lane of the wave crosses the threshold.
-template <KvType KV, int D, bool MASKED>
-__device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
-                                        float c0, float c1, const int (&see)[kPfNT], int live,
-                                        f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], PfRow (&row)[kPfNT]) {
+// Scores of one pair for this wave's columns: S^T[32 keys x 32 columns] =
+// K . Q^T from LDS; s0 holds keys 4c..4c+3 of the first block, s1 of the
+// second, for column r of each N-tile.
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_scores(const uint8_t* buf, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
+                                          f32x4 (&s0)[kPfNT], f32x4 (&s1)[kPfNT]) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
-  f32x4 s0[kPfNT], s1[kPfNT];
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) s0[n] = s1[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -428,6 +419,25 @@ __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[k
       s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qb[n][j], s1[n], 0, 0, 0);
     }
   }
+}
+
+// Softmax weights of one pair from its scores, and O^T += V^T . P^T. MASKED:
+// per-column key limits see[n] (keys of the pair the column sees) and the
+// pair's live keys (V rows at or past `live` are zeroed). c0 / c1: softmax
+// scale (log2 units) times the blocks' K scales, > 0.
+//
+// The weights are exp2(logit - m) with a lazily updated running max m: only
+// when a logit exceeds m by more than kSlack (so weights stay below 2^8 and fit
+// fp16) is m raised and the accumulators rescaled. Each lane first checks its
+// own 8 logits; the cross-lane max over the column's 4 lanes runs only when a
+// lane of the wave crosses the threshold.
+template <KvType KV, int D, bool MASKED>
+__device__ __forceinline__ void pf_softmax_pv(const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const uint8_t* buf,
+                                              float c0, float c1, const int (&see)[kPfNT], int live,
+                                              f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], PfRow (&row)[kPfNT]) {
+  using C = PfCfg<KV, D>;
+  const int l = lane_id();
+  const int r = l & 15, c = l >> 4;
   f16x8 ph[kPfNT];
   const f16x8 ones = {1, 1, 1, 1, 1, 1, 1, 1};
 #pragma unroll
@@ -487,6 +497,18 @@ __device__ __forceinline__ void pf_pair(const uint8_t* buf, const bf16x8 (&qb)[k
   }
 }
 
+// Per-pair values a wave needs after the pair's tiles are in LDS.
+struct PfMeta {
+  float c0, c1;  // softmax scale (log2 units) times the blocks' K scales, > 0
+  int live;      // keys of the pair that exist
+};
+
+template <KvType KV, int D>
+__device__ __forceinline__ PfMeta pf_meta(const PfStage<KV, D>& st, float scale_log2) {
+  // c > 0: a zero or tiny scale leaves every weight at 1 either way
+  return PfMeta{fmaxf(scale_log2 * st.ks[0], 1e-30f), fmaxf(scale_log2 * st.ks[1], 1e-30f), st.live};
+}
+
 template <KvType KV, int D>
 __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   using C = PfCfg<KV, D>;
@@ -529,6 +551,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const int nkeys = first + nt > 0 ? first + nt : 0;  // keys up to the tile's last position
   const int npairs = (nkeys + 31) / 32;
   const int nblk = (nkeys + 15) / 16;
+  // pairs this wave computes: those with a key at or before its last position
+  const int wpairs = !wave_on || pos_hi < 0 ? 0 : (pos_hi / 32 + 1 < npairs ? pos_hi / 32 + 1 : npairs);
   const int32_t* row = a.block_table + (int64_t)b * a.max_blocks;
   int status = 0;
 
@@ -541,38 +565,49 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) rows[n] = PfRow{kNegInf, 0.f, f32x4{0.f, 0.f, 0.f, 0.f}};
 
+  // pair j2's weights and P . V, on the masked path where some column of the
+  // wave does not see every key of the pair, or a key is past the tile
+  auto finish = [&](int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const PfMeta& m) {
+    const int key0 = 32 * j2;
+    const uint8_t* buf = lds + (j2 & 1) * C::BUF;
+    int see[kPfNT];
+    if (key0 + 31 <= pos_lo && m.live >= 32) {
+#pragma unroll
+      for (int n = 0; n < kPfNT; ++n) see[n] = 32;
+      pf_softmax_pv<KV, D, false>(s0, s1, buf, m.c0, m.c1, see, 32, acc, rows);
+    } else {
+#pragma unroll
+      for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < m.live ? vis[n] - key0 : m.live;
+      pf_softmax_pv<KV, D, true>(s0, s1, buf, m.c0, m.c1, see, m.live, acc, rows);
+    }
+  };
+
+  // Pair j + 1's tiles are loaded while pair j is computed; pair j comes from
+  // LDS buffer j % 2. (Running the two waves of a SIMD half a pair apart, so
+  // one's softmax would overlap the other's matrix work, measured slower.)
   PfStage<KV, D> st;
   PfIds ids;
   ids.q = -1;
   ids.nxt = pf_id_load(a, row, l, nblk, status);  // chunk 0, entered by the first load
+  PfMeta mj{1.f, 1.f, 0};
   if (npairs > 0) {
     pf_load<KV, D>(st, a, ids, row, 0, nblk, nkeys, kvh, status);
     pf_store<KV, D>(st, lds, status);
+    mj = pf_meta<KV, D>(st, a.scale_log2);
   }
   __syncthreads();
-  int cur = 0;
   for (int j2 = 0; j2 < npairs; ++j2) {
-    // c > 0: a zero or tiny scale leaves every weight at 1 either way
-    const float c0 = fmaxf(a.scale_log2 * st.ks[0], 1e-30f), c1 = fmaxf(a.scale_log2 * st.ks[1], 1e-30f);
-    const int live = st.live;
     if (j2 + 1 < npairs) pf_load<KV, D>(st, a, ids, row, 2 * (j2 + 1), nblk, nkeys, kvh, status);
-    const int key0 = 32 * j2;
-    if (wave_on && key0 <= pos_hi) {
-      const uint8_t* buf = lds + cur * C::BUF;
-      int see[kPfNT];
-      if (key0 + 31 <= pos_lo && live >= 32) {
-#pragma unroll
-        for (int n = 0; n < kPfNT; ++n) see[n] = 32;
-        pf_pair<KV, D, false>(buf, qb, c0, c1, see, 32, acc, rows);
-      } else {
-#pragma unroll
-        for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < live ? vis[n] - key0 : live;
-        pf_pair<KV, D, true>(buf, qb, c0, c1, see, live, acc, rows);
-      }
+    if (j2 < wpairs) {
+      f32x4 s0[kPfNT], s1[kPfNT];
+      pf_scores<KV, D>(lds + (j2 & 1) * C::BUF, qb, s0, s1);
+      finish(j2, s0, s1, mj);
     }
-    if (j2 + 1 < npairs) pf_store<KV, D>(st, lds + (cur ^ 1) * C::BUF, status);
+    if (j2 + 1 < npairs) {
+      pf_store<KV, D>(st, lds + ((j2 + 1) & 1) * C::BUF, status);
+      mj = pf_meta<KV, D>(st, a.scale_log2);
+    }
     __syncthreads();
-    cur ^= 1;
   }
   if (status) atomicOr(a.hdr + kHdrStatus, status);  // error paths only
   if (!wave_on) return;
