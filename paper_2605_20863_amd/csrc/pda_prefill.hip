@@ -304,8 +304,12 @@ __device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a
     const int off = (unit - blk * (C::TILEB / C::UB)) * C::UB;
     const bool on = blk < 2 && ((blk & 1) ? ok[1] : ok[0]);  // selects: no dynamically indexed array
     const int64_t base = (blk & 1 ? tile[1] : tile[0]) * C::TILEB;  // uniform
-    st.k[u] = on ? *reinterpret_cast<const Unit*>(kc + base + off) : Unit{};
-    st.v[u] = on ? *reinterpret_cast<const Unit*>(vc + base + off) : Unit{};
+    // a block that is not loaded keeps stale values: its keys are masked (scores
+    // to -inf, V rows zeroed bitwise) on every path that could read them
+    if (on) {
+      st.k[u] = *reinterpret_cast<const Unit*>(kc + base + off);
+      st.v[u] = *reinterpret_cast<const Unit*>(vc + base + off);
+    }
   }
 }
 
@@ -438,6 +442,7 @@ __device__ __forceinline__ void pf_softmax_pv(const f32x4 (&s0)[kPfNT], const f3
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
+  const uint8_t* vb = buf + C::KBUF;
   f16x8 ph[kPfNT];
   const f16x8 ones = {1, 1, 1, 1, 1, 1, 1, 1};
 #pragma unroll
@@ -486,7 +491,6 @@ __device__ __forceinline__ void pf_softmax_pv(const f32x4 (&s0)[kPfNT], const f3
       mk[h] = (k < live ? 0xFFFFu : 0u) | (k + 1 < live ? 0xFFFF0000u : 0u);
     }
   }
-  const uint8_t* vb = buf + C::KBUF;
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
     u32x4 w = *reinterpret_cast<const u32x4*>(vb + (16 * m + r) * C::VROW + 16 * c);
@@ -515,7 +519,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * C::BUF];
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
-  const int w = (int)(threadIdx.x >> 6);
+  const int w = uni((int)(threadIdx.x >> 6));  // wave-uniform: keeps per-wave values scalar
   const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
   const int item = (int)(blockIdx.x / (unsigned)a.Hkv);
   if (item >= a.hdr[kHdrItems]) return;  // the whole workgroup leaves together
