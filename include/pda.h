@@ -71,6 +71,10 @@ typedef enum pda_variant {
  *                for K and 1 for V; required for fp8 caches, ignored otherwise
  *   out          [num_seqs, num_q_heads, head_dim] out_dtype, contiguous
  *
+ * q, k_cache, v_cache and out must be 16-byte aligned (the kernels move them
+ * in 16-byte units); block_table, seq_lens and kv_scales 4-byte aligned.
+ * Misaligned pointers are rejected with PDA_EINVAL.
+ *
  * max_seq_len is a host-side upper bound on every seq_lens[b] (0 means
  * max_blocks_per_seq * block_size). Lengths above it, above
  * max_blocks_per_seq * block_size, or below 0 are clamped into range on the
@@ -315,8 +319,9 @@ typedef struct pda_prefill_problem {
  * non-decreasing within [0, T] make the call write nothing (bit 8).
  *
  * Errors: all checks run on the host before any HIP call: PDA_EINVAL for bad
- * sizes, dtypes or NULL pointers; PDA_EUNSUPPORTED for head_dim not in {64,
- * 128}, block_size != 16, G > 16, or an f32 cache. Uses the stream's
+ * sizes, dtypes, NULL pointers or misaligned ones (q, the caches and out need
+ * 16 bytes, the int32 and f32 arrays 4); PDA_EUNSUPPORTED for head_dim not in
+ * {64, 128}, block_size != 16, G > 16, or an f32 cache. Uses the stream's
  * workspace (16 bytes per work item of 256 / G query tokens).
  */
 int pda_paged_prefill_attention(const void* q,

@@ -12,6 +12,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -47,6 +48,20 @@ constexpr int64_t kChunkMinBytes = 512 << 10;  // of K and V: a chunk outlasts i
 constexpr int64_t kAlign = 256;
 
 int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct PtrAlign {
+  const void* p;
+  uintptr_t align;
+  const char* name;
+};
+
+// Null pointers pass (the callers check which ones are required).
+int check_alignment(std::initializer_list<PtrAlign> ptrs) {
+  for (const PtrAlign& x : ptrs)
+    if (reinterpret_cast<uintptr_t>(x.p) % x.align)
+      return fail(PDA_EINVAL, "%s is not %d-byte aligned", x.name, (int)x.align);
+  return PDA_OK;
+}
 
 struct Plan {
   int requested;  // the pda_variant the options asked for
@@ -346,6 +361,10 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
     return fail(PDA_EINVAL, "a required pointer (q, k_cache, v_cache, block_table, seq_lens, out) is NULL");
   if (problem->kv_dtype == PDA_DTYPE_FP8_E4M3 && !kv_scales)
     return fail(PDA_EINVAL, "an fp8 KV cache needs kv_scales");
+  if ((rc = check_alignment({{q, 16, "q"}, {k_cache, 16, "k_cache"}, {v_cache, 16, "v_cache"}, {out, 16, "out"},
+                             {block_table, 4, "block_table"}, {seq_lens, 4, "seq_lens"},
+                             {kv_scales, 4, "kv_scales"}})) != PDA_OK)
+    return rc;
 
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -416,7 +435,6 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   a.ws_m = reinterpret_cast<float*>(base + lay.m);
   a.ws_l = reinterpret_cast<float*>(base + lay.l);
   a.ws_acc = reinterpret_cast<float*>(base + lay.acc);
-
   if (gr.on && (e = pda::launch_prefix(a, gr.num_groups, stream)) != hipSuccess)
     return fail_hip(e, "prefix kernel launch");
   if ((e = pda::launch_decode(a, plan.variant, plan.kv, stream)) != hipSuccess)
@@ -539,6 +557,12 @@ int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, co
   if (!q || !q_offsets || !k_cache || !v_cache || !block_table || !seq_lens || !out)
     return fail(PDA_EINVAL, "a required pointer (q, q_offsets, k_cache, v_cache, block_table, seq_lens, out) is NULL");
   if (kd == PDA_DTYPE_FP8_E4M3 && !kv_scales) return fail(PDA_EINVAL, "an fp8 KV cache needs kv_scales");
+  {
+    const int rc = check_alignment({{q, 16, "q"}, {k_cache, 16, "k_cache"}, {v_cache, 16, "v_cache"},
+                                    {out, 16, "out"}, {q_offsets, 4, "q_offsets"}, {block_table, 4, "block_table"},
+                                    {seq_lens, 4, "seq_lens"}, {kv_scales, 4, "kv_scales"}});
+    if (rc != PDA_OK) return rc;
+  }
 
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);

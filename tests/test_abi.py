@@ -149,6 +149,16 @@ def test_null_pointers_rejected():
     assert L.raw_call(16, 16, 16, 16, 16, None, 16, 0.1, prob(kv_dtype=L.FP8_E4M3)) == L.EINVAL
 
 
+def test_misaligned_pointers_rejected():
+    # q, caches and out move in 16-byte units; the int32 / f32 arrays need 4 bytes
+    for i, bad in ((0, 24), (1, 8), (2, 40), (6, 18), (3, 18), (4, 2), (5, 6)):
+        ptrs = [64] * 7
+        ptrs[i] = bad
+        assert L.raw_call(*ptrs, 0.1, prob()) == L.EINVAL, i
+        assert "aligned" in L.last_error()
+    assert L.raw_call(*([64] * 7), 0.1, prob(num_seqs=0)) == L.OK
+
+
 def test_empty_batch_is_a_no_op():
     assert L.raw_call(None, None, None, None, None, None, None, 0.1, prob(num_seqs=0)) == L.OK
 
@@ -294,5 +304,11 @@ def test_prefill_argument_checks():
             assert call(pprob(kv_dtype=L.FP8_E4M3), ptrs) == L.EINVAL
         else:
             assert call(pprob(), ptrs) == L.EINVAL, i
+    # q (0), k_cache (2), v_cache (3), out (7) need 16-byte alignment; q_offsets (1), table (4), lens (5) 4
+    for i, bad in ((0, 24), (2, 8), (3, 40), (7, 20), (1, 2), (4, 6), (5, 18)):
+        ptrs = list(ok_ptrs)
+        ptrs[i] = bad
+        assert call(pprob(), ptrs) == L.EINVAL, i
+        assert "aligned" in L.last_error()
     assert call(pprob(num_seqs=0), [None] * 8) == L.OK      # empty batch: no-op
     assert call(pprob(num_tokens=0), [None] * 8) == L.OK    # no query rows: no-op
