@@ -18,23 +18,22 @@
 //   workgroups, which the dispatcher deals round-robin over the 8 XCDs, so with
 //   8 KV heads each XCD serves one KV head and its L2 holds only that head's
 //   keys and values, read by every tile of the sequence at nearly the same time.
-// * Attention kernel: one workgroup (4 waves) per (item, KV head). Its query
-//   columns are (token, head) pairs, 256 / G tokens times the G query heads of
-//   the KV head; each wave owns 64 columns (4 MFMA N-tiles), so every K or V
-//   operand read from LDS feeds 4 matrix products.
+// * Attention kernel: one workgroup (8 waves, 2 per SIMD) per (item, KV head).
+//   Its query columns are (token, head) pairs, 256 / G tokens times the G query
+//   heads of the KV head; each wave owns 32 columns (2 MFMA N-tiles).
 // * The KV prefix up to the tile's last position is walked two 16-token blocks
-//   (32 keys) at a time. The workgroup loads a pair's K and V tiles and writes
-//   them to one of two LDS buffers while the previous pair is computed from the
-//   other, one barrier per pair. K rows are padded so 16 rows hit distinct
-//   banks; V rows are stored with the two blocks' tokens interleaved in the
-//   order the P^T operand holds them, so each lane reads its 8 keys at once.
+//   (32 keys) at a time. The workgroup loads a pair's K and V tiles, decodes
+//   them (fp8 codes to bf16 K; V to fp16, fp8 as code times the block's V
+//   scale) and writes them to LDS, a few pairs ahead of the one being
+//   computed. K rows are padded so 16 rows hit distinct banks; V rows are
+//   stored with the two blocks' tokens interleaved in the order the P^T
+//   operand holds them, so each lane reads its 8 keys at once.
 // * Per wave and pair: S^T[32 keys x 32 columns] = K . Q^T on
 //   v_mfma_f32_16x16x32_bf16, online softmax on the accumulators (lazy
-//   rescale), O^T += V^T . P^T with P split into bf16 hi + lo (a bf16 weight
-//   alone is off by up to 2^-8 of itself, which rows with a few keys carry
-//   into the output; hi + lo keeps 16 bits). fp8 tiles are converted to bf16
-//   after the LDS read, the K scale goes on the logits and the V scale on the
-//   weights.
+//   rescale), weights packed to fp16 and O^T += V^T . P^T on
+//   v_mfma_f32_16x16x32_f16; the row sums come from a product with a ones
+//   operand, so they add exactly the fp16 weights the product uses. The K scale
+//   of an fp8 block goes on its logits.
 // * Causal masking selects per column (a key is seen iff it is at or before the
 //   column's position); V rows of keys past the tile's last position are zeroed,
 //   so NaN poison in unused slots never reaches the products. Only pairs that
