@@ -417,20 +417,28 @@ struct MfmaCfg {
   }
 };
 
-// V^T slice of one M-tile: 4 tokens of one head-dim row (bf16: 2 words, fp8: 1)
+// Token order of a pair of 16-token blocks (pair tokens 0-15 = block 0,
+// 16-31 = block 1). The P^T operand of lane (column, c) holds the weights of
+// pair tokens 8c .. 8c+7 (block c / 2), so the lane's V^T operand is 8
+// consecutive tokens of one head-dim row of one block: one 16-byte (bf16) or
+// 8-byte (fp8) load per M-tile. The score tiles deliver exactly those
+// weights: row i of the first tile is pair token 8 (i / 4) + i % 4, row i of
+// the second is that plus 4, so the accumulator lanes c hold tokens 8c .. 8c+3
+// and 8c+4 .. 8c+7. Lane (r, c) therefore loads K rows of block r / 8: tokens
+// 8 ((r / 4) % 2) + r % 4 and 4 more.
 template <KvType KV>
-using VSlice = typename std::conditional<KV == KvType::BF16, u32x2, uint32_t>::type;
+using VSlice = typename std::conditional<KV == KvType::BF16, u32x4, u32x2>::type;
 
 template <KvType KV, int D>
 struct MfmaPair {
   using C = MfmaCfg<KV, D>;
-  u32x4 k[2][C::NK4];
-  VSlice<KV> v[2][C::MT];
+  u32x4 k[2][C::NK4];  // A operands of the two score tiles
+  VSlice<KV> v[C::MT]; // V^T operands: 8 tokens of block c / 2 per M-tile
   float ks[2], vs[2];
   int rem[2];  // valid tokens from each block's first slot to the entry's end
 };
 
-// K A-operand of k-step j (8 bf16: dims qdim(j, c) .. +8 of token row r).
+// K A-operand of k-step j (8 bf16: dims qdim(j, c) .. +8 of the lane's token row).
 template <KvType KV, int D>
 __device__ __forceinline__ bf16x8 k_operand(const u32x4 (&k)[MfmaCfg<KV, D>::NK4], int j) {
   if constexpr (KV == KvType::BF16) {
@@ -455,38 +463,40 @@ __device__ __forceinline__ void mfma_issue(MfmaPair<KV, D>& bf, const DecodeArgs
   const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
   const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
   constexpr int64_t TILE = (int64_t)kBlockSize * D * C::ESZ;  // bytes per (block, head) tile
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int j = j0 + s;
-    if (s == 0 || j < j_hi) {
-      const Blk blk = block_at(a, ids, j, L, kvh, status);
-      bf.rem[s] = blk.rem;
-      const uint8_t* kt = kc + blk.tile * TILE + r * D * C::ESZ + 16 * c;
-#pragma unroll
-      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = ld_stream<u32x4>(kt + 64 * i);
-      const uint8_t* vt = vc + blk.tile * TILE + (r * kBlockSize + 4 * c) * C::ESZ;
-#pragma unroll
-      for (int m = 0; m < C::MT; ++m) {
-        const uint8_t* pv = vt + m * 16 * kBlockSize * C::ESZ;
-        bf.v[s][m] = ld_stream<VSlice<KV>>(pv);
-      }
-      if constexpr (KV == KvType::FP8) {
-        bf.ks[s] = a.kv_scales[blk.tile];
-        bf.vs[s] = a.kv_scales[a.num_blocks * a.Hkv + blk.tile];
-      } else {
-        bf.ks[s] = 1.f;
-        bf.vs[s] = 1.f;
-      }
+  const Blk b0 = block_at(a, ids, j0, L, kvh, status);
+  int64_t tile1 = b0.tile;  // a missing second block reads the first's tile, all of it masked
+  bf.rem[0] = b0.rem;
+  bf.rem[1] = 0;
+  bf.ks[1] = bf.vs[1] = 0.f;
+  if (j0 + 1 < j_hi) {
+    const Blk b1 = block_at(a, ids, j0 + 1, L, kvh, status);
+    tile1 = b1.tile;
+    bf.rem[1] = b1.rem;
+    if constexpr (KV == KvType::FP8) {
+      bf.ks[1] = a.kv_scales[b1.tile];
+      bf.vs[1] = a.kv_scales[a.num_blocks * a.Hkv + b1.tile];
     } else {
-      bf.rem[s] = 0;
-#pragma unroll
-      for (int i = 0; i < C::NK4; ++i) bf.k[s][i] = u32x4{0, 0, 0, 0};
-#pragma unroll
-      for (int m = 0; m < C::MT; ++m) bf.v[s][m] = VSlice<KV>{};
-      bf.ks[s] = 0.f;
-      bf.vs[s] = 0.f;
+      bf.ks[1] = bf.vs[1] = 1.f;
     }
   }
+  if constexpr (KV == KvType::FP8) {
+    bf.ks[0] = a.kv_scales[b0.tile];
+    bf.vs[0] = a.kv_scales[a.num_blocks * a.Hkv + b0.tile];
+  } else {
+    bf.ks[0] = bf.vs[0] = 1.f;
+  }
+  const int64_t ktile = r < 8 ? b0.tile : tile1;
+  const int tok = 8 * ((r >> 2) & 1) + (r & 3);
+  const uint8_t* kt = kc + ktile * TILE + tok * D * C::ESZ + 16 * c;
+#pragma unroll
+  for (int i = 0; i < C::NK4; ++i) {
+    bf.k[0][i] = ld_stream<u32x4>(kt + 64 * i);
+    bf.k[1][i] = ld_stream<u32x4>(kt + 4 * D * C::ESZ + 64 * i);
+  }
+  const int64_t vtile = c < 2 ? b0.tile : tile1;
+  const uint8_t* vt = vc + vtile * TILE + (r * kBlockSize + 8 * (c & 1)) * C::ESZ;
+#pragma unroll
+  for (int m = 0; m < C::MT; ++m) bf.v[m] = ld_stream<VSlice<KV>>(vt + m * 16 * kBlockSize * C::ESZ);
 }
 
 // Running-max slack (log2 units). The accumulators are rescaled only when a
@@ -509,40 +519,42 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
   const int l = lane_id();
   const int c = l >> 4;
 
-  // S^T = K . Q^T for both blocks: lane holds tokens 4c..4c+3 of head (lane & 15).
+  // S^T = K . Q^T, two 16-token tiles: lane holds pair tokens 8c .. 8c+7 of
+  // head (lane & 15), all from block c / 2 (first tile: 8c .. 8c+3).
   f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < C::KSTEPS; ++j) {
     s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[0], j), qb[j], s0, 0, 0, 0);
     s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[1], j), qb[j], s1, 0, 0, 0);
   }
+  const bool hib = c >= 2;        // the lane's tokens are in the second block
+  const int t0 = 8 * (c & 1);     // in-block slot of the lane's first token
   // scale_log2 > 0 here (a negative softmax scale enters through q's sign); a
   // zero or tiny scale leaves every weight at 1 either way
-  const float c0 = fmaxf(scale_log2 * bf.ks[0], 1e-30f);
-  const float c1 = fmaxf(scale_log2 * bf.ks[1], 1e-30f);
-  float y[8];  // raw scores; -inf where masked
+  const float cl = fmaxf(scale_log2 * (hib ? bf.ks[1] : bf.ks[0]), 1e-30f);
+  float y[8];  // raw scores of the lane's tokens; -inf where masked
   // live: the lane's token slot holds a token of the entry (the V rows this
   // lane feeds to PV are these tokens, for every column); the lane's column
   // sees the token only if it is also `hide` or more slots before the end
   bool live[8];
+  const int rem = hib ? bf.rem[1] : bf.rem[0];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     y[i] = s0[i];
     y[4 + i] = s1[i];
-    if constexpr (MASKED) {
-      live[i] = 4 * c + i < bf.rem[0];
-      live[4 + i] = 4 * c + i < bf.rem[1];
-      y[i] = 4 * c + i < bf.rem[0] - hide ? y[i] : kNegInf;
-      y[4 + i] = 4 * c + i < bf.rem[1] - hide ? y[4 + i] : kNegInf;
+  }
+  if constexpr (MASKED) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      live[i] = t0 + i < rem;
+      y[i] = t0 + i < rem - hide ? y[i] : kNegInf;
     }
   }
   // Lazy rescale: weights are exp2(logit - m) with the running max m raised
   // (and the partial rescaled) only when a logit exceeds m by kMaxSlack. Each
   // lane checks its own 8 logits; the max over the column's 4 lanes is taken
   // only when some lane of the wave crosses the threshold (wave-uniform).
-  const float m0 = fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3]));
-  const float m1 = fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]));
-  const float lm = KV == KvType::FP8 ? fmaxf(m0 * c0, m1 * c1) : fmaxf(m0, m1) * c0;
+  const float lm = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]))) * cl;
   if (__any(lm > m_run + kMaxSlack)) {  // -inf + slack = -inf starts a segment
     float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
@@ -559,16 +571,14 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
   float psum = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    p[i] = fast_exp2(__builtin_fmaf(y[i], i < 4 ? c0 : c1, nm));
+    p[i] = fast_exp2(__builtin_fmaf(y[i], cl, nm));
     psum += p[i];
   }
   l_run += psum;
   if constexpr (KV == KvType::FP8) {
+    const float vsl = hib ? bf.vs[1] : bf.vs[0];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      p[i] *= bf.vs[0];
-      p[4 + i] *= bf.vs[1];
-    }
+    for (int i = 0; i < 8; ++i) p[i] *= vsl;
   }
   // P^T operand in two bf16 terms: p = hi + lo + O(2^-17 p).
   bf16x8 phi, plo;
@@ -578,26 +588,23 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
     phi[i] = h;
     plo[i] = (__bf16)(p[i] - (float)h);
   }
-  uint32_t m0a = ~0u, m0b = ~0u, m1a = ~0u, m1b = ~0u;
+  uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
   if constexpr (MASKED) {
     // select, so NaN poison in dead slots cannot leak through 0 * NaN
-    m0a = (live[0] ? 0xFFFFu : 0u) | (live[1] ? 0xFFFF0000u : 0u);
-    m0b = (live[2] ? 0xFFFFu : 0u) | (live[3] ? 0xFFFF0000u : 0u);
-    m1a = (live[4] ? 0xFFFFu : 0u) | (live[5] ? 0xFFFF0000u : 0u);
-    m1b = (live[6] ? 0xFFFFu : 0u) | (live[7] ? 0xFFFF0000u : 0u);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) mk[h] = (live[2 * h] ? 0xFFFFu : 0u) | (live[2 * h + 1] ? 0xFFFF0000u : 0u);
   }
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
-    u32x2 v0, v1;
+    u32x4 w;
     if constexpr (KV == KvType::BF16) {
-      v0 = bf.v[0][m];
-      v1 = bf.v[1][m];
+      w = bf.v[m];
     } else {
-      v0 = fp8x4_to_bf16x4(bf.v[0][m]);
-      v1 = fp8x4_to_bf16x4(bf.v[1][m]);
+      const u32x2 a = fp8x4_to_bf16x4(bf.v[m].x);
+      const u32x2 b = fp8x4_to_bf16x4(bf.v[m].y);
+      w = u32x4{a.x, a.y, b.x, b.y};
     }
-    u32x4 w = {v0.x, v0.y, v1.x, v1.y};
-    if constexpr (MASKED) w = u32x4{v0.x & m0a, v0.y & m0b, v1.x & m1a, v1.y & m1b};
+    if constexpr (MASKED) w = u32x4{w.x & mk[0], w.y & mk[1], w.z & mk[2], w.w & mk[3]};
     const bf16x8 va = __builtin_bit_cast(bf16x8, w);
     acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[m], 0, 0, 0);
     acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[m], 0, 0, 0);
