@@ -95,6 +95,11 @@ WORKLOADS = {
     # fp8 (OCP e4m3) KV cache at scale with per-(block, KV head) scales.
     "fp8kv": Workload("fp8kv", 512, 64, 8, 128, "bf16", "fp8_e4m3",
                       ("lognormal", 8192, 0.9, 128, 65536), cfg_id=4),
+    # One GPU's share of the fp8 step under 8-way tensor parallelism over KV
+    # heads (rollout TP 8): the same sequences and lengths, 1 KV head and its
+    # 8 query heads.
+    "fp8kv_tp8": Workload("fp8kv_tp8", 512, 8, 1, 128, "bf16", "fp8_e4m3",
+                          ("lognormal", 8192, 0.9, 128, 65536), cfg_id=4),
     # GRPO groups over long shared contexts (3-6k-token prompts, ~1k-token
     # responses): the shape where reading shared blocks once matters most.
     "grpo_longprompt_bf16": Workload("grpo_longprompt_bf16", 256, 32, 8, 128, "bf16", "bf16",
