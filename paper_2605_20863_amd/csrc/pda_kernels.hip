@@ -1103,34 +1103,50 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   const int tid = threadIdx.x;
   // this sequence's columns for the KV head: G heads times its query tokens
   const int ncol = a.Qn * G;
-  const int64_t share = a.share[0];
+  // Every value the segment ranges need, loaded at once (one round trip):
+  // the length, the prefix sums of the sequence's entries and Q, and in
+  // shared-prefix mode the group's shared blocks. All indices are in range in
+  // either mode (in plain mode g = 0 and the shared-block read goes to cum[0]).
+  const int g = a.shared ? b / a.group_size : 0;
+  const int mi = b - g * a.group_size;  // member index in the group
+  const int sub = a.shared ? mi / a.M : 0;
+  const int v_own = a.shared ? a.n_prefix + b : b;
+  const int v_pre = g * a.nsub + sub;
+  const int32_t* sgp = a.shared ? a.sg : a.cum;
+  const int raw = a.seq_lens[b];
+  const int cum_own = a.cum[v_own];
+  const int cum_pre = a.cum[a.shared ? v_pre : 0];
+  const int S = sgp[g];
+  const int share32 = a.share[0];
+  // keep Q's load beside the others (the compiler would sink it into the
+  // branch that uses it, one more round trip)
+  asm volatile("" ::"v"(share32));
+  const int64_t share = share32;
 
   int64_t slot0[2];
   int nseg[2], col0[2];
   int parts = 0;
-  const int v_own = a.shared ? a.n_prefix + b : b;
-  const Entry own = entry_of(a, v_own);
-  if (own.nb > 0) {
-    const int64_t start = (int64_t)a.cum[v_own] * a.Hkv + (int64_t)kvh * own.nb;
+  // the sequence's own entry (its suffix after the shared blocks in shared-prefix mode)
+  const int Lf = clamp_len(a, raw);
+  const int S_own = a.shared ? S : 0;
+  const int nb_raw = (Lf + kBlockSize - 1) / kBlockSize - S_own;
+  const int own_nb = nb_raw > 0 ? nb_raw : 0;
+  const bool own_may_final = S_own == 0;
+  if (own_nb > 0) {
+    const int64_t start = (int64_t)cum_own * a.Hkv + (int64_t)kvh * own_nb;
     const int64_t w0 = start / share;
-    nseg[parts] = (int)((start + own.nb - 1) / share - w0) + 1;
+    nseg[parts] = (int)((start + own_nb - 1) / share - w0) + 1;
     slot0[parts] = (int64_t)v_own * a.Hkv + kvh + w0;
     col0[parts] = 0;
     ++parts;
   }
-  if (a.shared) {
-    const int g = b / a.group_size, i = b - g * a.group_size;
-    const int sub = i / a.M;
-    const int v = g * a.nsub + sub;
-    const int S = a.sg[g];
-    if (S > 0) {
-      const int64_t start = (int64_t)a.cum[v] * a.Hkv + (int64_t)kvh * S;
-      const int64_t w0 = start / share;
-      nseg[parts] = (int)((start + S - 1) / share - w0) + 1;
-      slot0[parts] = (int64_t)v * a.Hkv + kvh + w0;
-      col0[parts] = (i - sub * a.M) * G;
-      ++parts;
-    }
+  if (a.shared && S > 0) {  // the group's prefix entry: columns of member i
+    const int64_t start = (int64_t)cum_pre * a.Hkv + (int64_t)kvh * S;
+    const int64_t w0 = start / share;
+    nseg[parts] = (int)((start + S - 1) / share - w0) + 1;
+    slot0[parts] = (int64_t)v_pre * a.Hkv + kvh + w0;
+    col0[parts] = (mi - sub * a.M) * G;
+    ++parts;
   }
   // output row of column r: query token r / G, head kvh * G + r % G of sequence b
   auto out_row = [&](int r) { return (((int64_t)b * a.Qn + r / G) * a.Hq + (int64_t)kvh * G + r % G) * D; };
@@ -1142,7 +1158,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
     }
     return;
   }
-  if (parts == 1 && nseg[0] == 1 && own.may_final) return;  // one chunk wrote the output
+  if (parts == 1 && nseg[0] == 1 && own_may_final) return;  // one chunk wrote the output
 
   // thread t owns column h = t / 16 (if < ncol) and dims [ (t % 16) * D/16, +D/16 )
   constexpr int DE = D / 16;
