@@ -86,6 +86,14 @@ WORKLOADS = {
     # 7B-class GQA step: 28 query / 4 KV heads, bf16.
     "gqa7b_bf16": Workload("gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
                            ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1),
+    # The attention shapes of the paper's two larger models (Sec. 6.1): 32 / 4
+    # heads (Qwen3-30B-A3B) and 64 / 4 heads (Qwen3-235B-A22B, G = 16 fills
+    # every MFMA column), head_dim 128, at the 7B step's lengths (same seeds),
+    # so the KV bytes equal the 7B step's and only G differs.
+    "qwen30b_bf16": Workload("qwen30b_bf16", 64, 32, 4, 128, "bf16", "bf16",
+                             ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1),
+    "qwen235b_bf16": Workload("qwen235b_bf16", 64, 64, 4, 128, "bf16", "bf16",
+                              ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1),
     # RLVR rollout batch: 32 prompts x 8 GRPO samples sharing prompt blocks.
     "grpo_bf16": Workload("grpo_bf16", 256, 32, 8, 128, "bf16", "bf16",
                           ("grpo", 32, 8, 256, 1024, 4096, 1.0, 32768), cfg_id=2),

@@ -200,7 +200,7 @@ def test_out_of_range_inputs_are_contained(lib):
     assert lib.read_device_status() == 0
 
 
-FULL = ["gqa7b_bf16", "grpo_bf16", "straggler_bf16", "fp8kv", "fp8kv_tp8"]
+FULL = ["gqa7b_bf16", "grpo_bf16", "straggler_bf16", "fp8kv", "fp8kv_tp8", "qwen30b_bf16", "qwen235b_bf16"]
 
 
 @pytest.mark.parametrize("name", FULL)
