@@ -262,15 +262,27 @@ def cpu_baseline(inp, budget_s):
 
 # ----------------------------------------------------------------- traffic
 
+def source_digest(path):
+    """sha256 of a kernel source's code: comments removed and whitespace
+    collapsed, so that editing a comment keeps measurements taken on the same
+    code valid, while any change to the code itself invalidates them."""
+    import re
+
+    text = open(path, encoding="utf-8").read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = " ".join(text.split())
+    return hashlib.sha256(text.encode()).hexdigest()
+
+
 def measured_traffic(workload_name, per_launch_bytes, source=KERNEL_SOURCE):
     """HBM bytes per call from committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs,
-    or None when absent or taken on a different kernel source."""
+    or None when absent or taken on different kernel code."""
     path = os.path.join(PROFILES, f"traffic_{workload_name}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = hashlib.sha256(open(source, "rb").read()).hexdigest()
-    if rec.get("kernel_source_sha256") != src:
+    if rec.get("kernel_code_sha256") != source_digest(source):
         return None
     return rec.get("hbm_bytes_per_call")
 

@@ -25,9 +25,11 @@
 //     S^T[16 tok x 16 heads] = K[16 x D] . Q^T[D x 16] on v_mfma_f32_16x16x32_bf16
 //     (the GQA group's G <= 16 heads padded to 16 columns), online softmax on
 //     the accumulator registers, then O^T[D x 16] += V^T[D x 32 tok] . P^T[32 x 16].
-//     The accumulator layout of S^T already holds, per lane, the 4+4 token
-//     weights that the P^T operand needs, so P never moves between lanes. The
-//     price is the dim-major V tile [D][16] in the cache layout. P is split
+//     The score tiles' token rows are ordered so that each lane's accumulators
+//     hold the weights of 8 consecutive tokens of one block, exactly what its
+//     P^T operand needs: P never moves between lanes, and the lane's V^T
+//     operand is one 16-byte (bf16) or 8-byte (fp8) load of one head-dim row.
+//     The price is the dim-major V tile [D][16] in the cache layout. P is split
 //     into two bf16 terms (hi + lo) so that rounding P costs ~2^-17, not 2^-9.
 //   - Vector (any cache dtype, G <= 8): each 16-lane row owns 4 tokens; QK dot
 //     products are lane-partial FMAs reduced across the row with DPP row
