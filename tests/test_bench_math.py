@@ -74,3 +74,14 @@ def test_append_bytes_by_hand():
     assert bench.append_bytes(wl(kv="bf16"), B) == 2 * B * 2 * 64 * (2 + 2) + 8 * B
     # fp8: new rows read as bf16, written as codes; K and V scales read and written
     assert bench.append_bytes(wl(kv="fp8_e4m3"), B) == 2 * B * 2 * 64 * (2 + 1) + 2 * 2 * B * 2 * 4 + 8 * B
+
+
+def test_source_digest_ignores_comments_only(tmp_path):
+    a = tmp_path / "a.hip"
+    a.write_text("// header\nint f(int x) {  /* twice */ return 2 * x; }\n")
+    b = tmp_path / "b.hip"
+    b.write_text("// a different header\n\nint f(int x) {\n  return 2 * x;  // doubled\n}\n")
+    c = tmp_path / "c.hip"
+    c.write_text("// header\nint f(int x) { return 3 * x; }\n")
+    assert bench.source_digest(a) == bench.source_digest(b)
+    assert bench.source_digest(a) != bench.source_digest(c)
