@@ -1248,7 +1248,7 @@ __device__ __forceinline__ int block_min(int x, int* red) {
   return x;
 }
 
-__global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(DecodeArgs a, int num_groups) {
+__global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(DecodeArgs a) {  // grid: one workgroup per group
   __shared__ int red[kPrefixThreads / 64];
   const int g = blockIdx.x;
   const int tid = threadIdx.x;
@@ -1360,8 +1360,7 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
 hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s) {
   if (num_groups <= 0) return hipSuccess;
   DecodeArgs args = a;
-  int ng = num_groups;
-  void* params[] = {&args, &ng};
+  void* params[] = {&args};
   return hipLaunchKernel(reinterpret_cast<void*>(&prefix_kernel), dim3(num_groups), dim3(kPrefixThreads), params, 0,
                          s);
 }
