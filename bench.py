@@ -342,7 +342,7 @@ def main():
     if args.workload is None:
         args.workload = "logprob_gqa7b_bf16" if args.op == "prefill" else "gqa7b_bf16"
     w = W.WORKLOADS[args.workload]
-    if (args.op == "prefill") != (w.prefill_frac > 0):
+    if (args.op == "prefill") != w.is_prefill:
         print(f"--op {args.op} does not fit workload {w.name}", file=sys.stderr)
         sys.exit(2)
     if args.op == "prefill":

@@ -66,6 +66,13 @@ class Workload:
     # > 0: a prefill (log-prob forward) whose sequence b has n_b =
     # clip(rint(prefill_frac * L_b), 1, L_b) packed query tokens, its last n_b
     prefill_frac: float = 0.0
+    # > 0: a chunked prefill instead, n_b = min(prefill_chunk, L_b): each
+    # sequence's last chunk of new tokens attends over its whole cache
+    prefill_chunk: int = 0
+
+    @property
+    def is_prefill(self) -> bool:
+        return self.prefill_frac > 0 or self.prefill_chunk > 0
 
     @property
     def group(self) -> int:
@@ -120,6 +127,10 @@ WORKLOADS = {
     # The same log-prob forward over an fp8 (e4m3) cache with per-tile scales.
     "logprob_gqa7b_fp8kv": Workload("logprob_gqa7b_fp8kv", 64, 28, 4, 128, "bf16", "fp8_e4m3",
                                     ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, prefill_frac=1.0),
+    # Chunked prefill over the 7B GQA step's caches: each sequence's last 512
+    # tokens (all of a shorter one) attend causally over its whole cache.
+    "chunk512_gqa7b_bf16": Workload("chunk512_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
+                                    ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, prefill_chunk=512),
     # Speculative verification on the 7B GQA step: 2 query tokens per sequence
     # (the drafted one and the next), 14 of the 16 MFMA columns.
     "spec2_gqa7b_bf16": Workload("spec2_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
@@ -263,6 +274,8 @@ def group_prefix(w: Workload, layout: Layout):
 def prefill_counts(w: Workload, seq_lens) -> np.ndarray:
     """Query tokens per sequence of a prefill workload: its last n_b tokens."""
     L = np.asarray(seq_lens, dtype=np.int64)
+    if w.prefill_chunk > 0:
+        return np.minimum(L, w.prefill_chunk).astype(np.int32)
     n = np.clip(np.rint(w.prefill_frac * L), 1, np.maximum(L, 1))
     return np.where(L > 0, n, 0).astype(np.int32)
 

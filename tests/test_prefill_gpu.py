@@ -259,7 +259,7 @@ def sampled_reference(pin, rows_per_seq, seqs, rng):
     return rows.cpu().numpy(), ref
 
 
-@pytest.mark.parametrize("name,out_dtype", [("logprob_gqa7b_bf16", torch.bfloat16)])
+@pytest.mark.parametrize("name,out_dtype", [("logprob_gqa7b_bf16", torch.bfloat16), ("chunk512_gqa7b_bf16", torch.bfloat16)])
 def test_prefill_full_size_sampled(lib, name, out_dtype):
     """The benchmarked log-prob forward at full size (64 sequences, ~190k
     packed tokens, 28 / 4 heads) in the launch the benchmark times, checked on
