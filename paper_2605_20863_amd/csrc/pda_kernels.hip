@@ -661,22 +661,53 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
   float m_run = kNegInf, l_run = 0.f;
 
   const int npairs = (j_hi - j_lo + 1) >> 1;
-  MfmaPair<KV, D> b0, b1;
-  if (npairs > 0) mfma_issue<KV, D>(b0, a, ids, j_lo, j_hi, L, kvh, status);
-  if (npairs > 1) mfma_issue<KV, D>(b1, a, ids, j_lo + 2, j_hi, L, kvh, status);
-  int i = 0;
-  for (; i + 3 < npairs; i += 2) {
-    mfma_step<KV, D>(b0, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
-    mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
-    mfma_step<KV, D>(b1, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
-    mfma_issue<KV, D>(b1, a, ids, j_lo + 2 * (i + 3), j_hi, L, kvh, status);
+  auto step = [&](const MfmaPair<KV, D>& bf) { mfma_step<KV, D>(bf, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide); };
+  auto issue = [&](MfmaPair<KV, D>& bf, int p) { mfma_issue<KV, D>(bf, a, ids, j_lo + 2 * p, j_hi, L, kvh, status); };
+  if constexpr (KV == KvType::BF16) {
+    // three pairs in flight (one wave per SIMD leaves the registers for it)
+    MfmaPair<KV, D> b0, b1, b2;
+    if (npairs > 0) issue(b0, 0);
+    if (npairs > 1) issue(b1, 1);
+    if (npairs > 2) issue(b2, 2);
+    int i = 0;
+    for (; i + 5 < npairs; i += 3) {
+      step(b0);
+      issue(b0, i + 3);
+      step(b1);
+      issue(b1, i + 4);
+      step(b2);
+      issue(b2, i + 5);
+    }
+    // at most five pairs left: i, i+1, i+2 in flight in b0, b1, b2
+    if (i < npairs) {
+      step(b0);
+      if (i + 3 < npairs) issue(b0, i + 3);
+    }
+    if (i + 1 < npairs) {
+      step(b1);
+      if (i + 4 < npairs) issue(b1, i + 4);
+    }
+    if (i + 2 < npairs) step(b2);
+    if (i + 3 < npairs) step(b0);
+    if (i + 4 < npairs) step(b1);
+  } else {
+    MfmaPair<KV, D> b0, b1;
+    if (npairs > 0) issue(b0, 0);
+    if (npairs > 1) issue(b1, 1);
+    int i = 0;
+    for (; i + 3 < npairs; i += 2) {
+      step(b0);
+      issue(b0, i + 2);
+      step(b1);
+      issue(b1, i + 3);
+    }
+    if (i < npairs) {
+      step(b0);
+      if (i + 2 < npairs) issue(b0, i + 2);
+    }
+    if (i + 1 < npairs) step(b1);
+    if (i + 2 < npairs) step(b0);
   }
-  if (i < npairs) {
-    mfma_step<KV, D>(b0, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
-    if (i + 2 < npairs) mfma_issue<KV, D>(b0, a, ids, j_lo + 2 * (i + 2), j_hi, L, kvh, status);
-  }
-  if (i + 1 < npairs) mfma_step<KV, D>(b1, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
-  if (i + 2 < npairs) mfma_step<KV, D>(b0, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
 
   // Lanes c = 0..3 hold disjoint token subsets of head r: total the denominator.
   l_run += __shfl_xor(l_run, 16, 64);
