@@ -168,7 +168,7 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
 }
 
 // Shared-prefix mode: groups of group_size consecutive sequences; each
-// group's shared blocks become nsub work entries of M members (M * G <= 16
+// group's shared blocks become nsub work entries of M members (M * G <= 32
 // query columns), ahead of one entry per sequence for the rest of it.
 struct Groups {
   bool on = false;
@@ -191,7 +191,7 @@ int validate_groups(const pda_problem* pr, int32_t group_size, const int32_t* sh
   plan->variant = pda::Variant::Mfma;
   gr->on = true;
   gr->group_size = group_size;
-  const int per = pda::kMaxGroup / plan->G;
+  const int per = pda::kWideColumns / plan->G;  // members whose heads fill two MFMA N-tiles
   gr->M = group_size < per ? group_size : (per > 0 ? per : 1);
   gr->nsub = (group_size + gr->M - 1) / gr->M;
   gr->num_groups = pr->num_seqs / group_size;
@@ -263,8 +263,8 @@ int device_info(int dev, DeviceInfo* out) {
   return PDA_OK;
 }
 
-int occupancy(int dev, pda::Variant v, pda::KvType kv, int D, int G, int* wgs) {
-  const int gb = v == pda::Variant::Mfma ? 16 : (G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8);
+int occupancy(int dev, pda::Variant v, pda::KvType kv, int D, int G, bool wide, int* wgs) {
+  const int gb = v == pda::Variant::Mfma ? (wide ? pda::kWideColumns : 16) : (G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8);
   auto key = std::make_tuple(dev, (int)v, (int)kv, D, gb);
   {
     std::lock_guard<std::mutex> lk(g_mu);
@@ -275,7 +275,7 @@ int occupancy(int dev, pda::Variant v, pda::KvType kv, int D, int G, int* wgs) {
     }
   }
   int n = 0;
-  hipError_t e = pda::decode_occupancy(v, kv, D, G, &n);
+  hipError_t e = pda::decode_occupancy(v, kv, D, G, wide, &n);
   if (e != hipSuccess) return fail_hip(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
   if (n < 1) n = 1;
   std::lock_guard<std::mutex> lk(g_mu);
@@ -375,7 +375,8 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
 
   int wpc = plan.waves_per_cu;
   if (wpc == 0) {
-    if ((rc = occupancy(dev, plan.variant, plan.kv, problem->head_dim, plan.G, &wpc)) != PDA_OK) return rc;
+    const bool wide = gr.on && gr.M * plan.G > 16;
+    if ((rc = occupancy(dev, plan.variant, plan.kv, problem->head_dim, plan.G, wide, &wpc)) != PDA_OK) return rc;
     if (wpc > kDefaultWavesPerCu) wpc = kDefaultWavesPerCu;
   }
   const int waves = di.cus * wpc;

@@ -11,6 +11,7 @@ constexpr int kBlockSize = 16;     // tokens per KV block
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kMaxGroup = 16;      // query heads per KV head (MFMA N dimension)
 constexpr int kMaxGroupVector = 8; // vector kernel keeps G x D/16 query values per lane
+constexpr int kWideColumns = 32;   // query columns of a shared-prefix entry (two MFMA N-tiles)
 
 enum class KvType : int { F32 = 0, BF16 = 1, FP8 = 2 };
 enum class Variant : int { Vector = 1, Mfma = 2 };
@@ -59,7 +60,7 @@ struct DecodeArgs {
   int32_t E;
   int32_t shared;       // 1: shared-prefix mode
   int32_t group_size;   // members per group (sequences g * group_size ..)
-  int32_t M;            // members per prefix entry (M * G <= 16)
+  int32_t M;            // members per prefix entry (M * G <= kWideColumns)
   int32_t nsub;         // prefix entries per group = ceil(group_size / M)
   int32_t n_prefix;     // num_groups * nsub
   int32_t Gp;           // query columns per partial row: Qn * G, or M * G in shared-prefix mode
@@ -132,6 +133,7 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // Shared-prefix mode: the groups' real shared block counts, before the decode kernel.
 hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s);
 // Max resident waves per CU for the decode kernel that (v, kv, D, G) selects.
-hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* waves_per_cu);
+// wide: the shared-prefix kernel whose prefix entries carry up to kWideColumns query columns
+hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, bool wide, int* waves_per_cu);
 
 }  // namespace pda

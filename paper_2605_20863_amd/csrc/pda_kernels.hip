@@ -140,7 +140,8 @@ __device__ __forceinline__ int clamp_len(const DecodeArgs& a, int L) {
 }
 
 // One work entry: a run of blocks read through one block-table row and
-// applied to up to 16 query columns. In plain mode entry b is sequence b with
+// applied to up to 16 query columns (32 for a shared-prefix entry, in two
+// MFMA N-tiles that share every K and V operand). In plain mode entry b is sequence b with
 // its G query heads. In shared-prefix mode (GRPO-style groups of equal size
 // whose members share leading blocks) entry (g, s) < n_prefix is group g's
 // shared blocks applied to the heads of members s*M .. s*M + M - 1 (column r
@@ -513,82 +514,107 @@ constexpr float kMaxSlack = 8.f;
 // the lane's column may not see -- past the sequence end, a skipped block, or
 // (several query tokens per sequence) past the column's causal end, `hide`
 // tokens before the end: those tokens get logit -inf and zero V.
-template <KvType KV, int D, bool MASKED>
-__device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[MfmaCfg<KV, D>::KSTEPS],
-                                             float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT],
-                                             float& m_run, float& l_run, int hide) {
+template <KvType KV, int D, bool MASKED, int NT>
+__device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf,
+                                             const bf16x8 (&qb)[NT][MfmaCfg<KV, D>::KSTEPS], float scale_log2,
+                                             f32x4 (&acc)[MfmaCfg<KV, D>::MT][NT], float (&m_run)[NT],
+                                             float (&l_run)[NT], const int (&hide)[NT]) {
   using C = MfmaCfg<KV, D>;
   const int l = lane_id();
   const int c = l >> 4;
 
-  // S^T = K . Q^T, two 16-token tiles: lane holds pair tokens 8c .. 8c+7 of
-  // head (lane & 15), all from block c / 2 (first tile: 8c .. 8c+3).
-  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+  // S^T = K . Q^T per N-tile of 16 columns, two 16-token tiles each: lane
+  // holds pair tokens 8c .. 8c+7 of column (lane & 15), all from block c / 2
+  // (first tile: 8c .. 8c+3).
+  f32x4 s0[NT], s1[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) s0[n] = s1[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < C::KSTEPS; ++j) {
-    s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[0], j), qb[j], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand<KV, D>(bf.k[1], j), qb[j], s1, 0, 0, 0);
+    const bf16x8 k0 = k_operand<KV, D>(bf.k[0], j), k1 = k_operand<KV, D>(bf.k[1], j);
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      s0[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qb[n][j], s0[n], 0, 0, 0);
+      s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qb[n][j], s1[n], 0, 0, 0);
+    }
   }
   const bool hib = c >= 2;        // the lane's tokens are in the second block
   const int t0 = 8 * (c & 1);     // in-block slot of the lane's first token
   // scale_log2 > 0 here (a negative softmax scale enters through q's sign); a
   // zero or tiny scale leaves every weight at 1 either way
   const float cl = fmaxf(scale_log2 * (hib ? bf.ks[1] : bf.ks[0]), 1e-30f);
-  float y[8];  // raw scores of the lane's tokens; -inf where masked
   // live: the lane's token slot holds a token of the entry (the V rows this
   // lane feeds to PV are these tokens, for every column); the lane's column
   // sees the token only if it is also `hide` or more slots before the end
   bool live[8];
   const int rem = hib ? bf.rem[1] : bf.rem[0];
+  float y[NT][8];  // raw scores of the lane's tokens; -inf where masked
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    y[i] = s0[i];
-    y[4 + i] = s1[i];
+  for (int n = 0; n < NT; ++n) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      y[n][i] = s0[n][i];
+      y[n][4 + i] = s1[n][i];
+    }
   }
   if constexpr (MASKED) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       live[i] = t0 + i < rem;
-      y[i] = t0 + i < rem - hide ? y[i] : kNegInf;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) y[n][i] = t0 + i < rem - hide[n] ? y[n][i] : kNegInf;
     }
   }
   // Lazy rescale: weights are exp2(logit - m) with the running max m raised
   // (and the partial rescaled) only when a logit exceeds m by kMaxSlack. Each
   // lane checks its own 8 logits; the max over the column's 4 lanes is taken
   // only when some lane of the wave crosses the threshold (wave-uniform).
-  const float lm = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]))) * cl;
-  if (__any(lm > m_run + kMaxSlack)) {  // -inf + slack = -inf starts a segment
-    float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
+  float lm[NT];
+  bool up = false;
 #pragma unroll
-    for (int m = 0; m < C::MT; ++m) acc[m] *= alpha;
+  for (int n = 0; n < NT; ++n) {
+    lm[n] = fmaxf(fmaxf(fmaxf(y[n][0], y[n][1]), fmaxf(y[n][2], y[n][3])),
+                  fmaxf(fmaxf(y[n][4], y[n][5]), fmaxf(y[n][6], y[n][7]))) * cl;
+    up |= lm[n] > m_run[n] + kMaxSlack;  // -inf + slack = -inf starts a segment
   }
-  const float nm = m_run == kNegInf ? 0.f : -m_run;
+  if (__any(up)) {
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      float mx = fmaxf(lm[n], __shfl_xor(lm[n], 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run[n], mx);
+      const float alpha = m_new == kNegInf ? 1.f : fast_exp2(m_run[n] - m_new);
+      m_run[n] = m_new;
+      l_run[n] *= alpha;
+#pragma unroll
+      for (int m = 0; m < C::MT; ++m) acc[m][n] *= alpha;
+    }
+  }
 
-  float p[8];
-  float psum = 0.f;
+  // P^T operands in two bf16 terms: p = hi + lo + O(2^-17 p).
+  bf16x8 phi[NT], plo[NT];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    p[i] = fast_exp2(__builtin_fmaf(y[i], cl, nm));
-    psum += p[i];
-  }
-  l_run += psum;
-  if constexpr (KV == KvType::FP8) {
-    const float vsl = hib ? bf.vs[1] : bf.vs[0];
+  for (int n = 0; n < NT; ++n) {
+    const float nm = m_run[n] == kNegInf ? 0.f : -m_run[n];
+    float p[8];
+    float psum = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) p[i] *= vsl;
-  }
-  // P^T operand in two bf16 terms: p = hi + lo + O(2^-17 p).
-  bf16x8 phi, plo;
+    for (int i = 0; i < 8; ++i) {
+      p[i] = fast_exp2(__builtin_fmaf(y[n][i], cl, nm));
+      psum += p[i];
+    }
+    l_run[n] += psum;
+    if constexpr (KV == KvType::FP8) {
+      const float vsl = hib ? bf.vs[1] : bf.vs[0];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const __bf16 h = (__bf16)p[i];
-    phi[i] = h;
-    plo[i] = (__bf16)(p[i] - (float)h);
+      for (int i = 0; i < 8; ++i) p[i] *= vsl;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const __bf16 h = (__bf16)p[i];
+      phi[n][i] = h;
+      plo[n][i] = (__bf16)(p[i] - (float)h);
+    }
   }
   uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
   if constexpr (MASKED) {
@@ -596,6 +622,7 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
 #pragma unroll
     for (int h = 0; h < 4; ++h) mk[h] = (live[2 * h] ? 0xFFFFu : 0u) | (live[2 * h + 1] ? 0xFFFF0000u : 0u);
   }
+  // O^T += V^T . P^T: one V operand per M-tile serves every N-tile
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
     u32x4 w;
@@ -608,63 +635,89 @@ __device__ __forceinline__ void mfma_compute(const MfmaPair<KV, D>& bf, const bf
     }
     if constexpr (MASKED) w = u32x4{w.x & mk[0], w.y & mk[1], w.z & mk[2], w.w & mk[3]};
     const bf16x8 va = __builtin_bit_cast(bf16x8, w);
-    acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, acc[m], 0, 0, 0);
-    acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, acc[m], 0, 0, 0);
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[n], acc[m][n], 0, 0, 0);
+      acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[n], acc[m][n], 0, 0, 0);
+    }
   }
 }
 
 // `full`: rem at which every column sees all 16 tokens of a block (16 plus
 // the largest `hide`, wave-uniform).
-template <KvType KV, int D>
-__device__ __forceinline__ void mfma_step(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[MfmaCfg<KV, D>::KSTEPS],
-                                          float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT], float& m_run,
-                                          float& l_run, int full, int hide) {
+template <KvType KV, int D, int NT>
+__device__ __forceinline__ void mfma_step(const MfmaPair<KV, D>& bf, const bf16x8 (&qb)[NT][MfmaCfg<KV, D>::KSTEPS],
+                                          float scale_log2, f32x4 (&acc)[MfmaCfg<KV, D>::MT][NT],
+                                          float (&m_run)[NT], float (&l_run)[NT], int full, const int (&hide)[NT]) {
   if (bf.rem[0] >= full && bf.rem[1] >= full)
-    mfma_compute<KV, D, false>(bf, qb, scale_log2, acc, m_run, l_run, hide);
+    mfma_compute<KV, D, false, NT>(bf, qb, scale_log2, acc, m_run, l_run, hide);
   else
-    mfma_compute<KV, D, true>(bf, qb, scale_log2, acc, m_run, l_run, hide);
+    mfma_compute<KV, D, true, NT>(bf, qb, scale_log2, acc, m_run, l_run, hide);
 }
 
-template <KvType KV, int D>
+// NT N-tiles of 16 query columns: 1 for plain entries, 2 for the prefix
+// entries of shared-prefix mode (up to 32 members' heads per shared block).
+// DEPTH pairs in flight: 3 or 2 (the two-tile body has the registers for 2;
+// the shared-prefix kernel gives every segment the same depth, so the waves
+// that carry prefix entries keep as many bytes in flight as the others and
+// take an even share of the bandwidth).
+template <KvType KV, int D, int NT, int DEPTH>
 __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds) {
   using C = MfmaCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
   const int kvh = sg.kvh, L = sg.L, j_lo = sg.j_lo, j_hi = sg.j_hi;
 
-  // Q^T B-operand: column r = (mem, head) with mem = r / G the member
-  // (shared-prefix entries) or the query token (several per sequence), dims
-  // qdim(j, c) .. +8 for k-step j. q rows are [sequence, query token, head].
-  const int mem = r / a.G, head = r - mem * a.G;
-  const int64_t qo_row = ((int64_t)sg.qs * a.Qn + mem) * a.Hq + kvh * a.G + head;
-  // query token mem of Qn sits Qn - 1 - mem tokens before the sequence end
-  const int hide = a.Qn > 1 && mem < a.Qn ? a.Qn - 1 - mem : 0;
+  // Q^T B-operand of N-tile n: column col = 16n + r = (mem, head) with
+  // mem = col / G the member (shared-prefix entries) or the query token
+  // (several per sequence), dims qdim(j, c) .. +8 for k-step j. q rows are
+  // [sequence, query token, head].
+  int64_t qo_row[NT];
+  int hide[NT];
+  bool on[NT];
   const int full = kBlockSize + a.Qn - 1;
-  bf16x8 qb[C::KSTEPS];
-  {
-    const uint32_t qflip = a.neg_scale ? 0x80008000u : 0u;  // a negative scale goes into q's sign
-    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + qo_row * D;
+  bf16x8 qb[NT][C::KSTEPS];
+  const uint32_t qflip = a.neg_scale ? 0x80008000u : 0u;  // a negative scale goes into q's sign
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int col = 16 * n + r;
+    const int mem = col / a.G, head = col - mem * a.G;
+    on[n] = col < sg.ncols;
+    qo_row[n] = ((int64_t)sg.qs * a.Qn + mem) * a.Hq + kvh * a.G + head;
+    // query token mem of Qn sits Qn - 1 - mem tokens before the sequence end
+    hide[n] = a.Qn > 1 && mem < a.Qn ? a.Qn - 1 - mem : 0;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + (on[n] ? qo_row[n] : 0) * D;
 #pragma unroll
     for (int j = 0; j < C::KSTEPS; ++j) {
       u32x4 w = {0, 0, 0, 0};
-      if (r < sg.ncols) w = ld<u32x4>(qrow + C::qdim(j, c));
-      qb[j] = __builtin_bit_cast(bf16x8, w ^ qflip);
+      if (on[n]) w = ld<u32x4>(qrow + C::qdim(j, c));
+      qb[n][j] = __builtin_bit_cast(bf16x8, w ^ qflip);
     }
   }
 
   BlockIds ids{sg.row, j_hi, 0, id_lds};
   ids.fill(j_lo);
 
-  f32x4 acc[C::MT];
+  f32x4 acc[C::MT][NT];
 #pragma unroll
-  for (int m = 0; m < C::MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = kNegInf, l_run = 0.f;
+  for (int m = 0; m < C::MT; ++m)
+#pragma unroll
+    for (int n = 0; n < NT; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run[NT], l_run[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    m_run[n] = kNegInf;
+    l_run[n] = 0.f;
+  }
 
   const int npairs = (j_hi - j_lo + 1) >> 1;
-  auto step = [&](const MfmaPair<KV, D>& bf) { mfma_step<KV, D>(bf, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide); };
+  auto step = [&](const MfmaPair<KV, D>& bf) {
+    mfma_step<KV, D, NT>(bf, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
+  };
   auto issue = [&](MfmaPair<KV, D>& bf, int p) { mfma_issue<KV, D>(bf, a, ids, j_lo + 2 * p, j_hi, L, kvh, status); };
-  if constexpr (KV == KvType::BF16) {
-    // three pairs in flight (one wave per SIMD leaves the registers for it)
+  static_assert(DEPTH == 2 || DEPTH == 3, "pairs in flight");
+  if constexpr (DEPTH == 3) {
+    // three pairs in flight (one bf16 wave per SIMD leaves the registers for it)
     MfmaPair<KV, D> b0, b1, b2;
     if (npairs > 0) issue(b0, 0);
     if (npairs > 1) issue(b1, 1);
@@ -709,36 +762,39 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
     if (i + 2 < npairs) step(b0);
   }
 
-  // Lanes c = 0..3 hold disjoint token subsets of head r: total the denominator.
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-
-  if (r >= sg.ncols) return;
-  if (sg.final) {  // plain entry: column r is query token mem, head `head` of sequence qs
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    const int64_t orow = qo_row * D;
-    if (a.out_bf16) {
-      uint16_t* o = static_cast<uint16_t*>(a.out) + orow;
 #pragma unroll
-      for (int m = 0; m < C::MT; ++m) {
-        u32x2 w;
-        w.x = f32_to_bf16_bits(acc[m][0] * inv) | (f32_to_bf16_bits(acc[m][1] * inv) << 16);
-        w.y = f32_to_bf16_bits(acc[m][2] * inv) | (f32_to_bf16_bits(acc[m][3] * inv) << 16);
-        *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) = w;
+  for (int n = 0; n < NT; ++n) {
+    // Lanes c = 0..3 hold disjoint token subsets of column r: total the denominator.
+    float lt = l_run[n];
+    lt += __shfl_xor(lt, 16, 64);
+    lt += __shfl_xor(lt, 32, 64);
+    if (!on[n]) continue;
+    if (sg.final) {  // plain entry: the column is query token mem, head `head` of sequence qs
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+      const int64_t orow = qo_row[n] * D;
+      if (a.out_bf16) {
+        uint16_t* o = static_cast<uint16_t*>(a.out) + orow;
+#pragma unroll
+        for (int m = 0; m < C::MT; ++m) {
+          u32x2 w;
+          w.x = f32_to_bf16_bits(acc[m][n][0] * inv) | (f32_to_bf16_bits(acc[m][n][1] * inv) << 16);
+          w.y = f32_to_bf16_bits(acc[m][n][2] * inv) | (f32_to_bf16_bits(acc[m][n][3] * inv) << 16);
+          *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) = w;
+        }
+      } else {
+        float* o = static_cast<float*>(a.out) + orow;
+#pragma unroll
+        for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m][n] * inv;
       }
     } else {
-      float* o = static_cast<float*>(a.out) + orow;
+      const int64_t prow = sg.slot * a.Gp + 16 * n + r;
+      float* arow = a.ws_acc + prow * D;
 #pragma unroll
-      for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m] * inv;
-    }
-  } else {
-    const int64_t prow = sg.slot * a.Gp + r;
-    float* arow = a.ws_acc + prow * D;
-#pragma unroll
-    for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(arow + 16 * m + 4 * c) = acc[m];
-    if (c == 0) {
-      a.ws_m[prow] = m_run;
-      a.ws_l[prow] = l_run;
+      for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(arow + 16 * m + 4 * c) = acc[m][n];
+      if (c == 0) {
+        a.ws_m[prow] = m_run[n];
+        a.ws_l[prow] = lt;
+      }
     }
   }
 }
@@ -1055,8 +1111,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       const int j_hi = (int64_t)(nb - j_lo) <= room ? nb : j_lo + (int)room;
       const Seg sg{e.row, e.L, j_lo, j_hi, kvh, e.qs, e.ncols, e.may_final && j_lo == 0 && j_hi == nb,
                    (int64_t)v * a.Hkv + kvh + c};
-      if constexpr (V == Variant::Mfma) {
-        mfma_segment<KV, D>(a, sg, status, id_lds);
+      if constexpr (V == Variant::Mfma && GV == kWideColumns) {
+        // shared-prefix kernel: prefix entries may carry up to 32 columns
+        if (sg.ncols > 16) mfma_segment<KV, D, 2, 2>(a, sg, status, id_lds);
+        else mfma_segment<KV, D, 1, 2>(a, sg, status, id_lds);
+      } else if constexpr (V == Variant::Mfma) {
+        mfma_segment<KV, D, 1, KV == KvType::BF16 ? 3 : 2>(a, sg, status, id_lds);
       } else {
         vec_segment<KV, D, GV>(a, sg, status, id_lds);
       }
@@ -1323,15 +1383,17 @@ __global__ __launch_bounds__(kPrefixThreads) void prefix_kernel(DecodeArgs a) { 
 
 template <Variant V, KvType KV, int D, int GV>
 void* kernel_ptr() {
-  if constexpr (V == Variant::Mfma && KV == KvType::FP8) return reinterpret_cast<void*>(&decode_kernel_occ2<V, KV, D, GV>);
+  // the two-tile body of the wide kernel does not fit two fp8 waves per SIMD
+  if constexpr (V == Variant::Mfma && KV == KvType::FP8 && GV != kWideColumns)
+    return reinterpret_cast<void*>(&decode_kernel_occ2<V, KV, D, GV>);
   else if constexpr (V == Variant::Mfma) return reinterpret_cast<void*>(&decode_kernel<V, KV, D, GV>);
   else return reinterpret_cast<void*>(&decode_kernel_vec<V, KV, D, GV>);
 }
 
 template <Variant V, KvType KV, int D>
-void* pick_g(int G) {
+void* pick_g(int G, bool wide) {
   if constexpr (V == Variant::Mfma) {
-    return kernel_ptr<V, KV, D, 16>();
+    return wide ? kernel_ptr<V, KV, D, kWideColumns>() : kernel_ptr<V, KV, D, 16>();
   } else {
     if (G <= 1) return kernel_ptr<V, KV, D, 1>();
     if (G <= 2) return kernel_ptr<V, KV, D, 2>();
@@ -1341,25 +1403,26 @@ void* pick_g(int G) {
 }
 
 template <Variant V, KvType KV>
-void* pick_d(int D, int G) {
-  return D == 64 ? pick_g<V, KV, 64>(G) : pick_g<V, KV, 128>(G);
+void* pick_d(int D, int G, bool wide) {
+  return D == 64 ? pick_g<V, KV, 64>(G, wide) : pick_g<V, KV, 128>(G, wide);
 }
 
-void* pick(Variant v, KvType kv, int D, int G) {
+void* pick(Variant v, KvType kv, int D, int G, bool wide) {
   if (v == Variant::Mfma) {
-    if (kv == KvType::BF16) return pick_d<Variant::Mfma, KvType::BF16>(D, G);
-    if (kv == KvType::FP8) return pick_d<Variant::Mfma, KvType::FP8>(D, G);
+    if (kv == KvType::BF16) return pick_d<Variant::Mfma, KvType::BF16>(D, G, wide);
+    if (kv == KvType::FP8) return pick_d<Variant::Mfma, KvType::FP8>(D, G, wide);
     return nullptr;
   }
-  if (kv == KvType::F32) return pick_d<Variant::Vector, KvType::F32>(D, G);
-  if (kv == KvType::BF16) return pick_d<Variant::Vector, KvType::BF16>(D, G);
-  return pick_d<Variant::Vector, KvType::FP8>(D, G);
+  if (wide) return nullptr;
+  if (kv == KvType::F32) return pick_d<Variant::Vector, KvType::F32>(D, G, false);
+  if (kv == KvType::BF16) return pick_d<Variant::Vector, KvType::BF16>(D, G, false);
+  return pick_d<Variant::Vector, KvType::FP8>(D, G, false);
 }
 
 }  // namespace
 
 hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t s) {
-  void* fn = pick(v, kv, a.D, a.G);
+  void* fn = pick(v, kv, a.D, a.G, a.shared && a.Gp > 16);
   if (!fn) return hipErrorInvalidValue;
   DecodeArgs args = a;
   const void* q = a.q;
@@ -1396,8 +1459,8 @@ hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s) {
                          s);
 }
 
-hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, int* waves_per_cu) {
-  void* fn = pick(v, kv, D, G);
+hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, bool wide, int* waves_per_cu) {
+  void* fn = pick(v, kv, D, G, wide);
   if (!fn) return hipErrorInvalidValue;
   int wgs = 0;
   const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&wgs, fn, 64, 0);

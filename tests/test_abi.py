@@ -210,17 +210,25 @@ def test_shared_prefix_argument_checks():
 
 
 def test_shared_prefix_plan_and_workspace():
-    # GRPO step: 256 sequences = 32 groups of 8, 32/8 heads (G = 4): entries hold 4 members
-    # (16 query columns), so each group's shared blocks form 2 entries ahead of 256 suffix entries.
+    # GRPO step: 256 sequences = 32 groups of 8, 32/8 heads (G = 4): a prefix entry holds up to
+    # 32 / G = 8 members (32 query columns, two MFMA N-tiles), so each group's shared blocks form
+    # one entry ahead of 256 suffix entries.
     p = prob(num_seqs=256, num_q_heads=32, num_kv_heads=8, max_blocks_per_seq=2048)
     info = L.query_plan_shared_prefix(p, 8, L.make_options(waves_per_cu=4), num_compute_units=256)
     assert info.variant == L.VARIANT_MFMA and info.waves == 1024 and info.chunks_max == 1024
-    entries = 32 * 2 + 256
+    entries = 32 * 1 + 256
     slots = entries * 8 + info.chunks_max
     up = lambda x: (x + 255) // 256 * 256
-    gp = 4 * 4
+    gp = 8 * 4
     assert info.workspace_bytes == (up(64) + up(32 * 4) + up(entries * 4) + 2 * up(slots * gp * 4)
                                     + up(slots * gp * 128 * 4))
+    # G = 8, groups of 8: 4 members per entry (32 columns), 2 entries per group
+    p8 = prob(num_seqs=64, num_q_heads=64, num_kv_heads=8, max_blocks_per_seq=2048)
+    info = L.query_plan_shared_prefix(p8, 8, L.make_options(waves_per_cu=4), num_compute_units=256)
+    entries = 8 * 2 + 64
+    slots = entries * 8 + info.chunks_max
+    assert info.workspace_bytes == (up(64) + up(8 * 4) + up(entries * 4) + 2 * up(slots * 32 * 4)
+                                    + up(slots * 32 * 128 * 4))
     # G = 4 with a small group: a G < 4 batch also runs on the MFMA kernel in this mode
     assert L.query_plan_shared_prefix(prob(num_seqs=6, num_q_heads=4, num_kv_heads=4), 2).variant == L.VARIANT_MFMA
 

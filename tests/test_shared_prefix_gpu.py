@@ -44,7 +44,7 @@ SPLITS = {
     "dynamic": {"chunks_per_wave": 16, "min_blocks_per_chunk": 1, "min_blocks_per_wave": 1, "waves_per_cu": 1},
 }
 
-# (prompts, samples, Hq, Hkv, D, kv): G = 1, 2, 4, 7, 8, 16 (M = 16, 8, 4, 2, 2, 1 members per
+# (prompts, samples, Hq, Hkv, D, kv): G = 1, 2, 4, 7, 8, 16 (M = 32, 16, 8, 4, 4, 2 members per
 # prefix entry), groups smaller and larger than M (ragged last entry), group size 1.
 CASES = [
     (2, 8, 32, 8, 128, "bf16"),
