@@ -275,6 +275,24 @@ def source_digest(path):
     return hashlib.sha256(text.encode()).hexdigest()
 
 
+def per_call_spread(step, n, stream, first):
+    """GPU time of each of n more calls (us), every call between two HIP events
+    on the calls' stream, run after the timed region: events between calls add
+    their own GPU time, so this gives the spread (median, min, max) and the
+    headline figure stays the one of the timed region."""
+    import torch
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for i in range(n):
+        step(first + i)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    t = sorted(evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(n))
+    med = t[n // 2] if n % 2 else 0.5 * (t[n // 2 - 1] + t[n // 2])
+    return {"median": round(med, 2), "min": round(t[0], 2), "max": round(t[-1], 2), "calls": n}
+
+
 def measured_traffic(workload_name, per_launch_bytes, source=KERNEL_SOURCE):
     """HBM bytes per call from committed rocprofv3 FETCH_SIZE / WRITE_SIZE runs,
     or None when absent or taken on different kernel code."""
@@ -425,9 +443,11 @@ def main():
     wall = time.perf_counter() - t0
     call_ms = ev0.elapsed_time(ev1) / args.steps
     ms_per_step = wall * 1e3 / args.steps
+    spread = per_call_spread(step, args.steps, stream, args.steps)
     status = _lib.read_device_status()
     print(f"[bench] {w.name}: {ms_per_step * 1e3:.1f} us/step wall, {call_ms * 1e3:.1f} us/call GPU "
-          f"(HIP events over the timed region), {ncopies} cache copies, status {status}",
+          f"(HIP events over the timed region), {ncopies} cache copies, status {status}; single calls: "
+          f"median {spread['median']} us, min {spread['min']}, max {spread['max']}",
           file=sys.stderr, flush=True)
 
     achieved = nbytes / (call_ms * 1e-3) / 1e9
@@ -479,6 +499,7 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_call": nbytes,
             "call_us": round(call_ms * 1e3, 2),
+            "single_call_us": spread,
         },
         "cpu_baseline": None,
     }
@@ -538,8 +559,10 @@ def prefill_main(args, w, dev):
     wall = time.perf_counter() - t0
     call_ms = ev0.elapsed_time(ev1) / args.steps
     ms_per_step = wall * 1e3 / args.steps
+    spread = per_call_spread(step, args.steps, stream, args.steps)
     status = _lib.read_device_status()
-    print(f"[bench] {w.name}: {ms_per_step * 1e3:.1f} us/step wall, {call_ms * 1e3:.1f} us/call GPU, status {status}",
+    print(f"[bench] {w.name}: {ms_per_step * 1e3:.1f} us/step wall, {call_ms * 1e3:.1f} us/call GPU, status {status}; "
+          f"single calls: median {spread['median']} us, min {spread['min']}, max {spread['max']}",
           file=sys.stderr, flush=True)
     achieved = flops / (call_ms * 1e-3) / 1e12
     value = flops / (ms_per_step * 1e-3) / 1e12
@@ -583,6 +606,7 @@ def prefill_main(args, w, dev):
             "traffic": measured_traffic(w.name, flops, PREFILL_SOURCE),
             "algorithmic_flops_per_call": flops,
             "call_us": round(call_ms * 1e3, 2),
+            "single_call_us": spread,
         },
         "cpu_baseline": None,
     }

@@ -99,7 +99,7 @@ typedef struct pda_problem {
                                   [B, Q, Hq, D], the cache already holds the Q new tokens as the
                                   sequence's last Q, and query token i attends causally to tokens
                                   0 .. L - Q + i (zeros if none). Needs the MFMA kernel (bf16 or fp8
-                                  cache) and Q * G <= 16. */
+                                  cache) and Q * G <= 32. */
 } pda_problem;
 
 /* Optional tuning knobs; pass NULL for the defaults (all zero). */

@@ -131,8 +131,9 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
   if (Q > 1) {  // several query tokens: MFMA columns are (token, head) pairs
     if (kd == PDA_DTYPE_F32 || variant == PDA_VARIANT_VECTOR)
       return fail(PDA_EUNSUPPORTED, "q_tokens > 1 runs on the MFMA kernel: it needs a bf16 or fp8 KV cache");
-    if (Q * G > pda::kMaxGroup)
-      return fail(PDA_EUNSUPPORTED, "q_tokens * (num_q_heads / num_kv_heads) = %d exceeds %d", Q * G, pda::kMaxGroup);
+    if (Q * G > pda::kWideColumns)
+      return fail(PDA_EUNSUPPORTED, "q_tokens * (num_q_heads / num_kv_heads) = %d exceeds %d", Q * G,
+                  pda::kWideColumns);
     variant = PDA_VARIANT_MFMA;
   }
   if (variant == PDA_VARIANT_AUTO)
@@ -375,7 +376,7 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
 
   int wpc = plan.waves_per_cu;
   if (wpc == 0) {
-    const bool wide = gr.on && gr.M * plan.G > 16;
+    const bool wide = (gr.on ? gr.M * plan.G : plan.Q * plan.G) > 16;
     if ((rc = occupancy(dev, plan.variant, plan.kv, problem->head_dim, plan.G, wide, &wpc)) != PDA_OK) return rc;
     if (wpc > kDefaultWavesPerCu) wpc = kDefaultWavesPerCu;
   }

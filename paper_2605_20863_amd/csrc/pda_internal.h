@@ -11,7 +11,7 @@ constexpr int kBlockSize = 16;     // tokens per KV block
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kMaxGroup = 16;      // query heads per KV head (MFMA N dimension)
 constexpr int kMaxGroupVector = 8; // vector kernel keeps G x D/16 query values per lane
-constexpr int kWideColumns = 32;   // query columns of a shared-prefix entry (two MFMA N-tiles)
+constexpr int kWideColumns = 32;   // query columns of a wide entry (two MFMA N-tiles)
 
 enum class KvType : int { F32 = 0, BF16 = 1, FP8 = 2 };
 enum class Variant : int { Vector = 1, Mfma = 2 };
@@ -133,7 +133,8 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // Shared-prefix mode: the groups' real shared block counts, before the decode kernel.
 hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s);
 // Max resident waves per CU for the decode kernel that (v, kv, D, G) selects.
-// wide: the shared-prefix kernel whose prefix entries carry up to kWideColumns query columns
+// wide: the kernel whose entries carry up to kWideColumns query columns (shared-prefix
+// prefix entries, several query tokens per sequence)
 hipError_t decode_occupancy(Variant v, KvType kv, int D, int G, bool wide, int* waves_per_cu);
 
 }  // namespace pda

@@ -1112,7 +1112,8 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       const Seg sg{e.row, e.L, j_lo, j_hi, kvh, e.qs, e.ncols, e.may_final && j_lo == 0 && j_hi == nb,
                    (int64_t)v * a.Hkv + kvh + c};
       if constexpr (V == Variant::Mfma && GV == kWideColumns) {
-        // shared-prefix kernel: prefix entries may carry up to 32 columns
+        // wide kernel: shared-prefix prefix entries, or several query tokens
+        // per sequence, carry up to 32 columns
         if (sg.ncols > 16) mfma_segment<KV, D, 2, 2>(a, sg, status, id_lds);
         else mfma_segment<KV, D, 1, 2>(a, sg, status, id_lds);
       } else if constexpr (V == Variant::Mfma) {
@@ -1188,14 +1189,16 @@ constexpr int kCombineChunk = 8;  // segments whose loads are in flight together
 template <bool OUT_BF16, int D>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) {
   // the decode kernel has finished with the chunk counter: rearm it for the next call
-  if (blockIdx.x == 0 && threadIdx.x == 0) a.hdr[kHdrNext] = 0;
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) a.hdr[kHdrNext] = 0;
   const int u = blockIdx.x;
   const int b = u / a.Hkv;
   const int kvh = u - b * a.Hkv;
   const int G = a.G;
   const int tid = threadIdx.x;
-  // this sequence's columns for the KV head: G heads times its query tokens
+  // this sequence's columns for the KV head: G heads times its query tokens;
+  // workgroup y takes columns 16y .. 16y + 15 of them
   const int ncol = a.Qn * G;
+  const int cbase = 16 * (int)blockIdx.y;
   // Every value the segment ranges need, loaded at once (one round trip):
   // the length, the prefix sums of the sequence's entries and Q, and in
   // shared-prefix mode the group's shared blocks. All indices are in range in
@@ -1244,8 +1247,9 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   // output row of column r: query token r / G, head kvh * G + r % G of sequence b
   auto out_row = [&](int r) { return (((int64_t)b * a.Qn + r / G) * a.Hq + (int64_t)kvh * G + r % G) * D; };
   if (parts == 0) {
-    for (int i = tid; i < ncol * D; i += kCombineThreads) {
-      const int64_t at = out_row(i / D) + i % D;
+    const int nz = (ncol - cbase < 16 ? ncol - cbase : 16) * D;
+    for (int i = tid; i < nz; i += kCombineThreads) {
+      const int64_t at = out_row(cbase + i / D) + i % D;
       if constexpr (OUT_BF16) static_cast<uint16_t*>(a.out)[at] = 0;
       else static_cast<float*>(a.out)[at] = 0.f;
     }
@@ -1253,9 +1257,9 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   }
   if (parts == 1 && nseg[0] == 1 && own_may_final) return;  // one chunk wrote the output
 
-  // thread t owns column h = t / 16 (if < ncol) and dims [ (t % 16) * D/16, +D/16 )
+  // thread t owns column h = cbase + t / 16 (if < ncol) and dims [ (t % 16) * D/16, +D/16 )
   constexpr int DE = D / 16;
-  const int h = tid >> 4;
+  const int h = cbase + (tid >> 4);
   const int d0 = (tid & 15) * DE;
   if (h >= ncol) return;
   float acc[DE];
@@ -1422,7 +1426,7 @@ void* pick(Variant v, KvType kv, int D, int G, bool wide) {
 }  // namespace
 
 hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t s) {
-  void* fn = pick(v, kv, a.D, a.G, a.shared && a.Gp > 16);
+  void* fn = pick(v, kv, a.D, a.G, a.Gp > 16);
   if (!fn) return hipErrorInvalidValue;
   DecodeArgs args = a;
   const void* q = a.q;
@@ -1446,9 +1450,10 @@ hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
                    : reinterpret_cast<void*>(&combine_kernel<false, 128>);
   const unsigned units = (unsigned)a.B * (unsigned)a.Hkv;
   if (units == 0) return hipSuccess;
+  const unsigned halves = (unsigned)(a.Qn * a.G + 15) / 16;  // 16 columns per workgroup
   DecodeArgs args = a;
   void* params[] = {&args};
-  return hipLaunchKernel(fn, dim3(units), dim3(kCombineThreads), params, 0, s);
+  return hipLaunchKernel(fn, dim3(units, halves), dim3(kCombineThreads), params, 0, s);
 }
 
 hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s) {

@@ -135,6 +135,9 @@ WORKLOADS = {
     # (the drafted one and the next), 14 of the 16 MFMA columns.
     "spec2_gqa7b_bf16": Workload("spec2_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
                                  ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, q_tokens=2),
+    # 4 query tokens (three drafted): 28 columns, the two-tile MFMA body
+    "spec4_gqa7b_bf16": Workload("spec4_gqa7b_bf16", 64, 28, 4, 128, "bf16", "bf16",
+                                 ("lognormal", 2048, 0.8, 64, 16384), cfg_id=1, q_tokens=4),
 }
 
 # Reduced versions with the same heads, dtypes and length structure, sized so the

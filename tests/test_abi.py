@@ -260,10 +260,10 @@ def test_append_argument_checks():
 
 def test_multi_token_checks_and_plan():
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=-1)) == L.EINVAL
-    # several query tokens need the MFMA kernel (bf16 / fp8 cache) and Q * G <= 16
+    # several query tokens need the MFMA kernel (bf16 / fp8 cache) and Q * G <= 32
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1,
                       prob(q_tokens=2, q_dtype=L.F32, kv_dtype=L.F32)) == L.EUNSUPPORTED
-    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=5)) == L.EUNSUPPORTED   # G = 4: 20 columns
+    assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=9)) == L.EUNSUPPORTED   # G = 4: 36 columns
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=4),
                       L.make_options("vector")) == L.EUNSUPPORTED
     assert L.raw_call_shared_prefix(16, 16, 16, 16, 16, 16, 16, 0.1, 2, 16, prob(q_tokens=2)) == L.EUNSUPPORTED
@@ -274,6 +274,12 @@ def test_multi_token_checks_and_plan():
     slots = 64 * 4 + info.chunks_max
     up = lambda x: (x + 255) // 256 * 256
     assert info.workspace_bytes == up(64) + up(64 * 4) + 2 * up(slots * 8 * 4) + up(slots * 8 * 128 * 4)
+    # Q = 8, G = 4: 32 columns (the two-tile kernel), partial rows of 32 columns
+    p = prob(num_seqs=64, num_q_heads=8, num_kv_heads=2, q_tokens=8)
+    info = L.query_plan(p, L.make_options(waves_per_cu=4), num_compute_units=256)
+    assert info.variant == L.VARIANT_MFMA
+    slots = 64 * 2 + info.chunks_max
+    assert info.workspace_bytes == up(64) + up(64 * 4) + 2 * up(slots * 32 * 4) + up(slots * 32 * 128 * 4)
 
 
 def pprob(**kw):

@@ -59,9 +59,12 @@ SPLITS = {
     "unsplit": {"min_blocks_per_wave": 1 << 20},
 }
 
-# (Q, Hq, Hkv, D, kv): Q * G columns from 6 to 16
+# (Q, Hq, Hkv, D, kv): Q * G columns from 6 to 32 (above 16: the two-tile
+# body, whose second tile is partly or wholly used)
 CASES = [(2, 8, 2, 128, "bf16"), (4, 16, 4, 128, "bf16"), (3, 8, 4, 64, "bf16"), (8, 16, 8, 64, "bf16"),
-         (16, 8, 8, 128, "bf16"), (4, 16, 4, 128, "fp8_e4m3"), (2, 64, 8, 128, "fp8_e4m3")]
+         (16, 8, 8, 128, "bf16"), (4, 16, 4, 128, "fp8_e4m3"), (2, 64, 8, 128, "fp8_e4m3"),
+         (4, 28, 4, 128, "bf16"), (8, 8, 2, 128, "bf16"), (32, 4, 4, 64, "bf16"), (17, 4, 4, 128, "bf16"),
+         (9, 4, 2, 128, "fp8_e4m3"), (3, 56, 8, 64, "fp8_e4m3")]
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: f"Q{c[0]}_G{c[1] // c[2]}_D{c[3]}_{c[4]}")
@@ -100,9 +103,9 @@ def test_multitoken_peaked_fp32_out(lib):
 
 
 def test_multitoken_full_size_sampled(lib):
-    """Speculative verification of 4 tokens on the 7B GQA shape at full size
-    (G = 7 does not fit 4 tokens in 16 columns, so 2 KV heads per query group
-    of 4: 8 / 2 heads), checked on sampled sequences."""
+    """Speculative verification of 4 tokens at full size on one N-tile (the
+    7B lengths with 8 / 2 heads: G = 4, 16 columns), checked on sampled
+    sequences."""
     w = W.WORKLOADS["gqa7b_bf16"].replace(name="mt_full", num_q_heads=8, num_kv_heads=2)
     inp = W.generate(w, DEV)
     q = queries(inp, 4, seed=9)
@@ -112,4 +115,20 @@ def test_multitoken_full_size_sampled(lib):
     seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(len(lens), 3, replace=False).tolist()})
     ref = reference(inp, q, seqs)
     U.assert_close(U.out_to_f64(got)[seqs], ref, "bf16", "multi-token full size")
+    assert lib.read_device_status() == 0
+
+
+def test_multitoken_wide_full_size_sampled(lib):
+    """4 query tokens on the 7B GQA step itself (28 / 4 heads, G = 7: 28
+    columns in the two-tile body), checked on sampled sequences."""
+    w = W.WORKLOADS["spec4_gqa7b_bf16"]
+    inp = W.generate(w, DEV)
+    q = inp.q                                   # [64, 4, 28, 128]
+    assert q.shape[1] == 4
+    got = run(lib, inp, q)
+    lens = inp.layout.seq_lens
+    rng = np.random.default_rng(4)
+    seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(len(lens), 3, replace=False).tolist()})
+    ref = reference(inp, q, seqs)
+    U.assert_close(U.out_to_f64(got)[seqs], ref, "bf16", "wide multi-token full size")
     assert lib.read_device_status() == 0

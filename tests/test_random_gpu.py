@@ -50,8 +50,8 @@ def test_random_decode(lib, seed):
     if kv == "f32":
         G = min(G, 8)
     Q = 1
-    if kv != "f32" and G <= 8 and rng.random() < 0.4:
-        Q = int(rng.integers(2, 16 // G + 1)) if 16 // G >= 2 else 1
+    if kv != "f32" and G <= 16 and rng.random() < 0.4:
+        Q = int(rng.integers(2, 32 // G + 1))
     variants = ["auto"]
     if Q == 1 and G <= 8:
         variants.append("vector")
