@@ -137,6 +137,15 @@ typedef struct pda_plan_info {
  * grown on demand (growth synchronises that stream) and released by
  * pda_release_workspaces().
  *
+ * HIP graphs: once the stream's workspace is large enough (a call of the same
+ * or a larger size has run on it), a call enqueues kernel launches only, so it
+ * can be captured into a graph and replayed; the captured launches keep the
+ * pointers and sizes of the capture, and inputs may change in place between
+ * replays. A call that would grow the workspace during capture returns
+ * PDA_EINVAL instead of allocating; growth after a capture keeps the old
+ * allocation for the graph until pda_release_workspaces(), after which no
+ * graph captured before may be replayed. This holds for every call below.
+ *
  * Errors: all argument checks run on the host before any HIP call, so invalid
  * arguments return PDA_EINVAL / PDA_EUNSUPPORTED without touching a device.
  * Returns PDA_OK once the kernels are enqueued.

@@ -19,6 +19,7 @@
 #include <string>
 #include <tuple>
 #include <utility>
+#include <vector>
 
 namespace {
 
@@ -238,6 +239,10 @@ struct Workspace {
   // The combine kernel zeroes the chunk counter after each decode kernel; if a
   // combine launch failed, the next call zeroes it first.
   bool rearm = false;
+  // A graph captured on the stream holds `ptr`: growth then keeps the old
+  // allocation (in `retired`) so that replays stay valid.
+  bool captured = false;
+  std::vector<void*> retired;
 };
 
 std::mutex g_mu;
@@ -292,13 +297,31 @@ Workspace* workspace_for(int dev, hipStream_t s) {
   return slot.get();
 }
 
+// True while `s` records into a HIP graph: allocation, frees, waits and
+// memsets must then stay out of the call.
+bool capturing(hipStream_t s) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  return hipStreamIsCapturing(s, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
+}
+
 // Grow ws (caller holds ws->mu) to at least `bytes`; growth waits for `s`.
 int ensure_workspace(Workspace* ws, int64_t bytes, hipStream_t s) {
+  const bool cap = capturing(s);
+  if (cap) ws->captured = true;
   if (ws->bytes >= bytes) return PDA_OK;
+  if (cap)
+    return fail(PDA_EINVAL,
+                "the stream's workspace must grow to %lld bytes, which cannot be recorded into a graph: make one "
+                "call of this size (or larger) on the stream before capturing it",
+                (long long)bytes);
   hipError_t e;
   if (ws->ptr) {
-    if ((e = hipStreamSynchronize(s)) != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
-    if ((e = hipFree(ws->ptr)) != hipSuccess) return fail_hip(e, "hipFree");
+    if (ws->captured) {
+      ws->retired.push_back(ws->ptr);
+    } else {
+      if ((e = hipStreamSynchronize(s)) != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+      if ((e = hipFree(ws->ptr)) != hipSuccess) return fail_hip(e, "hipFree");
+    }
     ws->ptr = nullptr;
     ws->bytes = 0;
   }
@@ -389,6 +412,8 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   if ((rc = ensure_workspace(ws, lay.total, stream)) != PDA_OK) return rc;
   char* base = static_cast<char*>(ws->ptr);
   if (ws->rearm) {
+    if (capturing(stream))
+      return fail(PDA_EINVAL, "the workspace needs a reset after a failed launch: make one call outside capture");
     if ((e = hipMemsetAsync(base + pda::kHdrNext * 4, 0, 4, stream)) != hipSuccess)
       return fail_hip(e, "hipMemsetAsync");
     ws->rearm = false;
@@ -666,12 +691,23 @@ int pda_read_device_status(hipStream_t stream) {
   Workspace* ws = workspace_for(dev, stream);
   std::lock_guard<std::mutex> lk(ws->mu);
   if ((e = hipStreamSynchronize(stream)) != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
-  if (!ws->ptr) return 0;
-  int32_t word = 0;
-  int32_t* hdr = static_cast<int32_t*>(ws->ptr) + pda::kHdrStatus;
-  if ((e = hipMemcpy(&word, hdr, 4, hipMemcpyDeviceToHost)) != hipSuccess) return fail_hip(e, "hipMemcpy");
-  if (word && (e = hipMemset(hdr, 0, 4)) != hipSuccess) return fail_hip(e, "hipMemset");
-  return word;
+  // the current workspace and any a captured graph still writes to
+  int32_t all = 0;
+  for (void* p : ws->retired) {
+    int32_t word = 0;
+    int32_t* hdr = static_cast<int32_t*>(p) + pda::kHdrStatus;
+    if ((e = hipMemcpy(&word, hdr, 4, hipMemcpyDeviceToHost)) != hipSuccess) return fail_hip(e, "hipMemcpy");
+    if (word && (e = hipMemset(hdr, 0, 4)) != hipSuccess) return fail_hip(e, "hipMemset");
+    all |= word;
+  }
+  if (ws->ptr) {
+    int32_t word = 0;
+    int32_t* hdr = static_cast<int32_t*>(ws->ptr) + pda::kHdrStatus;
+    if ((e = hipMemcpy(&word, hdr, 4, hipMemcpyDeviceToHost)) != hipSuccess) return fail_hip(e, "hipMemcpy");
+    if (word && (e = hipMemset(hdr, 0, 4)) != hipSuccess) return fail_hip(e, "hipMemset");
+    all |= word;
+  }
+  return all;
 }
 
 int pda_release_workspaces(void) {
@@ -683,13 +719,16 @@ int pda_release_workspaces(void) {
   for (auto& kv : g_workspaces) {
     Workspace* ws = kv.second.get();
     std::lock_guard<std::mutex> wl(ws->mu);
-    if (!ws->ptr) continue;
+    if (!ws->ptr && ws->retired.empty()) continue;
     hipError_t e = hipSetDevice(kv.first.first);
     if (e == hipSuccess) e = hipDeviceSynchronize();
-    if (e == hipSuccess) e = hipFree(ws->ptr);
+    if (e == hipSuccess && ws->ptr) e = hipFree(ws->ptr);
+    for (void* p : ws->retired)
+      if (e == hipSuccess) e = hipFree(p);
     if (e != hipSuccess) rc = fail_hip(e, "releasing a workspace");
     ws->ptr = nullptr;
     ws->bytes = 0;
+    ws->retired.clear();
   }
   g_workspaces.clear();
   if (have_dev) (void)hipSetDevice(cur);
