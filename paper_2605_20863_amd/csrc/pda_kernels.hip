@@ -25,6 +25,9 @@
 //     S^T[16 tok x 16 heads] = K[16 x D] . Q^T[D x 16] on v_mfma_f32_16x16x32_bf16
 //     (the GQA group's G <= 16 heads padded to 16 columns), online softmax on
 //     the accumulator registers, then O^T[D x 16] += V^T[D x 32 tok] . P^T[32 x 16].
+//     An entry with 17 to 32 columns (several query tokens per sequence, or a
+//     shared-prefix entry serving several sequences) runs two such N-tiles on
+//     the same K and V operands.
 //     The score tiles' token rows are ordered so that each lane's accumulators
 //     hold the weights of 8 consecutive tokens of one block, exactly what its
 //     P^T operand needs: P never moves between lanes, and the lane's V^T
@@ -655,12 +658,13 @@ __device__ __forceinline__ void mfma_step(const MfmaPair<KV, D>& bf, const bf16x
     mfma_compute<KV, D, true, NT>(bf, qb, scale_log2, acc, m_run, l_run, hide);
 }
 
-// NT N-tiles of 16 query columns: 1 for plain entries, 2 for the prefix
-// entries of shared-prefix mode (up to 32 members' heads per shared block).
-// DEPTH pairs in flight: 3 or 2 (the two-tile body has the registers for 2;
-// the shared-prefix kernel gives every segment the same depth, so the waves
-// that carry prefix entries keep as many bytes in flight as the others and
-// take an even share of the bandwidth).
+// NT N-tiles of 16 query columns: 1 for entries of up to 16 columns, 2 for
+// up to 32 (the prefix entries of shared-prefix mode, with several members'
+// heads per shared block, or several query tokens per sequence). DEPTH pairs
+// in flight: 3 or 2 (the two-tile body has the registers for 2; the wide
+// kernel gives every segment the same depth, so the waves that carry two-tile
+// entries keep as many bytes in flight as the others and take an even share
+// of the bandwidth).
 template <KvType KV, int D, int NT, int DEPTH>
 __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds) {
   using C = MfmaCfg<KV, D>;
