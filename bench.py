@@ -334,8 +334,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build is a single-GPU kernel library "
-              "(sharding across GPUs is described in DESIGN.md, not implemented); run with --gpus 1",
+        print("bench.py measures one GPU: the library has no multi-GPU path (the step shards by sequence "
+              "or by KV head with no exchange, but nothing here launches on several GPUs); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 
