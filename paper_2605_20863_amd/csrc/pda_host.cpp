@@ -98,8 +98,8 @@ int validate(const pda_problem* pr, const pda_options* op, float softmax_scale, 
   if (pr->num_blocks < 1) return fail(PDA_EINVAL, "num_blocks = %lld < 1", (long long)pr->num_blocks);
   const int64_t table_tokens = (int64_t)pr->max_blocks_per_seq * pda::kBlockSize;
   if (table_tokens > INT32_MAX) return fail(PDA_EINVAL, "max_blocks_per_seq * 16 overflows int32");
-  if ((int64_t)pr->num_seqs * pr->max_blocks_per_seq * pr->num_kv_heads > INT32_MAX)
-    return fail(PDA_EINVAL, "num_seqs * max_blocks_per_seq * num_kv_heads overflows int32");
+  if ((int64_t)pr->num_seqs * ((int64_t)pr->max_blocks_per_seq + pda::kUnitCostPlain) * pr->num_kv_heads > INT32_MAX)
+    return fail(PDA_EINVAL, "num_seqs * (max_blocks_per_seq + %d) * num_kv_heads overflows int32", pda::kUnitCostPlain);
   if ((int64_t)pr->num_seqs * pr->num_q_heads > INT32_MAX) return fail(PDA_EINVAL, "num_seqs * num_q_heads too large");
   if (pr->max_seq_len < 0) return fail(PDA_EINVAL, "max_seq_len = %d < 0", pr->max_seq_len);
   if (pr->max_seq_len > table_tokens)
@@ -199,8 +199,10 @@ int validate_groups(const pda_problem* pr, int32_t group_size, const int32_t* sh
   gr->num_groups = pr->num_seqs / group_size;
   gr->n_prefix = (int64_t)gr->num_groups * gr->nsub;
   gr->shared_blocks = shared_blocks;
-  if ((gr->n_prefix + pr->num_seqs) * pr->max_blocks_per_seq * pr->num_kv_heads > INT32_MAX)
-    return fail(PDA_EINVAL, "(entries) * max_blocks_per_seq * num_kv_heads overflows int32");
+  if ((gr->n_prefix + pr->num_seqs) * pr->num_kv_heads *
+          ((int64_t)pr->max_blocks_per_seq + pda::kUnitCostShared) > INT32_MAX)
+    return fail(PDA_EINVAL, "(entries) * num_kv_heads * (max_blocks_per_seq + %d) overflows int32",
+                pda::kUnitCostShared);
   return PDA_OK;
 }
 

@@ -12,6 +12,15 @@ constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kMaxGroup = 16;      // query heads per KV head (MFMA N dimension)
 constexpr int kMaxGroupVector = 8; // vector kernel keeps G x D/16 query values per lane
 constexpr int kWideColumns = 32;   // query columns of a wide entry (two MFMA N-tiles)
+// The stream-K split cuts a stream in which every block-head is one unit of
+// work and every (entry, KV head) with blocks costs this many more before its
+// first block: a wave's fixed cost of starting a segment (query loads, the
+// load pipeline filling, the partial's write; about two block-heads' time for
+// a one-tile segment, more for a two-tile one with twice the query columns
+// and partial), so waves whose chunks cross many short units get fewer
+// blocks. In shared-prefix mode and in plain mode.
+constexpr int kUnitCostShared = 4;
+constexpr int kUnitCostPlain = 2;
 
 enum class KvType : int { F32 = 0, BF16 = 1, FP8 = 2 };
 enum class Variant : int { Vector = 1, Mfma = 2 };
@@ -31,6 +40,10 @@ constexpr int kHdrItems = 3;  // prefill: work items the plan kernel listed
 constexpr int kHdrWords = 16;
 
 // Everything one decode step's kernels need. Plain data; passed by value.
+// The decode kernels keep it in registers; two more int32 fields once made
+// the compiler place the whole struct in scratch memory (248 bytes per lane,
+// every kernel), so a new field is worth checking with the resource-usage
+// remarks.
 struct DecodeArgs {
   const void* q;
   const void* k_cache;
@@ -46,7 +59,7 @@ struct DecodeArgs {
   int32_t max_blocks;   // block_table row stride
   int64_t num_blocks;   // physical blocks (for the bounds check of table entries)
   int32_t len_cap;      // lengths are clamped into [0, len_cap]
-  int32_t min_share;    // smallest chunk, in block-heads
+  int32_t min_share;    // smallest chunk, in stream units (block-heads plus unit start costs)
   int32_t chunk_min;    // a dynamic split makes no chunk smaller than this
   int32_t chunks_max;   // at most this many chunks; <= waves means a static split
   int32_t waves;        // launched persistent waves (a multiple of waves_per_group)

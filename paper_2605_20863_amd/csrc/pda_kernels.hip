@@ -195,6 +195,10 @@ __device__ __forceinline__ Entry entry_of(const DecodeArgs& a, int v) {
   return e;
 }
 
+// Stream units a (entry, KV head) unit with blocks costs before its first
+// block (see kUnitCostShared); every block-head is one unit.
+__device__ __forceinline__ int unit_cost(const DecodeArgs& a) { return a.shared ? kUnitCostShared : kUnitCostPlain; }
+
 // Stream-K plan, computed by every wave from seq_lens. The stream of
 // block-heads is cut into chunks of Q block-heads, chunk c covering
 // [c*Q, (c+1)*Q). In a static split Q = ceil(total / waves) and wave w runs
@@ -250,6 +254,7 @@ __device__ __forceinline__ int load_tile(const DecodeArgs& a, int t0, int (&incl
       n = (L + kBlockSize - 1) / kBlockSize - sh[i];
       n = n > 0 ? n : 0;
     }
+    n = n > 0 ? n + unit_cost(a) : 0;  // stream units
     run += n;
     incl[i] = run;
   }
@@ -1102,30 +1107,42 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     while (pos < end && v < a.E) {
       const Entry e = entry_of(a, v);
       const int nb = e.nb;
+      // the entry's units in stream units: KV head kvh's blocks occupy
+      // [base + kvh * nbw, base + (kvh + 1) * nbw), block j starting at j * wt
+      // (offsets within an entry fit in 32 bits: the host bounds entries *
+      // blocks * KV heads * weight by INT32_MAX)
+      const int f = nb > 0 ? unit_cost(a) : 0;  // block j starts at f + j
+      const int nbw = f + nb;
       const int64_t base = (int64_t)cum_v * a.Hkv;
-      if (pos >= base + (int64_t)nb * a.Hkv) {
-        cum_v += nb;
+      if (pos >= base + (int64_t)nbw * a.Hkv) {
+        cum_v += nbw;
         ++v;
         continue;
       }
-      const int64_t rel = pos - base;
-      const int kvh = (int)(rel / nb);
-      const int j_lo = (int)(rel - (int64_t)kvh * nb);
-      const int64_t room = end - pos;
-      const int j_hi = (int64_t)(nb - j_lo) <= room ? nb : j_lo + (int)room;
-      const Seg sg{e.row, e.L, j_lo, j_hi, kvh, e.qs, e.ncols, e.may_final && j_lo == 0 && j_hi == nb,
-                   (int64_t)v * a.Hkv + kvh + c};
-      if constexpr (V == Variant::Mfma && GV == kWideColumns) {
-        // wide kernel: shared-prefix prefix entries, or several query tokens
-        // per sequence, carry up to 32 columns
-        if (sg.ncols > 16) mfma_segment<KV, D, 2, 2>(a, sg, status, id_lds);
-        else mfma_segment<KV, D, 1, 2>(a, sg, status, id_lds);
-      } else if constexpr (V == Variant::Mfma) {
-        mfma_segment<KV, D, 1, KV == KvType::BF16 ? 3 : 2>(a, sg, status, id_lds);
-      } else {
-        vec_segment<KV, D, GV>(a, sg, status, id_lds);
+      const int rel = (int)(pos - base);
+      const int kvh = rel / nbw;
+      const int r0 = rel - kvh * nbw;  // pos within the unit
+      const int64_t u0 = pos - r0;     // the unit's first stream unit
+      const int r_end = end - u0 < nbw ? (int)(end - u0) : nbw;
+      // this chunk's blocks: those that start in [pos, end)
+      const int j_lo = r0 > f ? r0 - f : 0;
+      const int j_hi = r_end > f ? r_end - f : 0;
+      if (j_lo < j_hi) {
+        const Seg sg{e.row, e.L, j_lo, j_hi, kvh, e.qs, e.ncols, e.may_final && j_lo == 0 && j_hi == nb,
+                     (int64_t)v * a.Hkv + kvh + c};
+        if constexpr (V == Variant::Mfma && GV == kWideColumns) {
+          // wide kernel: shared-prefix prefix entries, or several query tokens
+          // per sequence, carry up to 32 columns
+          if (sg.ncols > 16) mfma_segment<KV, D, 2, 2>(a, sg, status, id_lds);
+          else mfma_segment<KV, D, 1, 2>(a, sg, status, id_lds);
+        } else if constexpr (V == Variant::Mfma) {
+          mfma_segment<KV, D, 1, KV == KvType::BF16 ? 3 : 2>(a, sg, status, id_lds);
+        } else {
+          vec_segment<KV, D, GV>(a, sg, status, id_lds);
+        }
       }
-      pos += j_hi - j_lo;
+      // on to the start of block j_hi, or past the unit
+      pos = u0 + (j_hi < nb ? f + j_hi : nbw);
     }
     c = dynamic ? (int64_t)a.waves + uni(ticket) : plan.nchunks;
   }
@@ -1232,8 +1249,12 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
   const int nb_raw = (Lf + kBlockSize - 1) / kBlockSize - S_own;
   const int own_nb = nb_raw > 0 ? nb_raw : 0;
   const bool own_may_final = S_own == 0;
+  // a unit's segments: the chunks from the one holding its first block to
+  // the one holding its last (its start cost, before the first block, may
+  // end a chunk that holds none of its blocks)
   if (own_nb > 0) {
-    const int64_t start = (int64_t)cum_own * a.Hkv + (int64_t)kvh * own_nb;
+    const int f = unit_cost(a);
+    const int64_t start = (int64_t)cum_own * a.Hkv + (int64_t)kvh * (f + own_nb) + f;
     const int64_t w0 = start / share;
     nseg[parts] = (int)((start + own_nb - 1) / share - w0) + 1;
     slot0[parts] = (int64_t)v_own * a.Hkv + kvh + w0;
@@ -1241,7 +1262,8 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(DecodeArgs a) 
     ++parts;
   }
   if (a.shared && S > 0) {  // the group's prefix entry: columns of member i
-    const int64_t start = (int64_t)cum_pre * a.Hkv + (int64_t)kvh * S;
+    const int f = unit_cost(a);
+    const int64_t start = (int64_t)cum_pre * a.Hkv + (int64_t)kvh * (f + S) + f;
     const int64_t w0 = start / share;
     nseg[parts] = (int)((start + S - 1) / share - w0) + 1;
     slot0[parts] = (int64_t)v_pre * a.Hkv + kvh + w0;
