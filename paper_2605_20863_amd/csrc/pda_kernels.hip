@@ -8,10 +8,11 @@
 // how lengths are distributed:
 //
 // * Stream-K split. The (sequence, KV head) units are laid end to end as one
-//   stream of 16-token block-heads (sequence-major, KV head minor), cut into
-//   equal chunks. By default wave w of a persistent grid takes chunk w, the
-//   range [w*Q, (w+1)*Q) with Q = ceil(total / waves), so every wave reads the
-//   same number of KV bytes no matter how lengths are distributed; optionally
+//   stream of 16-token block-heads (sequence-major, KV head minor), each unit
+//   preceded by a small start cost (a segment's fixed work, in block-heads),
+//   and the stream is cut into equal chunks. By default wave w of a persistent
+//   grid takes chunk w, the range [w*Q, (w+1)*Q) with Q = ceil(total / waves),
+//   so every wave does the same work no matter how lengths are distributed; optionally
 //   the chunks are smaller and the waves take the rest from a counter in
 //   arrival order. A chunk that covers a whole unit writes its normalised
 //   output; otherwise it writes the unit's partial softmax state (m, l, acc)
@@ -199,9 +200,10 @@ __device__ __forceinline__ Entry entry_of(const DecodeArgs& a, int v) {
 // block (see kUnitCostShared); every block-head is one unit.
 __device__ __forceinline__ int unit_cost(const DecodeArgs& a) { return a.shared ? kUnitCostShared : kUnitCostPlain; }
 
-// Stream-K plan, computed by every wave from seq_lens. The stream of
-// block-heads is cut into chunks of Q block-heads, chunk c covering
-// [c*Q, (c+1)*Q). In a static split Q = ceil(total / waves) and wave w runs
+// Stream-K plan, computed by every wave from seq_lens. The stream (each
+// unit's start cost, then its block-heads, one stream unit each) is cut into
+// chunks of Q stream units, chunk c covering [c*Q, (c+1)*Q); a chunk runs the
+// blocks that start in it. In a static split Q = ceil(total / waves) and wave w runs
 // chunk w only. In a dynamic split Q is smaller (chunks_max > waves chunks at
 // most, none below chunk_min): wave w starts on chunk w and then takes chunks
 // waves, waves + 1, ... in arrival order from a counter in the workspace
