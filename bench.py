@@ -471,6 +471,7 @@ def main():
         "data": "synthetic",
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "kv_tokens_per_s": round(tokens / (ms_per_step * 1e-3), 1),
+        "kv_token_heads_per_s": round(tokens * w.num_kv_heads / (ms_per_step * 1e-3), 1),
         "config": {
             "workload": w.name,
             "num_seqs": len(lens),
@@ -497,6 +498,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
+            "traffic_over_algorithmic": round(traffic / nbytes, 4) if traffic else None,
             "algorithmic_bytes_per_call": nbytes,
             "call_us": round(call_ms * 1e3, 2),
             "single_call_us": spread,
