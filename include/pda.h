@@ -126,10 +126,11 @@ typedef struct pda_plan_info {
 /*
  * One batched decode-attention step, enqueued on `stream` (a hipStream_t; NULL
  * is the null stream). Asynchronous: results are valid once the stream has
- * reached this point. The step's KV blocks are cut into equal chunks that
- * persistent waves take in turn (each wave its own first chunk, the rest in
- * arrival order); a sequence split between chunks is finished by a
- * log-sum-exp combine kernel on the same stream. The result does not depend
+ * reached this point. The step's KV blocks (16 tokens of one KV head each,
+ * plus a small start cost per sequence and KV head counted in the same units)
+ * are cut into equal chunks that persistent waves take in turn (each wave its
+ * own first chunk, the rest in arrival order); a sequence split between
+ * chunks is finished by a log-sum-exp combine kernel on the same stream. The result does not depend
  * on which wave ran which chunk: repeated calls give identical output.
  *
  * Ownership: the caller owns every buffer; the library keeps no pointer to
