@@ -132,3 +132,20 @@ def test_multitoken_wide_full_size_sampled(lib):
     ref = reference(inp, q, seqs)
     U.assert_close(U.out_to_f64(got)[seqs], ref, "bf16", "wide multi-token full size")
     assert lib.read_device_status() == 0
+
+
+def test_multitoken_wide_fp8_full_size_sampled(lib):
+    """4 query tokens on the fp8 step's TP-8 share at full size (8 / 1 heads,
+    G = 8: all 32 columns of the two-tile body, fp8 e4m3 cache with per-block
+    scales, lengths up to 64k), checked on sampled sequences."""
+    w = W.WORKLOADS["fp8kv_tp8"].replace(name="mt_fp8_wide", q_tokens=4)
+    inp = W.generate(w, DEV)
+    q = inp.q
+    assert q.shape[1] == 4
+    got = run(lib, inp, q)
+    lens = inp.layout.seq_lens
+    rng = np.random.default_rng(6)
+    seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(len(lens), 3, replace=False).tolist()})
+    ref = reference(inp, q, seqs)
+    U.assert_close(U.out_to_f64(got)[seqs], ref, "fp8_e4m3", "wide multi-token fp8 full size")
+    assert lib.read_device_status() == 0
