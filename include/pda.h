@@ -266,7 +266,11 @@ typedef struct pda_append_problem {
  * A position at or past 16 * max_blocks_per_seq, or a block-table entry
  * outside [0, num_blocks), skips that sequence and sets status bit 1 or 2
  * (pda_read_device_status). Two sequences writing the same (block, slot) in
- * one call race; sequences normally append to private blocks.
+ * one call race. For an fp8 cache the unit of a write is the whole (block, KV
+ * head) tile: a new token may raise the tile's K and V scales and re-encode
+ * the tile's earlier codes, so two sequences of one call must not append into
+ * the same block at all, not even into different slots. Sequences normally
+ * append to private blocks (a shared prompt's blocks are full and read-only).
  *
  * Errors: all checks run on the host before any HIP call: PDA_EINVAL for bad
  * sizes, dtypes or NULL pointers, PDA_EUNSUPPORTED for head_dim not in {64,
@@ -301,9 +305,10 @@ typedef struct pda_prefill_problem {
 /*
  * Causal attention of many query tokens per sequence over the paged cache,
  * enqueued on `stream`: the log-prob forward of RLVR training (the
- * compute_log_prob phase of the paper's Sec. 6.2 breakdown, a forward call of
- * its Sec. 3 interface) and chunked prefill. The cache already holds every
- * token's key and value (pda_paged_kv_append, or the caller's own writes).
+ * compute_log_prob phase timed in the paper's Table 2, Sec. 6.3; a forward call
+ * of the remote execution interface of its Sec. 4.2) and chunked prefill. The
+ * cache already holds every token's key and value (pda_paged_kv_append, or the
+ * caller's own writes).
  *
  *   q            [T, Hq, D] bf16: rows q_offsets[b] .. q_offsets[b+1]-1 are the
  *                last n_b = q_offsets[b+1] - q_offsets[b] tokens of sequence b

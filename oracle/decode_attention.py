@@ -217,8 +217,8 @@ def paged_prefill_attention(q, q_offsets, k_cache, v_cache, block_table, seq_len
     """Reference output of a variable-length prefill over the paged cache,
     float64 [T, Hq, D] (rows of the listed ``seqs`` only when given; others 0).
 
-    The log-prob forward of RLVR training (the compute_log_prob phase of the
-    paper's Sec. 6.2 phase breakdown, one of the forward calls of its Sec. 3
+    The log-prob forward of RLVR training (the compute_log_prob phase timed in
+    the paper's Table 2, Sec. 6.3, one of the forward calls of its Sec. 4.2
     interface) and chunked prefill run attention for many query tokens per
     sequence at once. Packed q rows q_offsets[b] .. q_offsets[b + 1] - 1 are
     the last n_b tokens of sequence b (whose cache holds all L_b tokens), so

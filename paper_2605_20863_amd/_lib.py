@@ -355,6 +355,19 @@ def paged_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, posi
     float32 or bfloat16) into the paged cache at ``positions`` (int32 [B]);
     layouts as for paged_decode_attention. fp8 caches update ``kv_scales``."""
     torch = _torch()
+    # Shapes first: the kernel reads block_table[b, :] for every b < B, so a
+    # table with fewer rows (or a flat one) would be read past its end.
+    if k_new.dim() != 3 or v_new.shape != k_new.shape or v_new.dtype != k_new.dtype:
+        raise ValueError("k_new and v_new must both be [B, Hkv, D] with one dtype")
+    B, hkv, d = k_new.shape
+    if k_cache.dim() != 4 or v_cache.dim() != 4:
+        raise ValueError("k_cache must be [NB, Hkv, 16, D] and v_cache [NB, Hkv, D, 16]")
+    nb, hkv2, bs, d2 = k_cache.shape
+    if (hkv2, d2) != (hkv, d) or tuple(v_cache.shape) != (nb, hkv, d, bs) or tuple(positions.shape) != (B,):
+        raise ValueError("shapes: k_cache [NB, Hkv, 16, D], v_cache [NB, Hkv, D, 16], positions [B]")
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError(f"block_table must be [B, max_blocks_per_seq] with B = {B} rows (one per new token), "
+                         f"got {tuple(block_table.shape)}")
     tensors = {"k_new": k_new, "v_new": v_new, "k_cache": k_cache, "v_cache": v_cache,
                "block_table": block_table, "positions": positions}
     if kv_scales is not None:
@@ -367,12 +380,6 @@ def paged_kv_append(k_new, v_new, k_cache, v_cache, kv_scales, block_table, posi
             raise ValueError(f"{name} must be contiguous")
     if block_table.dtype != torch.int32 or positions.dtype != torch.int32:
         raise TypeError("block_table and positions must be int32")
-    if v_new.shape != k_new.shape or v_new.dtype != k_new.dtype:
-        raise ValueError("k_new and v_new must match")
-    B, hkv, d = k_new.shape
-    nb, hkv2, bs, d2 = k_cache.shape
-    if (hkv2, d2) != (hkv, d) or tuple(v_cache.shape) != (nb, hkv, d, bs) or positions.shape != (B,):
-        raise ValueError("shapes: k_cache [NB, Hkv, 16, D], v_cache [NB, Hkv, D, 16], positions [B]")
     kv_dt = _dtype_code(k_cache, "k_cache")
     if kv_dt == FP8_E4M3 and (kv_scales is None or tuple(kv_scales.shape) != (2, nb, hkv)
                               or kv_scales.dtype != torch.float32):

@@ -1,8 +1,8 @@
 // HIP kernels for variable-length causal prefill over the paged KV cache on
 // MI355X (gfx950, CDNA4).
 //
-// The log-prob forward of RLVR training (the compute_log_prob phase of the
-// paper's Sec. 6.2 breakdown; a forward call of its Sec. 3 interface) and
+// The log-prob forward of RLVR training (the compute_log_prob phase timed in
+// the paper's Table 2, Sec. 6.3; a forward call of its Sec. 4.2 interface) and
 // chunked prefill attend many query tokens per sequence at once: packed q rows
 // q_offsets[b] .. q_offsets[b+1]-1 are the last n_b of sequence b's L_b cached
 // tokens, and token i (position L_b - n_b + i) sees tokens 0 .. L_b - n_b + i.

@@ -258,6 +258,29 @@ def test_append_argument_checks():
     assert call(aprob(num_seqs=0), [None] * 7) == L.OK   # empty batch: no-op
 
 
+def test_append_binding_checks_block_table_rows():
+    """The append kernel reads block_table[b, :] for every new token b, so the
+    binding refuses a table without exactly B rows (or not 2-D) before it
+    looks at devices: a short table would be read past its end."""
+    import torch
+
+    B, hkv, d, nb = 3, 2, 64, 10
+    k_new = torch.zeros((B, hkv, d), dtype=torch.bfloat16)
+    v_new = torch.zeros_like(k_new)
+    kc = torch.zeros((nb, hkv, 16, d), dtype=torch.bfloat16)
+    vc = torch.zeros((nb, hkv, d, 16), dtype=torch.bfloat16)
+    pos = torch.zeros(B, dtype=torch.int32)
+    for bad in (torch.zeros((B - 1, 4), dtype=torch.int32), torch.zeros((B + 1, 4), dtype=torch.int32),
+                torch.zeros(4 * B, dtype=torch.int32)):
+        with pytest.raises(ValueError, match="block_table"):
+            L.paged_kv_append(k_new, v_new, kc, vc, None, bad, pos)
+    with pytest.raises(ValueError, match="k_new"):
+        L.paged_kv_append(k_new[0], v_new[0], kc, vc, None, torch.zeros((B, 4), dtype=torch.int32), pos)
+    # right shapes pass the shape checks and stop at the device check
+    with pytest.raises(ValueError, match="must be on"):
+        L.paged_kv_append(k_new, v_new, kc, vc, None, torch.zeros((B, 4), dtype=torch.int32), pos)
+
+
 def test_multi_token_checks_and_plan():
     assert L.raw_call(16, 16, 16, 16, 16, 16, 16, 0.1, prob(q_tokens=-1)) == L.EINVAL
     # several query tokens need the MFMA kernel (bf16 / fp8 cache) and Q * G <= 32
