@@ -6,10 +6,13 @@ kernel plus the log-sum-exp combine kernel) over one synthetic decode batch
 whose inputs are already resident in HBM. ``--op append`` times the KV append
 of a decode step instead, and ``--op prefill`` the causal varlen prefill of a
 log-prob forward (plan kernel plus attention kernel, MFMA-bound: reported in
-TFLOP/s of the causal QK^T and PV products). Default workload: the 7B-class GQA
-step (64 sequences, 28 query / 4 KV heads, head_dim 128, bf16, lognormal
-lengths with median 2048). The KV cache is rotated over enough copies that
-consecutive steps never find their cache in the 256 MB last-level cache.
+TFLOP/s of the causal QK^T and PV products). Default workload: the largest
+decode step that fits one GPU, fp8 KV at scale (512 sequences, 64 query / 8 KV
+heads, head_dim 128, e4m3 cache with per-tile scales, lognormal lengths with
+median 8192 up to 65,536); the same line then times the other long-tailed GQA
+steps (7B GQA, GRPO rollout batch, stragglers) under ``per_config``. Smaller
+caches are rotated over enough copies that consecutive steps never find their
+cache in the 256 MB last-level cache.
 
 Prints one JSON line. `value` is achieved GB/s of algorithmic bytes (K/V
 tiles of every token, fp8 scales, q, out, block-table entries, lengths) over
@@ -84,10 +87,41 @@ def prefill_flops(workload, seq_lens, counts):
 
 # ----------------------------------------------------------------- CPU baseline
 
+# A GPU machine gives the process of one GPU this many host cores (its share of
+# the host, whatever the affinity mask shows); more workers would only
+# oversubscribe them.
+CPU_SHARE = 16
+
+
 def _worker_init():
     # one BLAS thread per oracle process (the pool already uses every core)
     for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
         os.environ[k] = "1"
+
+
+def _pool_cores():
+    """(cores the affinity mask shows, worker processes used)."""
+    avail = len(os.sched_getaffinity(0))
+    return avail, min(avail, CPU_SHARE)
+
+
+def _cores_note(avail, used):
+    if used < avail:
+        return (f"{used} of the {avail} cores in the affinity mask: one GPU's share of the host is "
+                f"{CPU_SHARE} cores")
+    return f"all {avail} cores in the affinity mask"
+
+
+def _close_pool(pool):
+    """Terminate the oracle workers and wait for them and for the semaphore
+    tracker that the spawn start method runs, so no process outlives the bench."""
+    pool.terminate()
+    pool.join()
+    try:
+        from multiprocessing import resource_tracker
+        resource_tracker._resource_tracker._stop()
+    except Exception:  # private API; a leftover tracker exits with its parent
+        pass
 
 
 def _oracle_one(args):
@@ -151,7 +185,8 @@ def _prefill_rows_problem(pin, b, rows, raw):
 
 
 def cpu_baseline_prefill(pin, budget_s, rows_per_job=4):
-    """Time the oracle on seeded query rows of the prefill, all host cores (<= 16)."""
+    """Time the oracle on seeded query rows of the prefill, one worker process
+    per host core of one GPU's share."""
     import multiprocessing as mp
 
     import numpy as np
@@ -164,12 +199,13 @@ def cpu_baseline_prefill(pin, budget_s, rows_per_job=4):
         return t.numpy()
 
     w = pin.cache.workload
-    cores = min(len(os.sched_getaffinity(0)), 16)
+    avail, cores = _pool_cores()
     rng = np.random.default_rng(0)
     seq_of_row = np.repeat(np.arange(len(pin.counts)), pin.counts)
     ctx = mp.get_context("spawn")
     pairs, nrows, t_cpu = 0, 0, 0.0
-    with ctx.Pool(cores, initializer=_worker_init) as pool:
+    pool = ctx.Pool(cores, initializer=_worker_init)
+    try:
         t0 = time.perf_counter()
         pending = []
         while True:
@@ -189,11 +225,15 @@ def cpu_baseline_prefill(pin, budget_s, rows_per_job=4):
             t_cpu += res.get()
             pairs, nrows = pairs + pp, nrows + nr
         wall = time.perf_counter() - t0
+    finally:
+        _close_pool(pool)
     flops = 4 * w.head_dim * w.num_q_heads * pairs
     return {
         "value": round(flops / wall / 1e12, 6),
         "unit": "TFLOP/s",
         "cores": cores,
+        "cores_available": avail,
+        "cores_note": _cores_note(avail, cores),
         "kind": "oracle",
         "tokens_per_s": round(nrows / wall, 2),
         "seconds": round(wall, 2),
@@ -205,7 +245,8 @@ def cpu_baseline_prefill(pin, budget_s, rows_per_job=4):
 
 
 def cpu_baseline(inp, budget_s):
-    """Time the oracle over a seeded sample of sequences, all host cores (<= 16)."""
+    """Time the oracle over a seeded sample of sequences, one worker process
+    per host core of one GPU's share."""
     import multiprocessing as mp
 
     import numpy as np
@@ -217,12 +258,13 @@ def cpu_baseline(inp, budget_s):
             return t.view(torch.int16).numpy().view(np.uint16)
         return t.numpy()
 
-    cores = min(len(os.sched_getaffinity(0)), 16)
+    avail, cores = _pool_cores()
     lay = inp.layout
     order = np.random.default_rng(0).permutation(len(lay.seq_lens))
     ctx = mp.get_context("spawn")
     done, t_cpu = [], 0.0
-    with ctx.Pool(cores, initializer=_worker_init) as pool:
+    pool = ctx.Pool(cores, initializer=_worker_init)
+    try:
         t0 = time.perf_counter()
         pending = []
         # keep the pool fed, pass after pass over the step's sequences, until the
@@ -244,19 +286,23 @@ def cpu_baseline(inp, budget_s):
             t_cpu += r.get()
             done.append(bb)
         wall = time.perf_counter() - t0
+    finally:
+        _close_pool(pool)
     lens = lay.seq_lens[done]
     nbytes, tokens = algorithmic_bytes(inp.workload, lens)
     return {
         "value": round(nbytes / wall / 1e9, 4),
         "unit": "GB/s",
         "cores": cores,
+        "cores_available": avail,
+        "cores_note": _cores_note(avail, cores),
         "kind": "oracle",
         "kv_tokens_per_s": round(tokens / wall, 1),
         "seconds": round(wall, 2),
         "cpu_seconds": round(t_cpu, 2),
-        "sample": f"{len(done)} sequence evaluations ({tokens} tokens; passes over the step's "
-                  f"{len(lay.seq_lens)} sequences in a seeded order) of the same step, fp64 numpy "
-                  f"oracle, one process per core",
+        "sample": f"{len(done)} sequence evaluations ({tokens} tokens) of the same step, its "
+                  f"{len(lay.seq_lens)} sequences taken in a seeded order (again from the start if the budget "
+                  f"outlasts them), fp64 numpy oracle, one process per core",
     }
 
 
@@ -307,74 +353,27 @@ def measured_traffic(workload_name, per_launch_bytes, source=KERNEL_SOURCE):
 
 # ----------------------------------------------------------------- main
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default=None,
-                    help="default: gqa7b_bf16 (decode, append), logprob_gqa7b_bf16 (prefill)")
-    ap.add_argument("--variant", default="auto", choices=["auto", "vector", "mfma"])
-    ap.add_argument("--waves-per-cu", type=int, default=0)
-    ap.add_argument("--min-blocks-per-wave", type=int, default=0)
-    ap.add_argument("--chunks-per-wave", type=int, default=0, help="1 = static split; 0 = library default")
-    ap.add_argument("--min-blocks-per-chunk", type=int, default=0)
-    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle wall time")
-    ap.add_argument("--calibrate-copy", action="store_true",
-                    help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="decode", choices=["decode", "append", "prefill"],
-                    help="decode: one attention step (default); append: the KV append of one decode step "
-                         "(each sequence's new token written into its last slot); prefill: the causal varlen "
-                         "prefill of a log-prob forward")
-    ap.add_argument("--shared-prefix", action="store_true",
-                    help="GRPO workloads: read each group's shared prompt blocks once for several members "
-                         "(pda_paged_decode_attention_shared_prefix); bytes count the shared blocks once")
-    args = ap.parse_args()
+PER_CONFIG = ("gqa7b_bf16", "grpo_bf16", "straggler_bf16")   # the other long-tailed GQA decode steps
 
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: the library has no multi-GPU path (the step shards by sequence "
-              "or by KV head with no exchange, but nothing here launches on several GPUs); run with --gpus 1",
-              file=sys.stderr)
-        sys.exit(2)
 
-    import numpy as np
+def time_decode(args, w, dev, shared_prefix=False, op="decode"):
+    """Generate one step of workload ``w`` on ``dev`` and time ``args.steps``
+    calls after ``args.warmup`` untimed ones. Returns the inputs and the
+    measured figures (wall and HIP-event times, single-call spread, status)."""
     import torch
 
     from paper_2605_20863_amd import _lib
     from paper_2605_20863_amd import workloads as W
 
-    dev = torch.device("cuda:0")
-    if args.calibrate_copy:
-        # a copy kernel of known size: reads and writes 2^30 bytes per dispatch
-        src = torch.randn(1 << 28, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(args.warmup + args.steps):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"calibration": "copy", "bytes_read_per_dispatch": 1 << 30,
-                          "bytes_written_per_dispatch": 1 << 30, "dispatches": args.warmup + args.steps}))
-        return
-
-    if args.workload is None:
-        args.workload = "logprob_gqa7b_bf16" if args.op == "prefill" else "gqa7b_bf16"
-    w = W.WORKLOADS[args.workload]
-    if (args.op == "prefill") != w.is_prefill:
-        print(f"--op {args.op} does not fit workload {w.name}", file=sys.stderr)
-        sys.exit(2)
-    if args.op == "prefill":
-        prefill_main(args, w, dev)
-        return
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     inp = W.generate(w, dev)
     lens = inp.layout.seq_lens
     gp = W.group_prefix(w, inp.layout)
-    if args.shared_prefix and gp is None:
+    if shared_prefix and gp is None:
         print(f"--shared-prefix needs a GRPO workload (groups sharing prompt blocks); {w.name} has none",
               file=sys.stderr)
         sys.exit(2)
-    shared = gp if args.shared_prefix else None
+    shared = gp if shared_prefix else None
     nbytes, tokens = algorithmic_bytes(w, lens, shared)
     kv_bytes = inp.k_cache.numel() * inp.k_cache.element_size() * 2
     # rotate over >= 4 GB of cache copies (16x the last-level cache) between steps
@@ -392,12 +391,12 @@ def main():
                              args.min_blocks_per_chunk)
     ptrs = [(k.data_ptr(), v.data_ptr(), s.data_ptr() if s is not None else None) for k, v, s in caches]
     sh = stream.cuda_stream
-    qp, bp, lp, op = inp.q.data_ptr(), inp.block_table.data_ptr(), inp.seq_lens.data_ptr(), out.data_ptr()
+    qp, bp, lp, op_ = inp.q.data_ptr(), inp.block_table.data_ptr(), inp.seq_lens.data_ptr(), out.data_ptr()
 
     if shared is not None:
         sb_dev = torch.as_tensor(shared[1], device=dev)
 
-    if args.op == "append":
+    if op == "append":
         # one new token per sequence, written into its last slot (the block exists)
         gen = torch.Generator(device=dev).manual_seed(7)
         B, hkv, d = len(lens), w.num_kv_heads, w.head_dim
@@ -410,21 +409,21 @@ def main():
 
     def step(i):
         kp, vp, sp = ptrs[i % ncopies]
-        if args.op == "append":
+        if op == "append":
             rc = _lib.raw_kv_append(k_new.data_ptr(), v_new.data_ptr(), kp, vp, sp, bp, positions.data_ptr(),
                                     aprob, sh)
         elif shared is not None:
-            rc = _lib.raw_call_shared_prefix(qp, kp, vp, bp, lp, sp, op, inp.softmax_scale, shared[0],
+            rc = _lib.raw_call_shared_prefix(qp, kp, vp, bp, lp, sp, op_, inp.softmax_scale, shared[0],
                                              sb_dev.data_ptr(), prob, opts, sh)
         else:
-            rc = _lib.raw_call(qp, kp, vp, bp, lp, sp, op, inp.softmax_scale, prob, opts, sh)
+            rc = _lib.raw_call(qp, kp, vp, bp, lp, sp, op_, inp.softmax_scale, prob, opts, sh)
         if rc != 0:
             raise RuntimeError(f"pda error {rc}: {_lib.last_error()}")
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    if args.op == "decode":
+    if op == "decode":
         assert torch.isfinite(out.float()).all(), "non-finite output"
 
     # Timed region: K back-to-back calls. Two HIP events on the calls' stream
@@ -449,12 +448,110 @@ def main():
           f"(HIP events over the timed region), {ncopies} cache copies, status {status}; single calls: "
           f"median {spread['median']} us, min {spread['min']}, max {spread['max']}",
           file=sys.stderr, flush=True)
+    traffic = (measured_traffic(w.name + ("_shared" if shared is not None else ""), nbytes)
+               if op == "decode" else None)
+    del caches, ptrs
+    return dict(inp=inp, nbytes=nbytes, tokens=tokens, ncopies=ncopies, call_ms=call_ms, ms_per_step=ms_per_step,
+                spread=spread, status=status, traffic=traffic, shared=shared)
+
+
+def per_config_line(args, dev):
+    """The other long-tailed GQA decode steps, each generated, timed as the
+    headline step is, and freed in turn: per-call GPU time, fraction of peak
+    and measured-over-algorithmic HBM bytes."""
+    import torch
+
+    from paper_2605_20863_amd import workloads as W
+
+    res = {}
+    for name in PER_CONFIG:
+        w = W.WORKLOADS[name]
+        r = time_decode(args, w, dev)
+        achieved = r["nbytes"] / (r["call_ms"] * 1e-3) / 1e9
+        res[name] = {
+            "call_us": round(r["call_ms"] * 1e3, 2),
+            "ms_per_step": round(r["ms_per_step"], 5),
+            "achieved": round(achieved, 2),
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "value_wall_gbs": round(r["nbytes"] / (r["ms_per_step"] * 1e-3) / 1e9, 2),
+            "algorithmic_bytes_per_call": r["nbytes"],
+            "traffic_over_algorithmic": round(r["traffic"] / r["nbytes"], 4) if r["traffic"] else None,
+            "kv_tokens_per_s": round(r["tokens"] / (r["call_ms"] * 1e-3), 1),
+            "single_call_us": r["spread"],
+            "status": r["status"],
+        }
+        del r
+        torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None,
+                    help="default: fp8kv (decode; the largest single-GPU step), gqa7b_bf16 (append), "
+                         "logprob_gqa7b_bf16 (prefill)")
+    ap.add_argument("--variant", default="auto", choices=["auto", "vector", "mfma"])
+    ap.add_argument("--waves-per-cu", type=int, default=0)
+    ap.add_argument("--min-blocks-per-wave", type=int, default=0)
+    ap.add_argument("--chunks-per-wave", type=int, default=0, help="1 = static split; 0 = library default")
+    ap.add_argument("--min-blocks-per-chunk", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle wall time")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="decode: skip timing the other long-tailed GQA steps (" + ", ".join(PER_CONFIG) + ")")
+    ap.add_argument("--op", default="decode", choices=["decode", "append", "prefill"],
+                    help="decode: one attention step (default); append: the KV append of one decode step "
+                         "(each sequence's new token written into its last slot); prefill: the causal varlen "
+                         "prefill of a log-prob forward")
+    ap.add_argument("--shared-prefix", action="store_true",
+                    help="GRPO workloads: read each group's shared prompt blocks once for several members "
+                         "(pda_paged_decode_attention_shared_prefix); bytes count the shared blocks once")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the library has no multi-GPU path (the step shards by sequence "
+              "or by KV head with no exchange, but nothing here launches on several GPUs); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2605_20863_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    if args.calibrate_copy:
+        # a copy kernel of known size: reads and writes 2^30 bytes per dispatch
+        src = torch.randn(1 << 28, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read_per_dispatch": 1 << 30,
+                          "bytes_written_per_dispatch": 1 << 30, "dispatches": args.warmup + args.steps}))
+        return
+
+    if args.workload is None:
+        args.workload = {"prefill": "logprob_gqa7b_bf16", "append": "gqa7b_bf16"}.get(args.op, "fp8kv")
+    w = W.WORKLOADS[args.workload]
+    if (args.op == "prefill") != w.is_prefill:
+        print(f"--op {args.op} does not fit workload {w.name}", file=sys.stderr)
+        sys.exit(2)
+    if args.op == "prefill":
+        prefill_main(args, w, dev)
+        return
+    r = time_decode(args, w, dev, args.shared_prefix, args.op)
+    inp, nbytes, tokens, shared = r["inp"], r["nbytes"], r["tokens"], r["shared"]
+    call_ms, ms_per_step, traffic = r["call_ms"], r["ms_per_step"], r["traffic"]
+    lens = inp.layout.seq_lens
 
     achieved = nbytes / (call_ms * 1e-3) / 1e9
     value = nbytes / (ms_per_step * 1e-3) / 1e9
-    traffic = (measured_traffic(w.name + ("_shared" if shared is not None else ""), nbytes)
-               if args.op == "decode" else None)
-    dtype = {"f32": "f32", "bf16": "bf16", "fp8_e4m3": "fp8e4m3-kv/bf16-q"}[w.kv_dtype]
     res = {
         "metric": ("paged decode attention achieved HBM GB/s (% of peak) + KV tokens/s read" if args.op == "decode"
                    else "paged KV append achieved HBM GB/s (% of peak) + new tokens/s written"),
@@ -467,7 +564,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": dtype,
+        # arithmetic of the path: bf16 products (fp8 codes convert exactly to
+        # bf16) with fp32 sums, or fp32 throughout for an fp32 cache
+        "dtype": "f32" if w.kv_dtype == "f32" else "bf16",
         "data": "synthetic",
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "kv_tokens_per_s": round(tokens / (ms_per_step * 1e-3), 1),
@@ -478,12 +577,13 @@ def main():
             "q_heads": w.num_q_heads,
             "kv_heads": w.num_kv_heads,
             "head_dim": w.head_dim,
+            "q_dtype": w.q_dtype,
             "kv_dtype": w.kv_dtype,
             "block_size": w.block_size,
             "total_tokens": tokens,
             "max_seq_len": int(lens.max()),
             "variant": args.variant,
-            "cache_copies": ncopies,
+            "cache_copies": r["ncopies"],
             "shared_prefix": shared is not None,
             "q_tokens": w.q_tokens,
             "op": args.op,
@@ -501,10 +601,14 @@ def main():
             "traffic_over_algorithmic": round(traffic / nbytes, 4) if traffic else None,
             "algorithmic_bytes_per_call": nbytes,
             "call_us": round(call_ms * 1e3, 2),
-            "single_call_us": spread,
+            "single_call_us": r["spread"],
         },
         "cpu_baseline": None,
     }
+    del r
+    if (args.op == "decode" and not args.shared_prefix and not args.no_per_config
+            and args.workload not in PER_CONFIG):
+        res["per_config"] = per_config_line(args, dev)
     if not args.no_cpu_baseline and args.op == "decode" and w.q_tokens == 1:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)

@@ -68,6 +68,65 @@ def oracle_for(inp, seqs=None):
         q_dtype=w.q_dtype, kv_dtype=w.kv_dtype, kv_scales=ks)
 
 
+def _sequence_job(inp, q, b, kind):
+    """Sequence b of ``inp`` as a self-contained one-sequence oracle problem:
+    its query rows, host copies of its own blocks, its block-table row
+    renumbered to them (data movement only)."""
+    w = inp.workload
+    lay = inp.layout
+    n = (int(lay.seq_lens[b]) + 15) // 16
+    phys, local = np.unique(lay.block_table[b, :n].astype(np.int64), return_inverse=True)
+    if phys.size == 0:
+        phys, local = np.zeros(1, dtype=np.int64), np.zeros(0, dtype=np.int64)
+    idx = torch.from_numpy(phys).to(inp.device)
+    table = np.full((1, max(n, 1)), -1, dtype=np.int32)
+    table[0, :n] = local
+    kw = dict(q=raw(q[b:b + 1]), k_cache=raw(inp.k_cache.index_select(0, idx)),
+              v_cache=raw(inp.v_cache.index_select(0, idx)), block_table=table,
+              seq_lens=lay.seq_lens[b:b + 1].copy(), softmax_scale=inp.softmax_scale,
+              q_dtype=w.q_dtype, kv_dtype=w.kv_dtype,
+              kv_scales=raw(inp.kv_scales.index_select(1, idx)) if inp.kv_scales is not None else None)
+    return kind, b, kw
+
+
+def oracle_whole(inp, what="", q=None):
+    """Oracle output for every sequence of ``inp`` ([B, Hq, D], or [B, Q, Hq, D]
+    with several query tokens; ``q`` replaces inp.q), computed one sequence per
+    job in the worker pool of ``tests._oracle_pool``; longest sequences first,
+    so that the last jobs are short."""
+    from tests import _oracle_pool as P
+
+    q = inp.q if q is None else q
+    lens = inp.layout.seq_lens
+    B = len(lens)
+    kind = "decode" if q.dim() == 3 else "multi_token"
+    ref = np.zeros(tuple(q.shape), dtype=np.float64)
+
+    def put(b, out):
+        ref[b] = out[0]
+
+    order = np.argsort(-lens.astype(np.int64), kind="stable")
+    t = P.run_jobs((_sequence_job(inp, q, int(b), kind) for b in order), put,
+                   progress=lambda done, s: print(f"[oracle] {what}: {done}/{B} sequences, {s:.0f} s", flush=True))
+    print(f"[oracle] {what}: all {B} sequences ({int(lens.sum())} tokens) in {t:.1f} s on "
+          f"{P.cores_used()} worker processes", flush=True)
+    return ref
+
+
+def worst_row_rel_l2(got: np.ndarray, ref: np.ndarray):
+    """Largest relative L2 error of one output row (one sequence and query
+    head, over D), with its index; rows whose reference is zero use the
+    absolute norm. A diagnostic beside the whole-tensor bounds."""
+    d = got.shape[-1]
+    g = got.reshape(-1, d)
+    r = ref.reshape(-1, d)
+    num = np.linalg.norm(g - r, axis=1)
+    den = np.linalg.norm(r, axis=1)
+    rel = np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
+    i = int(np.argmax(rel))
+    return float(rel[i]), np.unravel_index(i, got.shape[:-1])
+
+
 def errors(got: np.ndarray, ref: np.ndarray):
     diff = got - ref
     max_abs = float(np.max(np.abs(diff))) if diff.size else 0.0

@@ -1,0 +1,39 @@
+"""The pooled oracle that the full-size GPU parity tests use (one sequence per
+worker job, each job a copy of that sequence's own blocks) gives exactly the
+one-process oracle's output, for plain, GRPO (shared blocks), fp8 and
+multi-token inputs, including empty sequences. Runs on the CPU."""
+
+import numpy as np
+import torch
+
+from paper_2605_20863_amd import workloads as W
+from tests import _gpu_util as U
+from tests import _oracle_pool as P
+
+
+def test_pooled_oracle_equals_one_process_oracle():
+    for name in ("gqa7b_bf16", "grpo_bf16", "fp8kv", "tiny_mha_f32"):
+        w = W.SMALL_WORKLOADS[name]
+        inp = W.generate(w, "cpu")
+        whole = U.oracle_whole(inp, name)
+        assert np.array_equal(whole, U.oracle_for(inp)), name
+    lens = [0, 1, 17, 300, 0, 45]
+    w = W.Workload("pool_mt", len(lens), 8, 2, 64, "bf16", "fp8_e4m3", ("uniform", 1, 1), cfg_id=55, q_tokens=3)
+    inp = W.generate(w, "cpu", seq_lens=lens)
+    whole = U.oracle_whole(inp, "multi-token")
+    import oracle
+    ref = oracle.paged_multi_token_attention(
+        q=U.raw(inp.q), k_cache=U.raw(inp.k_cache), v_cache=U.raw(inp.v_cache),
+        block_table=inp.layout.block_table, seq_lens=inp.layout.seq_lens, softmax_scale=inp.softmax_scale,
+        q_dtype="bf16", kv_dtype="fp8_e4m3", kv_scales=U.raw(inp.kv_scales))
+    assert np.array_equal(whole, ref)
+    assert P.cores_used() == min(P.cores_available(), P.MAX_CORES)
+
+
+def test_worst_row_diagnostic():
+    ref = np.ones((2, 3, 4))
+    got = ref.copy()
+    got[1, 2, 0] += 0.5
+    worst, at = U.worst_row_rel_l2(got, ref)
+    assert at == (1, 2) and abs(worst - 0.25) < 1e-15
+    assert torch.isfinite(torch.tensor(worst))

@@ -3,6 +3,8 @@ block tables share the prompt's blocks) against the fp64 oracle of plain
 paged attention: reading a shared block once for several members' queries
 must not change the result. Tolerances as in test_parity_gpu."""
 
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -112,20 +114,23 @@ def test_shared_prefix_without_shared_blocks(lib):
     assert lib.read_device_status() & 4
 
 
-def test_shared_prefix_full_size_grpo(lib):
-    """The full GRPO step through the shared-prefix path, checked on sampled sequences."""
-    w = W.WORKLOADS["grpo_bf16"]
-    print("[parity] shared-prefix full grpo: generating", flush=True)
+@pytest.mark.parametrize("name", ["grpo_bf16", "grpo_longprompt_bf16"])
+def test_shared_prefix_full_size_grpo(lib, name):
+    """The full GRPO steps through the shared-prefix path: every output (all
+    B x Hq x D) against the oracle, whose sequences run in a pool of worker
+    processes."""
+    w = W.WORKLOADS[name]
+    t0 = time.perf_counter()
+    print(f"[parity] shared-prefix full {name}: generating", flush=True)
     inp = W.generate(w, DEV)
     gs, sb = W.group_prefix(w, inp.layout)
-    got = run_shared(lib, inp, gs, sb)
-    assert torch.isfinite(got.float()).all()
-    lens = inp.layout.seq_lens
-    rng = np.random.default_rng(5)
-    seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(len(lens), 3, replace=False).tolist()})
-    print(f"[parity] shared-prefix full grpo: oracle on seqs {seqs}", flush=True)
-    ref = U.oracle_for(inp, seqs)
-    U.assert_close(U.out_to_f64(got)[seqs], ref, "bf16", "full grpo shared")
+    got = U.out_to_f64(run_shared(lib, inp, gs, sb))
     assert lib.read_device_status() == 0
-    del inp, got
+    ref = U.oracle_whole(inp, f"shared-prefix full {name}")
+    max_abs, rel_l2 = U.assert_close(got, ref, "bf16", f"full {name} shared")
+    worst, at = U.worst_row_rel_l2(got, ref)
+    print(f"[parity] shared-prefix full {name}: all {got.size} outputs: max_abs {max_abs:.2e} rel_l2 {rel_l2:.2e}, "
+          f"worst row rel_l2 {worst:.2e} at {tuple(int(i) for i in at)}; {time.perf_counter() - t0:.1f} s",
+          flush=True)
+    del inp
     torch.cuda.empty_cache()
