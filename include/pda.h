@@ -166,6 +166,49 @@ int pda_paged_decode_attention(const void* q,
                                const pda_options* options,
                                hipStream_t stream);
 
+/*
+ * For callers that cannot allocate device memory: code being captured into a
+ * HIP graph before any eager call has sized a workspace, tight serving loops,
+ * harnesses that forbid hipMalloc. The same decode step as
+ * pda_paged_decode_attention, with the same arguments, kernels and result
+ * (bitwise), but its workspace (partial results, per-sequence prefix sums,
+ * chunk counter, status word) is a fixed device array of PDA_NOALLOC_SCRATCH_BYTES
+ * (32 MiB) compiled into the library: each device the library runs on holds
+ * its own copy from load until the process ends. The call allocates nothing:
+ * no hipMalloc, hipFree or allocating library routine, on any call.
+ *
+ * Limit: a call whose workspace (pda_plan_info.workspace_bytes) exceeds the
+ * array returns PDA_EINVAL with the size it needed; at the default split that
+ * is about 25 MiB for 512 sequences x 8 KV heads x 8 query heads per KV head
+ * (more waves per CU, dynamic chunks or wider query groups need more).
+ *
+ * Sharing: every call on a device uses that device's one array, and the
+ * array keeps the last call's contents. Calls that overlap on one device
+ * (different streams, or threads without ordering between them) race on it
+ * and may give wrong results; order them on one stream. Calls on one stream
+ * from several threads are serialised by an internal lock, as are calls on
+ * different devices. The chunk counter starts at zero (the array is
+ * zero-initialised at load) and the combine kernel re-zeroes it after every
+ * call. Status bits go to the array's status word, which
+ * pda_read_device_status(stream) reads and clears too (after waiting for
+ * `stream` only).
+ *
+ * Errors as for pda_paged_decode_attention, plus PDA_EINVAL for the size limit
+ * above. Capturable into a HIP graph from the first call.
+ */
+#define PDA_NOALLOC_SCRATCH_BYTES (32LL << 20)
+int pda_paged_decode_attention_noalloc(const void* q,
+                                       const void* k_cache,
+                                       const void* v_cache,
+                                       const int32_t* block_table,
+                                       const int32_t* seq_lens,
+                                       const float* kv_scales,
+                                       void* out,
+                                       float softmax_scale,
+                                       const pda_problem* problem,
+                                       const pda_options* options,
+                                       hipStream_t stream);
+
 /* Validate `problem` / `options` and describe the launch, on the host only
  * (no HIP call). `num_compute_units` sizes the persistent grid (MI355X: 256).
  * With options.waves_per_cu = 0 the launch takes the decode kernel's
@@ -352,7 +395,9 @@ int pda_paged_prefill_attention(const void* q,
                                 hipStream_t stream);
 
 /* Wait for `stream`, then return (and clear) the device-side status bits that
- * calls on it recorded: 1 = a sequence length was clamped, 2 = a block-table
+ * calls on it recorded (and those in the fixed scratch of
+ * pda_paged_decode_attention_noalloc, once it has run on the device): 1 = a
+ * sequence length was clamped, 2 = a block-table
  * entry outside [0, num_blocks) was skipped, 4 = a group's members share fewer
  * leading blocks than shared_blocks declared, 8 = prefill q_offsets were not
  * non-decreasing within [0, T], 16 = a prefill V value outside the fp16 range

@@ -42,6 +42,7 @@ VARIANT_AUTO, VARIANT_VECTOR, VARIANT_MFMA = 0, 1, 2
 _VARIANTS = {"auto": VARIANT_AUTO, "vector": VARIANT_VECTOR, "mfma": VARIANT_MFMA}
 STATUS_LEN_CLAMPED, STATUS_BAD_BLOCK, STATUS_PREFIX_SHORTENED, STATUS_BAD_OFFSETS = 1, 2, 4, 8
 STATUS_HALF_RANGE = 16
+NOALLOC_SCRATCH_BYTES = 32 << 20   # PDA_NOALLOC_SCRATCH_BYTES
 
 
 class Problem(ctypes.Structure):
@@ -115,6 +116,8 @@ _vp = ctypes.c_void_p
 _lib.pda_paged_decode_attention.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_float,
                                             ctypes.POINTER(Problem), ctypes.POINTER(Options), _vp]
 _lib.pda_paged_decode_attention.restype = ctypes.c_int
+_lib.pda_paged_decode_attention_noalloc.argtypes = _lib.pda_paged_decode_attention.argtypes
+_lib.pda_paged_decode_attention_noalloc.restype = ctypes.c_int
 _lib.pda_query_plan.argtypes = [ctypes.POINTER(Problem), ctypes.POINTER(Options), ctypes.c_float,
                                 ctypes.c_int32, ctypes.POINTER(PlanInfo)]
 _lib.pda_query_plan.restype = ctypes.c_int
@@ -177,6 +180,14 @@ def raw_call(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax
              problem: Problem, options: Options | None = None, stream=None) -> int:
     """pda_paged_decode_attention with integer pointers; returns the status code."""
     return _lib.pda_paged_decode_attention(
+        q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, ctypes.c_float(softmax_scale),
+        ctypes.byref(problem), ctypes.byref(options) if options is not None else None, stream)
+
+
+def raw_call_noalloc(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale,
+                     problem: Problem, options: Options | None = None, stream=None) -> int:
+    """pda_paged_decode_attention_noalloc with integer pointers; returns the status code."""
+    return _lib.pda_paged_decode_attention_noalloc(
         q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, ctypes.c_float(softmax_scale),
         ctypes.byref(problem), ctypes.byref(options) if options is not None else None, stream)
 
@@ -296,6 +307,24 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, seq_lens, kv_scales
         rc = raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
                       seq_lens.data_ptr(), kv_scales.data_ptr() if kv_scales is not None else None,
                       out.data_ptr(), float(softmax_scale), prob, opts, _stream_handle(stream, q.device))
+    _check(rc)
+    return out
+
+
+def paged_decode_attention_noalloc(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out,
+                                   softmax_scale, max_seq_len=0, stream=None, variant="auto",
+                                   waves_per_cu=0, min_blocks_per_wave=0, chunks_per_wave=0,
+                                   min_blocks_per_chunk=0):
+    """paged_decode_attention through the entry point that allocates nothing:
+    its workspace is the library's fixed per-device scratch array
+    (NOALLOC_SCRATCH_BYTES), shared by every call on the device."""
+    torch = _torch()
+    prob, opts = _prepare(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, max_seq_len,
+                          variant, waves_per_cu, min_blocks_per_wave, chunks_per_wave, min_blocks_per_chunk)
+    with torch.cuda.device(q.device):
+        rc = raw_call_noalloc(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
+                              seq_lens.data_ptr(), kv_scales.data_ptr() if kv_scales is not None else None,
+                              out.data_ptr(), float(softmax_scale), prob, opts, _stream_handle(stream, q.device))
     _check(rc)
     return out
 

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libpda.so")
 
-SOURCES = ["pda_kernels.hip", "pda_append.hip", "pda_prefill.hip", "pda_host.cpp"]
+SOURCES = ["pda_kernels.hip", "pda_append.hip", "pda_prefill.hip", "pda_scratch.hip", "pda_host.cpp"]
 ARCH = "gfx950"
 
 # No packed-FP32 instructions: they are kept out of every HIP object.

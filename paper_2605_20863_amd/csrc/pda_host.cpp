@@ -21,6 +21,8 @@
 #include <utility>
 #include <vector>
 
+static_assert(pda::kScratchBytes == PDA_NOALLOC_SCRATCH_BYTES, "fixed scratch size differs from the header's");
+
 namespace {
 
 thread_local std::string g_error;
@@ -247,6 +249,18 @@ struct Workspace {
   std::vector<void*> retired;
 };
 
+// The no-allocation entry point's per-device state: the device address of
+// that device's copy of the fixed scratch array (looked up on the first call
+// with the device current) and the counter re-arm flag. A fixed table, so
+// that the entry point allocates nothing, not even host memory for its state.
+constexpr int kMaxDevices = 64;
+struct FixedScratch {
+  std::mutex mu;
+  void* ptr = nullptr;
+  bool rearm = false;
+};
+FixedScratch g_fixed[kMaxDevices];
+
 std::mutex g_mu;
 std::map<int, DeviceInfo> g_devices;
 std::map<std::pair<int, hipStream_t>, std::unique_ptr<Workspace>> g_workspaces;
@@ -372,10 +386,12 @@ int query_plan(const pda_problem* problem, const pda_options* options, float sof
   return PDA_OK;
 }
 
+// fixed_scratch: take the workspace from the device's fixed scratch array
+// (pda_paged_decode_attention_noalloc) instead of the stream's allocation.
 int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
         const int32_t* seq_lens, const float* kv_scales, void* out, float softmax_scale,
         const int32_t* group_size, const int32_t* shared_blocks, const pda_problem* problem,
-        const pda_options* options, hipStream_t stream) {
+        const pda_options* options, hipStream_t stream, bool fixed_scratch = false) {
   g_error.clear();
   Plan plan;
   int rc = validate(problem, options, softmax_scale, &plan);
@@ -409,16 +425,38 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   const int chunks_max = waves * plan.chunks_per_wave;
   const Layout lay = workspace_layout(problem, plan, gr, chunks_max);
 
-  Workspace* ws = workspace_for(dev, stream);
-  std::lock_guard<std::mutex> lk(ws->mu);
-  if ((rc = ensure_workspace(ws, lay.total, stream)) != PDA_OK) return rc;
-  char* base = static_cast<char*>(ws->ptr);
-  if (ws->rearm) {
+  std::unique_lock<std::mutex> lk;
+  char* base = nullptr;
+  bool* rearm = nullptr;
+  if (fixed_scratch) {
+    if (dev < 0 || dev >= kMaxDevices) return fail(PDA_EUNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+    if (lay.total > pda::kScratchBytes)
+      return fail(PDA_EINVAL,
+                  "this call needs %lld bytes of workspace; the no-allocation entry point's fixed scratch holds %lld "
+                  "(fewer sequences, KV heads or waves per call, or pda_paged_decode_attention)",
+                  (long long)lay.total, (long long)pda::kScratchBytes);
+    FixedScratch* fs = &g_fixed[dev];
+    lk = std::unique_lock<std::mutex>(fs->mu);
+    if (!fs->ptr) {  // first call on this device (current here): its copy of the array
+      void* p = nullptr;
+      if ((e = pda::scratch_address(&p)) != hipSuccess) return fail_hip(e, "hipGetSymbolAddress(scratch)");
+      fs->ptr = p;
+    }
+    base = static_cast<char*>(fs->ptr);
+    rearm = &fs->rearm;
+  } else {
+    Workspace* ws = workspace_for(dev, stream);
+    lk = std::unique_lock<std::mutex>(ws->mu);
+    if ((rc = ensure_workspace(ws, lay.total, stream)) != PDA_OK) return rc;
+    base = static_cast<char*>(ws->ptr);
+    rearm = &ws->rearm;
+  }
+  if (*rearm) {
     if (capturing(stream))
       return fail(PDA_EINVAL, "the workspace needs a reset after a failed launch: make one call outside capture");
     if ((e = hipMemsetAsync(base + pda::kHdrNext * 4, 0, 4, stream)) != hipSuccess)
       return fail_hip(e, "hipMemsetAsync");
-    ws->rearm = false;
+    *rearm = false;
   }
 
   pda::DecodeArgs a;
@@ -469,7 +507,7 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   if ((e = pda::launch_decode(a, plan.variant, plan.kv, stream)) != hipSuccess)
     return fail_hip(e, "decode kernel launch");
   if ((e = pda::launch_combine(a, stream)) != hipSuccess) {
-    ws->rearm = true;
+    *rearm = true;
     return fail_hip(e, "combine kernel launch");
   }
   return PDA_OK;
@@ -661,6 +699,14 @@ int pda_paged_decode_attention(const void* q, const void* k_cache, const void* v
              problem, options, stream);
 }
 
+int pda_paged_decode_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                       const int32_t* block_table, const int32_t* seq_lens, const float* kv_scales,
+                                       void* out, float softmax_scale, const pda_problem* problem,
+                                       const pda_options* options, hipStream_t stream) {
+  return run(q, k_cache, v_cache, block_table, seq_lens, kv_scales, out, softmax_scale, nullptr, nullptr,
+             problem, options, stream, /*fixed_scratch=*/true);
+}
+
 int pda_paged_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache, float* kv_scales,
                         const int32_t* block_table, const int32_t* positions, const pda_append_problem* problem,
                         hipStream_t stream) {
@@ -708,6 +754,18 @@ int pda_read_device_status(hipStream_t stream) {
     if ((e = hipMemcpy(&word, hdr, 4, hipMemcpyDeviceToHost)) != hipSuccess) return fail_hip(e, "hipMemcpy");
     if (word && (e = hipMemset(hdr, 0, 4)) != hipSuccess) return fail_hip(e, "hipMemset");
     all |= word;
+  }
+  // the device's fixed scratch, once the no-allocation entry point has used it
+  if (dev >= 0 && dev < kMaxDevices) {
+    FixedScratch* fs = &g_fixed[dev];
+    std::lock_guard<std::mutex> fl(fs->mu);
+    if (fs->ptr) {
+      int32_t word = 0;
+      int32_t* hdr = static_cast<int32_t*>(fs->ptr) + pda::kHdrStatus;
+      if ((e = hipMemcpy(&word, hdr, 4, hipMemcpyDeviceToHost)) != hipSuccess) return fail_hip(e, "hipMemcpy");
+      if (word && (e = hipMemset(hdr, 0, 4)) != hipSuccess) return fail_hip(e, "hipMemset");
+      all |= word;
+    }
   }
   return all;
 }

@@ -145,6 +145,16 @@ hipError_t launch_decode(const DecodeArgs& a, Variant v, KvType kv, hipStream_t 
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // Shared-prefix mode: the groups' real shared block counts, before the decode kernel.
 hipError_t launch_prefix(const DecodeArgs& a, int num_groups, hipStream_t s);
+// Fixed device scratch of pda_paged_decode_attention_noalloc: a file-scope
+// array in pda_scratch.hip, one copy per device, used in place of the
+// stream's workspace (same layout). 32 MiB holds the workspace of every
+// decode step up to 512 sequences x 8 KV heads x 32 query columns at the
+// default split (about 25 MiB for the fp8 step at 64 / 8 heads).
+constexpr int64_t kScratchBytes = 32ll << 20;
+// Device address of the current device's copy of that array
+// (hipGetSymbolAddress; the caller keeps it per device).
+hipError_t scratch_address(void** ptr);
+
 // Max resident waves per CU for the decode kernel that (v, kv, D, G) selects.
 // wide: the kernel whose entries carry up to kWideColumns query columns (shared-prefix
 // prefix entries, several query tokens per sequence)

@@ -26,7 +26,8 @@ def test_exports_every_declared_symbol():
     assert set(declared) == {"pda_paged_decode_attention", "pda_query_plan", "pda_read_device_status",
                              "pda_release_workspaces", "pda_last_error", "pda_version",
                              "pda_paged_decode_attention_shared_prefix", "pda_query_plan_shared_prefix",
-                             "pda_paged_kv_append", "pda_paged_prefill_attention"}
+                             "pda_paged_kv_append", "pda_paged_prefill_attention",
+                             "pda_paged_decode_attention_noalloc"}
     for name in declared:
         assert hasattr(L._lib, name), name
     nm = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True).stdout
@@ -161,6 +162,22 @@ def test_misaligned_pointers_rejected():
 
 def test_empty_batch_is_a_no_op():
     assert L.raw_call(None, None, None, None, None, None, None, 0.1, prob(num_seqs=0)) == L.OK
+
+
+@pytest.mark.parametrize("kw,code", BAD, ids=[str(k) for k, _ in BAD])
+def test_noalloc_entry_point_validates_like_the_decode_call(kw, code):
+    """The no-allocation entry point runs the decode call's host checks before
+    any HIP call: the same codes for bad problems, pointers and alignment."""
+    assert L.raw_call_noalloc(16, 16, 16, 16, 16, 16, 16, 0.1, prob(**kw)) == code, L.last_error()
+    for i in (0, 3, 6):
+        ptrs = [16] * 7
+        ptrs[i] = None
+        assert L.raw_call_noalloc(*ptrs, 0.1, prob()) == L.EINVAL
+    ptrs = [64] * 7
+    ptrs[1] = 8
+    assert L.raw_call_noalloc(*ptrs, 0.1, prob()) == L.EINVAL and "aligned" in L.last_error()
+    assert L.raw_call_noalloc(None, None, None, None, None, None, None, 0.1, prob(num_seqs=0)) == L.OK
+    assert L.NOALLOC_SCRATCH_BYTES == 32 << 20
 
 
 def test_query_plan_variants_and_workspace():
