@@ -113,10 +113,18 @@ def _cores_note(avail, used):
 
 
 def _close_pool(pool):
-    """Terminate the oracle workers and wait for them and for the semaphore
-    tracker that the spawn start method runs, so no process outlives the bench."""
+    """Terminate the oracle workers and wait for them to exit."""
     pool.terminate()
     pool.join()
+
+
+def _stop_semaphore_tracker():
+    """Wait for the semaphore tracker process that the spawn start method
+    runs, once every pool (and so every semaphore) is gone, so that no process
+    outlives the bench."""
+    import gc
+
+    gc.collect()
     try:
         from multiprocessing import resource_tracker
         resource_tracker._resource_tracker._stop()
@@ -407,7 +415,7 @@ def time_decode(args, w, dev, shared_prefix=False, op="decode"):
                                    _lib.BF16, _lib._dtype_code(inp.k_cache, "k_cache"))
         nbytes, tokens = append_bytes(w, B), B
 
-    def step(i):
+    def step(i, sh=sh):
         kp, vp, sp = ptrs[i % ncopies]
         if op == "append":
             rc = _lib.raw_kv_append(k_new.data_ptr(), v_new.data_ptr(), kp, vp, sp, bp, positions.data_ptr(),
@@ -450,9 +458,49 @@ def time_decode(args, w, dev, shared_prefix=False, op="decode"):
           file=sys.stderr, flush=True)
     traffic = (measured_traffic(w.name + ("_shared" if shared is not None else ""), nbytes)
                if op == "decode" else None)
+    graph_ms = graph_call_ms(step, ncopies, args.steps, dev) if op == "decode" else None
     del caches, ptrs
     return dict(inp=inp, nbytes=nbytes, tokens=tokens, ncopies=ncopies, call_ms=call_ms, ms_per_step=ms_per_step,
-                spread=spread, status=status, traffic=traffic, shared=shared)
+                spread=spread, status=status, traffic=traffic, shared=shared, graph_ms=graph_ms)
+
+
+def graph_call_ms(step, ncopies, steps, dev):
+    """Per-call GPU time of the same calls replayed from a HIP graph: one
+    graph holds one call per cache copy (so replays still rotate the copies),
+    and it is replayed until at least ``steps`` calls have run, between two
+    HIP events on the replay stream. Launch costs of the host drop out; what
+    remains is the device's own time per call, gaps between kernels included."""
+    import torch
+
+    s = torch.cuda.Stream(dev)
+    step(0, s.cuda_stream)  # an eager call sizes the stream's workspace before the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for i in range(ncopies):
+            step(i, s.cuda_stream)
+    reps = max(1, math.ceil(steps / ncopies))
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        g.replay()  # warm-up replay
+        ev0.record(s)
+        for _ in range(reps):
+            g.replay()
+        ev1.record(s)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / (reps * ncopies)
+    del g
+    return ms
+
+
+def graph_fields(nbytes, graph_ms):
+    """Per-call figures of the HIP-graph replay (None when not measured)."""
+    if graph_ms is None:
+        return None
+    achieved = nbytes / (graph_ms * 1e-3) / 1e9
+    return {"call_us": round(graph_ms * 1e3, 2), "achieved": round(achieved, 2),
+            "frac": round(achieved / HBM_PEAK_GBS, 4)}
 
 
 def per_config_line(args, dev):
@@ -478,6 +526,7 @@ def per_config_line(args, dev):
             "traffic_over_algorithmic": round(r["traffic"] / r["nbytes"], 4) if r["traffic"] else None,
             "kv_tokens_per_s": round(r["tokens"] / (r["call_ms"] * 1e-3), 1),
             "single_call_us": r["spread"],
+            "graph_replay": graph_fields(r["nbytes"], r["graph_ms"]),
             "status": r["status"],
         }
         del r
@@ -602,6 +651,7 @@ def main():
             "algorithmic_bytes_per_call": nbytes,
             "call_us": round(call_ms * 1e3, 2),
             "single_call_us": r["spread"],
+            "graph_replay": graph_fields(nbytes, r["graph_ms"]),
         },
         "cpu_baseline": None,
     }
@@ -612,6 +662,7 @@ def main():
     if not args.no_cpu_baseline and args.op == "decode" and w.q_tokens == 1:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
+        _stop_semaphore_tracker()
     print(json.dumps(res), flush=True)
 
 
@@ -719,6 +770,7 @@ def prefill_main(args, w, dev):
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline_prefill(pin, args.cpu_budget)
+        _stop_semaphore_tracker()
     print(json.dumps(res), flush=True)
 
 
