@@ -113,6 +113,36 @@ def pin_scale_growth(o):
     assert s2 == s1 and np.array_equal(codes3[:2], codes2[:2])
 
 
+def pin_scale_growth_non_pow2(o):
+    """A token whose amax is 1.37 times the tile's grows the scale by a factor
+    that is not a power of two. The new scale is the token's amax / 448, and
+    every re-encoded code is a nearest E4M3 neighbour of the exact real
+    dec(c) * old / new (fp64 here), up to the float32 rounding of that
+    quotient: a re-encode that truncates, or that drops the division by the
+    new scale, is caught (a power-of-two growth cannot tell them apart)."""
+    rng = np.random.default_rng(21)
+    x0 = rng.standard_normal((3, 64)).astype(np.float32)
+    codes, s = np.zeros((16, 64), np.uint8), np.float32(0)
+    for t in range(3):
+        codes, s = o.append_tile_fp8(codes, s, t, x0[t])
+    amax0 = np.float32(np.abs(x0).max())
+    assert s == np.float32(amax0 / np.float32(448))   # the largest of the first tokens set it
+    x1 = rng.standard_normal(64).astype(np.float32)
+    x1 = (x1 * np.float32(1.37 * amax0 / np.abs(x1).max())).astype(np.float32)
+    grown, s1 = o.append_tile_fp8(codes, s, 3, x1)
+    assert s1 == np.float32(np.float32(np.abs(x1).max()) / np.float32(448))
+    ratio = float(s) / float(s1)
+    assert abs(np.log2(ratio) - np.rint(np.log2(ratio))) > 0.1, "growth must not be a power of two"
+    z = (oracle.e4m3fn_to_f64(codes[:3]) * float(s) / float(s1)).ravel()
+    got = oracle.e4m3fn_to_f64(grown[:3]).ravel()
+    finite = oracle.e4m3fn_to_f64(np.array([c for c in range(256) if c & 0x7F != 0x7F], np.uint8))
+    dmin = np.min(np.abs(finite[None, :] - z[:, None]), axis=1)
+    assert np.all(np.abs(got - z) <= dmin + 2.0 ** -22 * np.abs(z))
+    assert np.all((got == 0) | (np.sign(got) == np.sign(z)))
+    assert not np.array_equal(grown[:3], codes[:3])
+    assert np.array_equal(grown[4:], codes[4:])      # slots past the new token are untouched
+
+
 def _cache(kv, NB=6, hkv=2, d=64, seed=12):
     rng = np.random.default_rng(seed)
     if kv == "f32":
@@ -192,7 +222,7 @@ def pin_fp8_cache(o):
 
 
 PINS = [pin_e4m3_roundtrip, pin_e4m3_hand_ties, pin_e4m3_vs_torch, pin_bf16, pin_fresh_tile, pin_tile_recipe,
-        pin_scale_growth, pin_placement_and_flags, pin_append_then_attend, pin_fp8_cache]
+        pin_scale_growth, pin_scale_growth_non_pow2, pin_placement_and_flags, pin_append_then_attend, pin_fp8_cache]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -272,7 +302,42 @@ def _mut_v_token_major(mp):
     mp.setattr(ka, "paged_kv_append", bad)
 
 
+def _reencode_variant(mp, reencode):
+    """The oracle's tile policy with its re-encode step replaced."""
+    def bad(codes, old_scale, slot, x):
+        codes = codes.copy()
+        x = np.asarray(x, dtype=np.float32)
+        amax = np.float32(np.max(np.abs(x)))
+        old = np.float32(old_scale)
+        keep = slot > 0 and old > 0 and amax <= np.float32(np.float32(448) * old)
+        if keep:
+            scale = old
+        else:
+            scale = max(np.float32(amax / np.float32(448)), np.float32(2.0 ** -126))
+            if slot > 0:
+                codes[:slot] = reencode(oracle.e4m3fn_to_f64(codes[:slot]).astype(np.float32), old, scale)
+        codes[slot] = ka.encode_e4m3fn(x / scale)
+        return codes, scale
+    mp.setattr(ka, "append_tile_fp8", bad)
+
+
+def _mut_reencode_truncates(mp):
+    vals = oracle.e4m3fn_to_f64(np.arange(0x7F, dtype=np.uint8))
+
+    def trunc(prev, old, scale):  # round toward zero instead of to nearest
+        z = np.minimum(np.abs((prev * old) / scale).astype(np.float64), 448.0)
+        code = (np.searchsorted(vals, z, side="right") - 1).astype(np.uint8)
+        return np.where(np.signbit((prev * old) / scale), code | 0x80, code).astype(np.uint8)
+    _reencode_variant(mp, trunc)
+
+
+def _mut_reencode_drops_division(mp):
+    _reencode_variant(mp, lambda prev, old, scale: ka.encode_e4m3fn(prev * old))
+
+
 MUTANTS = {
+    "fp8_reencode_truncates": _mut_reencode_truncates,
+    "fp8_reencode_drops_division": _mut_reencode_drops_division,
     "e4m3_ties_away_from_zero": _mut_ties_away,
     "e4m3_overflow_to_nan": _mut_overflow_nan,
     "bf16_truncated": _mut_bf16_truncate,
