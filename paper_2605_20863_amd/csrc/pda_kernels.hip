@@ -65,6 +65,14 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr float kNegInf = -__builtin_inff();
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+// The lane index, recomputed where it is used: values derived from it (LDS
+// and output addresses of a segment's start and end) are then not hoisted
+// into registers that stay live across a segment's pair loop.
+__device__ __forceinline__ int lane_id_here() {
+  int l = (int)(threadIdx.x & 63);
+  asm volatile("" : "+v"(l));
+  return l;
+}
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -303,7 +311,7 @@ __device__ void plan_stream(const DecodeArgs& a, int wave, int32_t* pre, StreamP
 // first block-head is <= pos; empty sequences after it are skipped by the
 // caller) and cum_b, the blocks of the sequences before it.
 __device__ void locate(const DecodeArgs& a, const int32_t* pre, int64_t pos, int& b, int& cum_b) {
-  const int l = lane_id();
+  const int l = lane_id_here();
   if (a.E <= kLdsSeqs) {
     // first the 64-sequence tile (its first entry), then the sequence in it
     const int nt = (a.E + 63) >> 6;
@@ -683,7 +691,7 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
   // mem = col / G the member (shared-prefix entries) or the query token
   // (several per sequence), dims qdim(j, c) .. +8 for k-step j. q rows are
   // [sequence, query token, head].
-  int64_t qo_row[NT];
+  int qo_row[NT];  // < 2^31: the host bounds num_seqs * q_tokens * num_q_heads
   int hide[NT];
   bool on[NT];
   const int full = kBlockSize + a.Qn - 1;
@@ -694,10 +702,10 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
     const int col = 16 * n + r;
     const int mem = col / a.G, head = col - mem * a.G;
     on[n] = col < sg.ncols;
-    qo_row[n] = ((int64_t)sg.qs * a.Qn + mem) * a.Hq + kvh * a.G + head;
+    qo_row[n] = (sg.qs * a.Qn + mem) * a.Hq + kvh * a.G + head;
     // query token mem of Qn sits Qn - 1 - mem tokens before the sequence end
     hide[n] = a.Qn > 1 && mem < a.Qn ? a.Qn - 1 - mem : 0;
-    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + (on[n] ? qo_row[n] : 0) * D;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + (int64_t)(on[n] ? qo_row[n] : 0) * D;
 #pragma unroll
     for (int j = 0; j < C::KSTEPS; ++j) {
       u32x4 w = {0, 0, 0, 0};
@@ -782,7 +790,11 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
     if (!on[n]) continue;
     if (sg.final) {  // plain entry: the column is query token mem, head `head` of sequence qs
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
-      const int64_t orow = qo_row[n] * D;
+      // the row index stays live across the pair loop, the address is formed
+      // only here (an address formed at the start would hold two more registers)
+      int qrow_end = qo_row[n];
+      asm volatile("" : "+v"(qrow_end));
+      const int64_t orow = (int64_t)qrow_end * D;
       if (a.out_bf16) {
         uint16_t* o = static_cast<uint16_t*>(a.out) + orow;
 #pragma unroll
@@ -1089,7 +1101,7 @@ template <Variant V, KvType KV, int D, int GV>
 __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   __shared__ int32_t id_lds_all[kWavesPerGroupMax][kIdChunk];
   __shared__ int32_t pre_all[kWavesPerGroupMax][kLdsSeqs];
-  const int wave_in_group = threadIdx.x >> 6;
+  const int wave_in_group = uni(threadIdx.x >> 6);  // wave-uniform: the LDS bases stay in scalar registers
   int32_t* id_lds = id_lds_all[wave_in_group];
   int32_t* pre = pre_all[wave_in_group];
   const int wave = blockIdx.x * (blockDim.x >> 6) + wave_in_group;
