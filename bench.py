@@ -458,7 +458,7 @@ def time_decode(args, w, dev, shared_prefix=False, op="decode"):
           file=sys.stderr, flush=True)
     traffic = (measured_traffic(w.name + ("_shared" if shared is not None else ""), nbytes)
                if op == "decode" else None)
-    graph_ms = graph_call_ms(step, ncopies, args.steps, dev) if op == "decode" else None
+    graph_ms = graph_call_ms(step, ncopies, args.steps, dev) if op == "decode" and not args.no_graph else None
     del caches, ptrs
     return dict(inp=inp, nbytes=nbytes, tokens=tokens, ncopies=ncopies, call_ms=call_ms, ms_per_step=ms_per_step,
                 spread=spread, status=status, traffic=traffic, shared=shared, graph_ms=graph_ms)
@@ -551,6 +551,8 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for scaling rocprofv3 byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="decode: skip the HIP-graph replay timing (profiled runs trace the eager calls only)")
     ap.add_argument("--no-per-config", action="store_true",
                     help="decode: skip timing the other long-tailed GQA steps (" + ", ".join(PER_CONFIG) + ")")
     ap.add_argument("--op", default="decode", choices=["decode", "append", "prefill"],

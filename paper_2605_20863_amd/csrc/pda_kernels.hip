@@ -680,8 +680,12 @@ __device__ __forceinline__ void mfma_step(const MfmaPair<KV, D>& bf, const bf16x
 // kernel gives every segment the same depth, so the waves that carry two-tile
 // entries keep as many bytes in flight as the others and take an even share
 // of the bandwidth).
+// claim: this is the last segment of a chunk of a dynamic split; the claim for
+// the wave's next chunk (an atomic on the workspace counter, into `ticket` of
+// lane 0) is issued right after the segment's last tile loads.
 template <KvType KV, int D, int NT, int DEPTH>
-__device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds) {
+__device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds, bool claim,
+                             int& ticket) {
   using C = MfmaCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
@@ -734,6 +738,12 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
     mfma_step<KV, D, NT>(bf, qb, a.mfma_scale_log2, acc, m_run, l_run, full, hide);
   };
   auto issue = [&](MfmaPair<KV, D>& bf, int p) { mfma_issue<KV, D>(bf, a, ids, j_lo + 2 * p, j_hi, L, kvh, status); };
+  // The claim follows the last pair's loads: vector-memory operations complete
+  // in issue order for s_waitcnt, so a claim issued earlier would hold up every
+  // tile wait after it for the atomic's round trip.
+  auto claim_next = [&]() {
+    if (claim && l == 0) ticket = atomicAdd(a.hdr + kHdrNext, 1);
+  };
   static_assert(DEPTH == 2 || DEPTH == 3, "pairs in flight");
   if constexpr (DEPTH == 3) {
     // three pairs in flight (one bf16 wave per SIMD leaves the registers for it)
@@ -759,6 +769,7 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
       step(b1);
       if (i + 4 < npairs) issue(b1, i + 4);
     }
+    claim_next();  // every pair is issued
     if (i + 2 < npairs) step(b2);
     if (i + 3 < npairs) step(b0);
     if (i + 4 < npairs) step(b1);
@@ -777,10 +788,15 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
       step(b0);
       if (i + 2 < npairs) issue(b0, i + 2);
     }
+    claim_next();  // every pair is issued
     if (i + 1 < npairs) step(b1);
     if (i + 2 < npairs) step(b0);
   }
 
+  // the output section takes the lane index afresh: addresses derived from it
+  // here are then formed here, not kept in registers across the pair loop
+  const int lo = lane_id_here();
+  const int ro = lo & 15, co = lo >> 4;
 #pragma unroll
   for (int n = 0; n < NT; ++n) {
     // Lanes c = 0..3 hold disjoint token subsets of column r: total the denominator.
@@ -802,19 +818,19 @@ __device__ void mfma_segment(const DecodeArgs& a, const Seg& sg, int& status, in
           u32x2 w;
           w.x = f32_to_bf16_bits(acc[m][n][0] * inv) | (f32_to_bf16_bits(acc[m][n][1] * inv) << 16);
           w.y = f32_to_bf16_bits(acc[m][n][2] * inv) | (f32_to_bf16_bits(acc[m][n][3] * inv) << 16);
-          *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) = w;
+          *reinterpret_cast<u32x2*>(o + 16 * m + 4 * co) = w;
         }
       } else {
         float* o = static_cast<float*>(a.out) + orow;
 #pragma unroll
-        for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m][n] * inv;
+        for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * co) = acc[m][n] * inv;
       }
     } else {
-      const int64_t prow = sg.slot * a.Gp + 16 * n + r;
+      const int64_t prow = sg.slot * a.Gp + 16 * n + ro;
       float* arow = a.ws_acc + prow * D;
 #pragma unroll
-      for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(arow + 16 * m + 4 * c) = acc[m][n];
-      if (c == 0) {
+      for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(arow + 16 * m + 4 * co) = acc[m][n];
+      if (co == 0) {
         a.ws_m[prow] = m_run[n];
         a.ws_l[prow] = lt;
       }
@@ -998,7 +1014,8 @@ __device__ __forceinline__ void vec_step(const VecBlock<KV, D>& bk, const float 
 
 // Plain mode only (the host sends shared-prefix calls to the MFMA kernel).
 template <KvType KV, int D, int GV>
-__device__ void vec_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds) {
+__device__ void vec_segment(const DecodeArgs& a, const Seg& sg, int& status, int32_t* id_lds, bool claim,
+                            int& ticket) {
   using C = VecCfg<KV, D>;
   const int l = lane_id();
   const int r4 = l >> 4, c16 = l & 15;
@@ -1039,19 +1056,22 @@ __device__ void vec_segment(const DecodeArgs& a, const Seg& sg, int& status, int
 
   const int n = j_hi - j_lo;
   VecBlock<KV, D> b0, b1;
-  if (n > 0) vec_issue<KV, D>(b0, a, ids, j_lo, L, kvh, status);
-  if (n > 1) vec_issue<KV, D>(b1, a, ids, j_lo + 1, L, kvh, status);
+  auto issue = [&](VecBlock<KV, D>& bk, int i) { vec_issue<KV, D>(bk, a, ids, j_lo + i, L, kvh, status); };
+  if (n > 0) issue(b0, 0);
+  if (n > 1) issue(b1, 1);
   int i = 0;
   for (; i + 3 < n; i += 2) {
     vec_step<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
-    vec_issue<KV, D>(b0, a, ids, j_lo + i + 2, L, kvh, status);
+    issue(b0, i + 2);
     vec_step<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
-    vec_issue<KV, D>(b1, a, ids, j_lo + i + 3, L, kvh, status);
+    issue(b1, i + 3);
   }
   if (i < n) {
     vec_step<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
-    if (i + 2 < n) vec_issue<KV, D>(b0, a, ids, j_lo + i + 2, L, kvh, status);
+    if (i + 2 < n) issue(b0, i + 2);
   }
+  // as in the MFMA body, the claim follows the last block's loads
+  if (claim && l == 0) ticket = atomicAdd(a.hdr + kHdrNext, 1);
   if (i + 1 < n) vec_step<KV, D, GV>(b1, qf, a.scale_log2, acc, m_run, l_run);
   if (i + 2 < n) vec_step<KV, D, GV>(b0, qf, a.scale_log2, acc, m_run, l_run);
 
@@ -1110,10 +1130,13 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const bool dynamic = plan.nchunks > a.waves;
   int status = 0;
   for (int64_t c = wave; c < plan.nchunks;) {
-    // the next chunk is claimed as this one starts, so the claim's round trip
-    // overlaps the chunk's loads
+    // A dynamic split claims the wave's next chunk from the counter near the end
+    // of this one: after the tile loads of its last segment, so the claims come
+    // in the order waves finish and the round trip overlaps the last pairs'
+    // work. A chunk whose last segment is not known in advance (the chunk ends
+    // in a unit's start cost), or that holds no blocks, claims after its loop.
     int ticket = 0;
-    if (dynamic && lane_id() == 0) ticket = atomicAdd(a.hdr + kHdrNext, 1);
+    bool claimed = !dynamic;
     int64_t pos = c * plan.chunk;
     const int64_t end = pos + plan.chunk < plan.total ? pos + plan.chunk : plan.total;
     int v, cum_v;
@@ -1141,23 +1164,28 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       // this chunk's blocks: those that start in [pos, end)
       const int j_lo = r0 > f ? r0 - f : 0;
       const int j_hi = r_end > f ? r_end - f : 0;
+      // on to the start of block j_hi, or past the unit
+      const int64_t next = u0 + (j_hi < nb ? f + j_hi : nbw);
       if (j_lo < j_hi) {
         const Seg sg{e.row, e.L, j_lo, j_hi, kvh, e.qs, e.ncols, e.may_final && j_lo == 0 && j_hi == nb,
                      (int64_t)v * a.Hkv + kvh + c};
+        // the chunk's last segment: it reaches the chunk's end, or no entry follows
+        const bool claim = !claimed && (next >= end || (j_hi == nb && kvh + 1 == a.Hkv && v + 1 >= a.E));
+        claimed |= claim;
         if constexpr (V == Variant::Mfma && GV == kWideColumns) {
           // wide kernel: shared-prefix prefix entries, or several query tokens
           // per sequence, carry up to 32 columns
-          if (sg.ncols > 16) mfma_segment<KV, D, 2, 2>(a, sg, status, id_lds);
-          else mfma_segment<KV, D, 1, 2>(a, sg, status, id_lds);
+          if (sg.ncols > 16) mfma_segment<KV, D, 2, 2>(a, sg, status, id_lds, claim, ticket);
+          else mfma_segment<KV, D, 1, 2>(a, sg, status, id_lds, claim, ticket);
         } else if constexpr (V == Variant::Mfma) {
-          mfma_segment<KV, D, 1, KV == KvType::BF16 ? 3 : 2>(a, sg, status, id_lds);
+          mfma_segment<KV, D, 1, KV == KvType::BF16 ? 3 : 2>(a, sg, status, id_lds, claim, ticket);
         } else {
-          vec_segment<KV, D, GV>(a, sg, status, id_lds);
+          vec_segment<KV, D, GV>(a, sg, status, id_lds, claim, ticket);
         }
       }
-      // on to the start of block j_hi, or past the unit
-      pos = u0 + (j_hi < nb ? f + j_hi : nbw);
+      pos = next;
     }
+    if (!claimed && lane_id() == 0) ticket = atomicAdd(a.hdr + kHdrNext, 1);
     c = dynamic ? (int64_t)a.waves + uni(ticket) : plan.nchunks;
   }
   if (__any(status) && lane_id() == 0) atomicOr(a.hdr + kHdrStatus, status);
