@@ -658,13 +658,17 @@ def main():
         "cpu_baseline": None,
     }
     del r
-    if (args.op == "decode" and not args.shared_prefix and not args.no_per_config
-            and args.workload not in PER_CONFIG):
-        res["per_config"] = per_config_line(args, dev)
     if not args.no_cpu_baseline and args.op == "decode" and w.q_tokens == 1:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(inp, args.cpu_budget)
         _stop_semaphore_tracker()
+    if (args.op == "decode" and not args.shared_prefix and not args.no_per_config
+            and args.workload not in PER_CONFIG):
+        # the headline step's inputs are freed first: each step is timed on
+        # fresh allocations, as it would be in a run of its own
+        del inp
+        torch.cuda.empty_cache()
+        res["per_config"] = per_config_line(args, dev)
     print(json.dumps(res), flush=True)
 
 
