@@ -22,10 +22,10 @@
 //   Its query columns are (token, head) pairs, 256 / G tokens times the G query
 //   heads of the KV head; each wave owns 32 columns (2 MFMA N-tiles).
 // * The KV prefix up to the tile's last position is walked two 16-token blocks
-//   (32 keys) at a time. The workgroup loads a pair's K and V tiles, decodes
-//   them (fp8 codes to bf16 K; V to fp16, fp8 as code times the block's V
-//   scale) and writes them to LDS, a few pairs ahead of the one being
-//   computed. K rows are padded so 16 rows hit distinct banks; V rows are
+//   (32 keys) at a time. The workgroup loads a pair's K and V tiles two pairs
+//   ahead of the one being computed, decodes them (fp8 codes to bf16 K; V to
+//   fp16, fp8 as code times the block's V scale) and writes them to LDS one
+//   pair ahead. K rows are padded so 16 rows hit distinct banks; V rows are
 //   stored with the two blocks' tokens interleaved in the order the P^T
 //   operand holds them, so each lane reads its 8 keys at once.
 // * Per wave and pair: S^T[32 keys x 32 columns] = K . Q^T on
@@ -301,14 +301,14 @@ __device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a
     const int unit = (int)threadIdx.x + kPfThreads * u;
     const int blk = uni(unit / (C::TILEB / C::UB));  // the same for the whole wave
     const int off = (unit - blk * (C::TILEB / C::UB)) * C::UB;
-    const bool on = blk < 2 && ((blk & 1) ? ok[1] : ok[0]);  // selects: no dynamically indexed array
     const int64_t base = (blk & 1 ? tile[1] : tile[0]) * C::TILEB;  // uniform
-    // a block that is not loaded keeps stale values: its keys are masked (scores
-    // to -inf, V rows zeroed bitwise) on every path that could read them
-    if (on) {
-      st.k[u] = *reinterpret_cast<const Unit*>(kc + base + off);
-      st.v[u] = *reinterpret_cast<const Unit*>(vc + base + off);
-    }
+    // Unconditional: a block with no id reads tile 0 of its KV head and a unit
+    // past the pair's tiles reads inside them (never stored), so every path
+    // issues the same loads and the store that consumes them waits for its own
+    // pair's loads only. The keys of a block with no id are masked (scores to
+    // -inf, V rows zeroed bitwise) on every path that could read them.
+    st.k[u] = *reinterpret_cast<const Unit*>(kc + base + off);
+    st.v[u] = *reinterpret_cast<const Unit*>(vc + base + off);
   }
 }
 
@@ -585,32 +585,41 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     }
   };
 
-  // Pair j + 1's tiles are loaded while pair j is computed; pair j comes from
-  // LDS buffer j % 2. (Running the two waves of a SIMD half a pair apart, so
-  // one's softmax would overlap the other's matrix work, measured slower.)
-  PfStage<KV, D> st;
+  // Pair j + 2's tiles are loaded while pair j is computed and pair j + 1 is
+  // staged: two register sets, the loop unrolled by two so neither set is ever
+  // copied (a copy would wait for its loads at once). Pair j comes from LDS
+  // buffer j % 2. (Running the two waves of a SIMD half a pair apart, so one's
+  // softmax would overlap the other's matrix work, measured slower.)
+  PfStage<KV, D> st0, st1;  // pairs of even and odd index
   PfIds ids;
   ids.q = -1;
   ids.nxt = pf_id_load(a, row, l, nblk, status);  // chunk 0, entered by the first load
   PfMeta mj{1.f, 1.f, 0};
   if (npairs > 0) {
-    pf_load<KV, D>(st, a, ids, row, 0, nblk, nkeys, kvh, status);
-    pf_store<KV, D>(st, lds, status);
-    mj = pf_meta<KV, D>(st, a.scale_log2);
+    pf_load<KV, D>(st0, a, ids, row, 0, nblk, nkeys, kvh, status);
+    pf_store<KV, D>(st0, lds, status);
+    mj = pf_meta<KV, D>(st0, a.scale_log2);
   }
+  if (npairs > 1) pf_load<KV, D>(st1, a, ids, row, 2, nblk, nkeys, kvh, status);
   __syncthreads();
-  for (int j2 = 0; j2 < npairs; ++j2) {
-    if (j2 + 1 < npairs) pf_load<KV, D>(st, a, ids, row, 2 * (j2 + 1), nblk, nkeys, kvh, status);
+  // sl: free set, receives pair j2 + 2; ss: holds pair j2 + 1
+  auto step = [&](int j2, PfStage<KV, D>& sl, PfStage<KV, D>& ss) {
+    // past the end the last pair is loaded again (unused): the same loads on every step
+    pf_load<KV, D>(sl, a, ids, row, 2 * (j2 + 2 < npairs ? j2 + 2 : npairs - 1), nblk, nkeys, kvh, status);
     if (j2 < wpairs) {
       f32x4 s0[kPfNT], s1[kPfNT];
       pf_scores<KV, D>(lds + (j2 & 1) * C::BUF, qb, s0, s1);
       finish(j2, s0, s1, mj);
     }
     if (j2 + 1 < npairs) {
-      pf_store<KV, D>(st, lds + ((j2 + 1) & 1) * C::BUF, status);
-      mj = pf_meta<KV, D>(st, a.scale_log2);
+      pf_store<KV, D>(ss, lds + ((j2 + 1) & 1) * C::BUF, status);
+      mj = pf_meta<KV, D>(ss, a.scale_log2);
     }
     __syncthreads();
+  };
+  for (int j2 = 0; j2 < npairs; j2 += 2) {
+    step(j2, st0, st1);
+    if (j2 + 1 < npairs) step(j2 + 1, st1, st0);
   }
   if (status) atomicOr(a.hdr + kHdrStatus, status);  // error paths only
   if (!wave_on) return;
