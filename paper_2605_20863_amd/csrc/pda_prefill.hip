@@ -22,10 +22,10 @@
 //   Its query columns are (token, head) pairs, 256 / G tokens times the G query
 //   heads of the KV head; each wave owns 32 columns (2 MFMA N-tiles).
 // * The KV prefix up to the tile's last position is walked two 16-token blocks
-//   (32 keys) at a time. The workgroup loads a pair's K and V tiles two pairs
-//   ahead of the one being computed, decodes them (fp8 codes to bf16 K; V to
-//   fp16, fp8 as code times the block's V scale) and writes them to LDS one
-//   pair ahead. K rows are padded so 16 rows hit distinct banks; V rows are
+//   (32 keys, a pair) at a time, two pairs per barrier. The workgroup loads the
+//   next two pairs' K and V tiles while it computes the current two, decodes
+//   them (fp8 codes to bf16 K; V to fp16, fp8 as code times the block's V
+//   scale) and writes them to the other two of four LDS buffers. K rows are padded so 16 rows hit distinct banks; V rows are
 //   stored with the two blocks' tokens interleaved in the order the P^T
 //   operand holds them, so each lane reads its 8 keys at once.
 // * Per wave and pair: S^T[32 keys x 32 columns] = K . Q^T on
@@ -515,7 +515,7 @@ __device__ __forceinline__ PfMeta pf_meta(const PfStage<KV, D>& st, float scale_
 template <KvType KV, int D>
 __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   using C = PfCfg<KV, D>;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * C::BUF];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[4 * C::BUF];
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
   const int w = uni((int)(threadIdx.x >> 6));  // wave-uniform: keeps per-wave values scalar
@@ -572,7 +572,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   // wave does not see every key of the pair, or a key is past the tile
   auto finish = [&](int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const PfMeta& m) {
     const int key0 = 32 * j2;
-    const uint8_t* buf = lds + (j2 & 1) * C::BUF;
+    const uint8_t* buf = lds + (j2 & 3) * C::BUF;
     int see[kPfNT];
     if (key0 + 31 <= pos_lo && m.live >= 32) {
 #pragma unroll
@@ -585,41 +585,53 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     }
   };
 
-  // Pair j + 2's tiles are loaded while pair j is computed and pair j + 1 is
-  // staged: two register sets, the loop unrolled by two so neither set is ever
-  // copied (a copy would wait for its loads at once). Pair j comes from LDS
-  // buffer j % 2. (Running the two waves of a SIMD half a pair apart, so one's
+  // Two pairs per barrier: step j computes pairs j and j + 1 from LDS buffers
+  // j % 4 and (j + 1) % 4 while pairs j + 2 and j + 3 are loaded into two
+  // register sets and staged into the other two buffers. The loads are
+  // unconditional (past the end the last pair again, never stored), so no
+  // loaded register is merged across paths: a copy of one would wait for its
+  // load at once. (Running the two waves of a SIMD half a pair apart, so one's
   // softmax would overlap the other's matrix work, measured slower.)
-  PfStage<KV, D> st0, st1;  // pairs of even and odd index
+  PfStage<KV, D> sa, sb;
   PfIds ids;
   ids.q = -1;
   ids.nxt = pf_id_load(a, row, l, nblk, status);  // chunk 0, entered by the first load
-  PfMeta mj{1.f, 1.f, 0};
+  PfMeta m0{1.f, 1.f, 0}, m1{1.f, 1.f, 0};
   if (npairs > 0) {
-    pf_load<KV, D>(st0, a, ids, row, 0, nblk, nkeys, kvh, status);
-    pf_store<KV, D>(st0, lds, status);
-    mj = pf_meta<KV, D>(st0, a.scale_log2);
+    pf_load<KV, D>(sa, a, ids, row, 0, nblk, nkeys, kvh, status);
+    pf_store<KV, D>(sa, lds, status);
+    m0 = pf_meta<KV, D>(sa, a.scale_log2);
   }
-  if (npairs > 1) pf_load<KV, D>(st1, a, ids, row, 2, nblk, nkeys, kvh, status);
+  if (npairs > 1) {
+    pf_load<KV, D>(sb, a, ids, row, 2, nblk, nkeys, kvh, status);
+    pf_store<KV, D>(sb, lds + C::BUF, status);
+    m1 = pf_meta<KV, D>(sb, a.scale_log2);
+  }
   __syncthreads();
-  // sl: free set, receives pair j2 + 2; ss: holds pair j2 + 1
-  auto step = [&](int j2, PfStage<KV, D>& sl, PfStage<KV, D>& ss) {
+  for (int j2 = 0; j2 < npairs; j2 += 2) {
     // past the end the last pair is loaded again (unused): the same loads on every step
-    pf_load<KV, D>(sl, a, ids, row, 2 * (j2 + 2 < npairs ? j2 + 2 : npairs - 1), nblk, nkeys, kvh, status);
+    const int ja = j2 + 2 < npairs ? j2 + 2 : npairs - 1, jb = j2 + 3 < npairs ? j2 + 3 : npairs - 1;
+    pf_load<KV, D>(sa, a, ids, row, 2 * ja, nblk, nkeys, kvh, status);
+    pf_load<KV, D>(sb, a, ids, row, 2 * jb, nblk, nkeys, kvh, status);
     if (j2 < wpairs) {
       f32x4 s0[kPfNT], s1[kPfNT];
-      pf_scores<KV, D>(lds + (j2 & 1) * C::BUF, qb, s0, s1);
-      finish(j2, s0, s1, mj);
+      pf_scores<KV, D>(lds + (j2 & 3) * C::BUF, qb, s0, s1);
+      finish(j2, s0, s1, m0);
     }
-    if (j2 + 1 < npairs) {
-      pf_store<KV, D>(ss, lds + ((j2 + 1) & 1) * C::BUF, status);
-      mj = pf_meta<KV, D>(ss, a.scale_log2);
+    if (j2 + 1 < wpairs) {
+      f32x4 s0[kPfNT], s1[kPfNT];
+      pf_scores<KV, D>(lds + ((j2 + 1) & 3) * C::BUF, qb, s0, s1);
+      finish(j2 + 1, s0, s1, m1);
+    }
+    if (j2 + 2 < npairs) {
+      pf_store<KV, D>(sa, lds + ((j2 + 2) & 3) * C::BUF, status);
+      m0 = pf_meta<KV, D>(sa, a.scale_log2);
+    }
+    if (j2 + 3 < npairs) {
+      pf_store<KV, D>(sb, lds + ((j2 + 3) & 3) * C::BUF, status);
+      m1 = pf_meta<KV, D>(sb, a.scale_log2);
     }
     __syncthreads();
-  };
-  for (int j2 = 0; j2 < npairs; j2 += 2) {
-    step(j2, st0, st1);
-    if (j2 + 1 < npairs) step(j2 + 1, st1, st0);
   }
   if (status) atomicOr(a.hdr + kHdrStatus, status);  // error paths only
   if (!wave_on) return;
