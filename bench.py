@@ -87,9 +87,9 @@ def prefill_flops(workload, seq_lens, counts):
 
 # ----------------------------------------------------------------- CPU baseline
 
-# A GPU machine gives the process of one GPU this many host cores (its share of
-# the host, whatever the affinity mask shows); more workers would only
-# oversubscribe them.
+# Host cores that the process driving one MI355X may use: one GPU's share of
+# an 8-GPU host's cores, whatever the affinity mask shows; more workers would
+# only oversubscribe them.
 CPU_SHARE = 16
 
 
