@@ -113,6 +113,54 @@ def oracle_whole(inp, what="", q=None):
     return ref
 
 
+def _prefill_rows_job(pin, b, i0, i1):
+    """Query rows i0 .. i1 - 1 of prefill sequence b as a self-contained oracle
+    problem (data movement only). Row i sits at position L - n + i, so these
+    rows are the last i1 - i0 query tokens of the same sequence cut to
+    L - n + i1 tokens: its first blocks, copied out, with a block table
+    renumbered to them."""
+    c = pin.cache
+    lay = c.layout
+    n, L = int(pin.counts[b]), int(lay.seq_lens[b])
+    Lc = L - n + i1
+    nb = (max(Lc, 0) + 15) // 16
+    phys, local = np.unique(lay.block_table[b, :nb].astype(np.int64), return_inverse=True)
+    if phys.size == 0:
+        phys, local = np.zeros(1, dtype=np.int64), np.zeros(0, dtype=np.int64)
+    idx = torch.from_numpy(phys).to(c.k_cache.device)
+    table = np.full((1, max(nb, 1)), -1, dtype=np.int32)
+    table[0, :nb] = local
+    r0 = int(pin.offsets[b])
+    kw = dict(q=raw(pin.q[r0 + i0:r0 + i1]), q_offsets=np.array([0, i1 - i0], dtype=np.int32),
+              k_cache=raw(c.k_cache.index_select(0, idx)), v_cache=raw(c.v_cache.index_select(0, idx)),
+              block_table=table, seq_lens=np.array([max(Lc, 0)], dtype=np.int32), softmax_scale=c.softmax_scale,
+              q_dtype="bf16", kv_dtype=c.workload.kv_dtype,
+              kv_scales=raw(c.kv_scales.index_select(1, idx)) if c.kv_scales is not None else None)
+    return "prefill", (r0 + i0, r0 + i1), kw
+
+
+def oracle_prefill_whole(pin, what="", rows_per_job=64):
+    """Oracle output [T, Hq, D] of every query row of prefill ``pin``, computed
+    over slices of ``rows_per_job`` rows in the worker pool of
+    ``tests._oracle_pool``, longest sequences first."""
+    from tests import _oracle_pool as P
+
+    T = int(pin.q.shape[0])
+    ref = np.zeros(tuple(pin.q.shape), dtype=np.float64)
+
+    def put(rows, out):
+        ref[rows[0]:rows[1]] = out
+
+    lens = pin.cache.layout.seq_lens
+    slices = ((int(b), i0, min(i0 + rows_per_job, int(pin.counts[b])))
+              for b in np.argsort(-lens.astype(np.int64), kind="stable")
+              for i0 in range(0, int(pin.counts[b]), rows_per_job))
+    t = P.run_jobs((_prefill_rows_job(pin, b, i0, i1) for b, i0, i1 in slices), put,
+                   progress=lambda done, s: print(f"[oracle] {what}: {done} row slices, {s:.0f} s", flush=True))
+    print(f"[oracle] {what}: {T} rows in {t:.1f} s on {P.cores_used()} worker processes", flush=True)
+    return ref
+
+
 def worst_row_rel_l2(got: np.ndarray, ref: np.ndarray):
     """Largest relative L2 error of one output row (one sequence and query
     head, over D), with its index; rows whose reference is zero use the

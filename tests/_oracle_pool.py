@@ -1,9 +1,9 @@
 """Run the CPU fp64 oracle over many sequences at once, one process per core.
 
 Test infrastructure: the full-size parity tests compare every output of a
-decode step with the oracle, and the oracle is plain numpy that handles one
-sequence at a time, so the sequences are spread over a pool of worker
-processes. Workers are started with ``spawn`` (never ``fork`` from a process
+decode step (and of the chunked prefill) with the oracle, and the oracle is
+plain numpy that handles one sequence at a time, so the sequences (or slices of
+a sequence's query rows) are spread over a pool of worker processes. Workers are started with ``spawn`` (never ``fork`` from a process
 that has initialised the GPU) and import nothing but numpy and ``oracle``.
 
 Jobs are self-contained one-sequence problems (the sequence's query rows, its
@@ -20,8 +20,8 @@ import time
 
 _POOL = None
 _CORES = 0
-# A GPU machine gives one GPU's process this many cores; a pool larger than that
-# only oversubscribes them.
+# Host cores that the process driving one MI355X may use (one GPU's share of
+# an 8-GPU host); a pool larger than that only oversubscribes them.
 MAX_CORES = 16
 
 
@@ -40,7 +40,8 @@ def _run(job):
 
     kind, key, kw = job
     fn = {"decode": oracle.paged_decode_attention,
-          "multi_token": oracle.paged_multi_token_attention}[kind]
+          "multi_token": oracle.paged_multi_token_attention,
+          "prefill": oracle.paged_prefill_attention}[kind]
     return key, fn(**kw)
 
 

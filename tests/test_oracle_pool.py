@@ -1,7 +1,9 @@
 """The pooled oracle that the full-size GPU parity tests use (one sequence per
 worker job, each job a copy of that sequence's own blocks) gives exactly the
 one-process oracle's output, for plain, GRPO (shared blocks), fp8 and
-multi-token inputs, including empty sequences. Runs on the CPU."""
+multi-token inputs, including empty sequences; and the prefill's row-slice
+jobs (a sequence's query rows split into slices, each a cut of the sequence)
+give exactly the one-process prefill oracle. Runs on the CPU."""
 
 import numpy as np
 import torch
@@ -28,6 +30,22 @@ def test_pooled_oracle_equals_one_process_oracle():
         q_dtype="bf16", kv_dtype="fp8_e4m3", kv_scales=U.raw(inp.kv_scales))
     assert np.array_equal(whole, ref)
     assert P.cores_used() == min(P.cores_available(), P.MAX_CORES)
+
+
+def test_pooled_prefill_oracle_equals_one_process_oracle():
+    import oracle
+    for kv in ("bf16", "fp8_e4m3"):
+        w = W.Workload(f"pool_pf_{kv}", 5, 8, 2, 64, "bf16", kv, ("uniform", 1, 1), cfg_id=56, prefill_chunk=100)
+        # lengths with an empty sequence, one shorter than its chunk and one of
+        # several slices; counts include one with tokens at negative positions
+        pin = W.generate_prefill(w, "cpu", seq_lens=[0, 40, 300, 17, 129], q_counts=[0, 40, 150, 30, 129])
+        c = pin.cache
+        ref = oracle.paged_prefill_attention(
+            q=U.raw(pin.q), q_offsets=pin.offsets, k_cache=U.raw(c.k_cache), v_cache=U.raw(c.v_cache),
+            block_table=c.layout.block_table, seq_lens=c.layout.seq_lens, softmax_scale=c.softmax_scale,
+            q_dtype="bf16", kv_dtype=kv, kv_scales=U.raw(c.kv_scales) if c.kv_scales is not None else None)
+        whole = U.oracle_prefill_whole(pin, kv, rows_per_job=37)
+        assert np.array_equal(whole, ref), kv
 
 
 def test_worst_row_diagnostic():
