@@ -16,6 +16,7 @@
 #include <map>
 #include <memory>
 #include <mutex>
+#include <numeric>
 #include <string>
 #include <tuple>
 #include <utility>
@@ -670,6 +671,8 @@ int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, co
   a.len_shift = shift;
   a.items_max = (int32_t)items_max;
   a.out_bf16 = pr->out_dtype == PDA_DTYPE_BF16;
+  a.cus = di.cus;
+  a.nq = std::gcd(a.Hkv, 8);
   a.hdr = reinterpret_cast<int32_t*>(base);
   a.items = reinterpret_cast<int4*>(base + items_off);
   const pda::KvType kv = kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8;

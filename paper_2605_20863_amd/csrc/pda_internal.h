@@ -37,6 +37,7 @@ constexpr int kHdrStatus = 0;
 constexpr int kHdrShare = 1;  // block-heads per chunk (decode writes, combine reads)
 constexpr int kHdrNext = 2;   // chunk counter of a dynamic split; zero between calls
 constexpr int kHdrItems = 3;  // prefill: work items the plan kernel listed
+constexpr int kHdrPfQueue = 8;  // prefill: words 8..15, the unit counters of the attention grid's queues
 constexpr int kHdrWords = 16;
 
 // Everything one decode step's kernels need. Plain data; passed by value.
@@ -132,9 +133,11 @@ struct PrefillArgs {
   int64_t num_blocks;
   int32_t len_cap;
   int32_t len_shift;    // sort key: length >> len_shift, below kPfBuckets
-  int32_t items_max;    // bound on the work items: the grid is items_max * Hkv
+  int32_t items_max;    // bound on the work items (units: items x KV heads)
   int32_t out_bf16;
-  int32_t* hdr;         // workspace header (status, item count)
+  int32_t cus;          // compute units of the device
+  int32_t nq;           // unit queues: gcd(Hkv, 8)
+  int32_t* hdr;         // workspace header (status, item count, queue counters)
   int4* items;          // [items_max] {sequence, first q row, tokens, first position}
 };
 

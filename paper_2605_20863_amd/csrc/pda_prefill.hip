@@ -13,14 +13,19 @@
 // * Plan kernel (one workgroup): per sequence, its tiles of 256 / G query
 //   tokens; sequences sorted by length, longest first (counting sort on the
 //   length), and a work list of (sequence, tile) items, each sequence's last
-//   (heaviest) tile first. Workgroup i of the attention kernel takes item
-//   i / Hkv for KV head i % Hkv: the KV heads of one tile go to consecutive
-//   workgroups, which the dispatcher deals round-robin over the 8 XCDs, so with
-//   8 KV heads each XCD serves one KV head and its L2 holds only that head's
-//   keys and values, read by every tile of the sequence at nearly the same time.
-// * Attention kernel: one workgroup (8 waves, 2 per SIMD) per (item, KV head).
-//   Its query columns are (token, head) pairs, 256 / G tokens times the G query
-//   heads of the KV head; each wave owns 32 columns (2 MFMA N-tiles).
+//   (heaviest) tile first.
+// * Attention kernel: a persistent grid, one workgroup (8 waves, 2 per SIMD)
+//   per CU, that takes (item, KV head) units from queues, so a CU goes from one
+//   unit to the next without a workgroup launch between them (which cost ~4 us
+//   per unit, with the drain of the last workgroup's waves). There are
+//   nq = gcd(Hkv, 8) queues; queue x holds the units of KV heads x, x + nq, ...
+//   in item order, and workgroup i works on queue (i % 8) % nq. The dispatcher
+//   deals workgroups round-robin over the 8 XCDs, so with 4 or 8 KV heads each
+//   XCD serves one KV head and its L2 holds only that head's keys and values,
+//   read by every tile of a sequence at nearly the same time (a drained queue
+//   sends its workgroups to the others; correctness never depends on the XCD).
+//   A unit's query columns are (token, head) pairs, 256 / G tokens times the G
+//   query heads of the KV head; each wave owns 32 columns (2 MFMA N-tiles).
 // * The KV prefix up to the tile's last position is walked two 16-token blocks
 //   (32 keys, a pair) at a time, two pairs per barrier. The workgroup loads the
 //   next two pairs' K and V tiles while it computes the current two, decodes
@@ -44,6 +49,7 @@
 
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 namespace pda {
@@ -141,6 +147,7 @@ __global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PrefillArgs 
   __shared__ int wave_sum[kPlanThreads / 64];
   const int tid = (int)threadIdx.x;
   for (int i = tid; i < kPfBuckets; i += kPlanThreads) cursor[i] = 0;
+  if (tid < 8) a.hdr[kHdrPfQueue + tid] = 0;
   __syncthreads();
   int status = 0;
   bool bad = false;
@@ -239,51 +246,44 @@ struct PfStage {
 // pair's ids come from v_readlane instead of a scalar load per block.
 struct PfIds {
   int q;          // current chunk
-  int id, nxt;    // ids of chunk q and of chunk q + 1 (-1: past the tile or out of range)
-  float ks, vs;   // fp8 scales of chunk q's blocks
+  int id, nxt;    // table entries of chunks q and q + 1, unchecked (lanes past the tile repeat its last block)
 };
 
-__device__ __forceinline__ int pf_id_load(const PrefillArgs& a, const int32_t* row, int j, int nblk, int& status) {
-  if (j >= nblk) return -1;
-  const int p = row[j];
-  if ((unsigned)p >= (uint64_t)a.num_blocks) {
-    status |= kStatusBadBlock;
-    return -1;
-  }
-  return p;
+// Unconditional, and checked only where a pair reads it (pf_load): a check
+// here would wait for the load at once and the next chunk would not be
+// prefetched. The table row has max_blocks >= 1 entries and nblk <= max_blocks.
+__device__ __forceinline__ int pf_id_load(const int32_t* row, int j, int nblk) {
+  const int last = nblk > 0 ? nblk - 1 : 0;
+  return row[j < last ? j : last];
 }
 
-template <KvType KV>
-__device__ __forceinline__ void pf_ids_enter(PfIds& ids, const PrefillArgs& a, const int32_t* row, int q, int nblk,
-                                             int kvh, int& status) {
-  const int l = lane_id();
+// Moves the ids to chunk q (q is ids.q or ids.q + 1) and loads chunk q + 1.
+// Unconditional: no loaded register is merged across paths (a copy of one
+// waits for its load), and the select reads a load issued a step earlier.
+__device__ __forceinline__ void pf_ids_advance(PfIds& ids, const int32_t* row, int q, int nblk) {
+  ids.id = q != ids.q ? ids.nxt : ids.id;
   ids.q = q;
-  ids.id = ids.nxt;
-  ids.nxt = pf_id_load(a, row, 64 * (q + 1) + l, nblk, status);
-  if constexpr (KV == KvType::FP8) {
-    const int64_t tile = (int64_t)(ids.id < 0 ? 0 : ids.id) * a.Hkv + kvh;
-    ids.ks = ids.id < 0 ? 1.f : a.kv_scales[tile];
-    ids.vs = ids.id < 0 ? 1.f : a.kv_scales[a.num_blocks * a.Hkv + tile];
-  }
+  ids.nxt = pf_id_load(row, 64 * (q + 1) + lane_id(), nblk);
 }
 
 template <KvType KV, int D>
-__device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, PfIds& ids, const int32_t* row,
-                                        int j0, int nblk, int nkeys, int kvh, int& status) {
+__device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, const PfIds& ids, int j0, int nblk,
+                                        int nkeys, int kvh, int& status) {
   using C = PfCfg<KV, D>;
-  if ((j0 >> 6) != ids.q) pf_ids_enter<KV>(ids, a, row, j0 >> 6, nblk, kvh, status);
   int64_t tile[2];
   int ok[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int p = __builtin_amdgcn_readlane(ids.id, (j0 + s) & 63);
-    ok[s] = p >= 0;
+    const bool inside = j0 + s < nblk;  // the block holds keys of the tile
+    ok[s] = inside && (uint64_t)(uint32_t)p < (uint64_t)a.num_blocks;
+    if (inside && !ok[s]) status |= kStatusBadBlock;
     tile[s] = (int64_t)(ok[s] ? p : 0) * a.Hkv + kvh;
     st.ks[s] = 1.f;
     st.vs[s] = 1.f;
-    if constexpr (KV == KvType::FP8) {
-      st.ks[s] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ids.ks), (j0 + s) & 63));
-      st.vs[s] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ids.vs), (j0 + s) & 63));
+    if constexpr (KV == KvType::FP8) {  // raw: a block with no id takes scale 1 where they are used
+      st.ks[s] = a.kv_scales[tile[s]];
+      st.vs[s] = a.kv_scales[a.num_blocks * a.Hkv + tile[s]];
     }
   }
   st.ok0 = ok[0];
@@ -368,7 +368,7 @@ __device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf,
       const u32x2 a0 = fp8x4_to_bf16x4(st.k[u].x), a1 = fp8x4_to_bf16x4(st.k[u].y);
       *reinterpret_cast<u32x4*>(kdst) = u32x4{a0.x, a0.y, a1.x, a1.y};
       // V: tokens t0 .. t0 + 7 of dim row d, code * scale in fp32, one rounding to fp16
-      const float vs = (blk & 1) ? st.vs[1] : st.vs[0];
+      const float vs = (blk & 1) ? (st.ok1 ? st.vs[1] : 1.f) : (st.ok0 ? st.vs[0] : 1.f);
       float f[8];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
@@ -509,150 +509,185 @@ struct PfMeta {
 template <KvType KV, int D>
 __device__ __forceinline__ PfMeta pf_meta(const PfStage<KV, D>& st, float scale_log2) {
   // c > 0: a zero or tiny scale leaves every weight at 1 either way
-  return PfMeta{fmaxf(scale_log2 * st.ks[0], 1e-30f), fmaxf(scale_log2 * st.ks[1], 1e-30f), st.live};
+  const float k0 = st.ok0 ? st.ks[0] : 1.f, k1 = st.ok1 ? st.ks[1] : 1.f;
+  return PfMeta{fmaxf(scale_log2 * k0, 1e-30f), fmaxf(scale_log2 * k1, 1e-30f), st.live};
 }
 
 template <KvType KV, int D>
 __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   using C = PfCfg<KV, D>;
   __shared__ __attribute__((aligned(16))) uint8_t lds[4 * C::BUF];
+  __shared__ int s_next[2];
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
   const int w = uni((int)(threadIdx.x >> 6));  // wave-uniform: keeps per-wave values scalar
-  const int kvh = (int)(blockIdx.x % (unsigned)a.Hkv);
-  const int item = (int)(blockIdx.x / (unsigned)a.Hkv);
-  if (item >= a.hdr[kHdrItems]) return;  // the whole workgroup leaves together
-  const int4 it = a.items[item];
-  const int b = it.x, row0 = it.y, nt = it.z, first = it.w;
-
-  // this wave's columns: column col = 32w + 16n + r is token col / G, head col % G
-  int vis[kPfNT], tokq[kPfNT];
-  bf16x8 qb[kPfNT][C::KSTEPS];
-  const uint32_t qflip = a.neg_scale ? 0x80008000u : 0u;  // a negative scale goes into q's sign
-#pragma unroll
-  for (int n = 0; n < kPfNT; ++n) {
-    const int col = kPfWaveCols * w + 16 * n + r;
-    const int tok = col / a.G, head = col - tok * a.G;
-    const bool ok = tok < nt;
-    vis[n] = first + tok + 1;  // keys the column sees
-    tokq[n] = ok ? ((row0 + tok) * a.Hq + kvh * a.G + head) : -1;
-    const uint16_t* qp = static_cast<const uint16_t*>(a.q) + (int64_t)(ok ? tokq[n] : 0) * D;
-#pragma unroll
-    for (int j = 0; j < C::KSTEPS; ++j) {
-      u32x4 v = {0, 0, 0, 0};
-      if (ok) v = *reinterpret_cast<const u32x4*>(qp + 32 * j + 8 * c);
-      qb[n][j] = __builtin_bit_cast(bf16x8, v ^ qflip);
-    }
-  }
-  const int tok_lo = kPfWaveCols * w / a.G;
-  const int tok_hi_raw = (kPfWaveCols * w + kPfWaveCols - 1) / a.G;
-  const int tok_hi = tok_hi_raw < nt - 1 ? tok_hi_raw : nt - 1;
-  const bool wave_on = tok_lo < nt;
-  const int pos_lo = first + tok_lo;  // this wave's first and last query positions
-  const int pos_hi = first + tok_hi;
-
-  const int nkeys = first + nt > 0 ? first + nt : 0;  // keys up to the tile's last position
-  const int npairs = (nkeys + 31) / 32;
-  const int nblk = (nkeys + 15) / 16;
-  // pairs this wave computes: those with a key at or before its last position
-  const int wpairs = !wave_on || pos_hi < 0 ? 0 : (pos_hi / 32 + 1 < npairs ? pos_hi / 32 + 1 : npairs);
-  const int32_t* row = a.block_table + (int64_t)b * a.max_blocks;
+  // Unit n of queue x is item n / hq for KV head x + nq (n % hq). The grid
+  // (a multiple of 8 workgroups) starts on the first gridDim / nq units of each
+  // queue; each further unit is claimed with a ticket from the queue's counter
+  // in the workspace header (zeroed by the plan kernel). Unit k's claim is
+  // issued as unit k starts and published in s_next[k & 1] at its first
+  // barrier; every thread reads it after its last, so a slot is rewritten only
+  // after all threads read it (two units later).
+  const int nq = a.nq, hq = a.Hkv / nq;
+  const int qsize = uni(a.hdr[kHdrItems]) * hq;  // units per queue
+  const int first_claims = (int)gridDim.x / nq;
+  const int xq = (int)(blockIdx.x & 7u);
+  const int q = xq % nq;
+  int un = (int)(blockIdx.x >> 3) * (8 / nq) + xq / nq, uq = q;  // current unit: index, queue
   int status = 0;
+  for (int k = 0; un < qsize; ++k) {
+    const int item = un / hq, kvh = uq + nq * (un - item * hq);
+    int tick = 0;
+    if (threadIdx.x == 0) tick = atomicAdd(a.hdr + kHdrPfQueue + q, 1);
+    const int4 it = a.items[item];
+    const int b = it.x, row0 = it.y, nt = it.z, first = it.w;
 
-  f32x4 acc[C::MT][kPfNT];
+    // this wave's columns: column col = 32w + 16n + r is token col / G, head col % G
+    int vis[kPfNT], tokq[kPfNT];
+    bf16x8 qb[kPfNT][C::KSTEPS];
+    const uint32_t qflip = a.neg_scale ? 0x80008000u : 0u;  // a negative scale goes into q's sign
 #pragma unroll
-  for (int m = 0; m < C::MT; ++m)
+    for (int n = 0; n < kPfNT; ++n) {
+      const int col = kPfWaveCols * w + 16 * n + r;
+      const int tok = col / a.G, head = col - tok * a.G;
+      const bool ok = tok < nt;
+      vis[n] = first + tok + 1;  // keys the column sees
+      tokq[n] = ok ? ((row0 + tok) * a.Hq + kvh * a.G + head) : -1;
+      const uint16_t* qp = static_cast<const uint16_t*>(a.q) + (int64_t)(ok ? tokq[n] : 0) * D;
 #pragma unroll
-    for (int n = 0; n < kPfNT; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  PfRow rows[kPfNT];
-#pragma unroll
-  for (int n = 0; n < kPfNT; ++n) rows[n] = PfRow{kNegInf, 0.f, f32x4{0.f, 0.f, 0.f, 0.f}};
+      for (int j = 0; j < C::KSTEPS; ++j) {
+        u32x4 v = {0, 0, 0, 0};
+        if (ok) v = *reinterpret_cast<const u32x4*>(qp + 32 * j + 8 * c);
+        qb[n][j] = __builtin_bit_cast(bf16x8, v ^ qflip);
+      }
+    }
+    const int tok_lo = kPfWaveCols * w / a.G;
+    const int tok_hi_raw = (kPfWaveCols * w + kPfWaveCols - 1) / a.G;
+    const int tok_hi = tok_hi_raw < nt - 1 ? tok_hi_raw : nt - 1;
+    const bool wave_on = tok_lo < nt;
+    const int pos_lo = first + tok_lo;  // this wave's first and last query positions
+    const int pos_hi = first + tok_hi;
 
-  // pair j2's weights and P . V, on the masked path where some column of the
-  // wave does not see every key of the pair, or a key is past the tile
-  auto finish = [&](int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const PfMeta& m) {
-    const int key0 = 32 * j2;
-    const uint8_t* buf = lds + (j2 & 3) * C::BUF;
-    int see[kPfNT];
-    if (key0 + 31 <= pos_lo && m.live >= 32) {
-#pragma unroll
-      for (int n = 0; n < kPfNT; ++n) see[n] = 32;
-      pf_softmax_pv<KV, D, false>(s0, s1, buf, m.c0, m.c1, see, 32, acc, rows);
-    } else {
-#pragma unroll
-      for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < m.live ? vis[n] - key0 : m.live;
-      pf_softmax_pv<KV, D, true>(s0, s1, buf, m.c0, m.c1, see, m.live, acc, rows);
-    }
-  };
+    const int nkeys = first + nt > 0 ? first + nt : 0;  // keys up to the tile's last position
+    const int npairs = (nkeys + 31) / 32;
+    const int nblk = (nkeys + 15) / 16;
+    // pairs this wave computes: those with a key at or before its last position
+    const int wpairs = !wave_on || pos_hi < 0 ? 0 : (pos_hi / 32 + 1 < npairs ? pos_hi / 32 + 1 : npairs);
+    const int32_t* row = a.block_table + (int64_t)b * a.max_blocks;
 
-  // Two pairs per barrier: step j computes pairs j and j + 1 from LDS buffers
-  // j % 4 and (j + 1) % 4 while pairs j + 2 and j + 3 are loaded into two
-  // register sets and staged into the other two buffers. The loads are
-  // unconditional (past the end the last pair again, never stored), so no
-  // loaded register is merged across paths: a copy of one would wait for its
-  // load at once. (Running the two waves of a SIMD half a pair apart, so one's
-  // softmax would overlap the other's matrix work, measured slower.)
-  PfStage<KV, D> sa, sb;
-  PfIds ids;
-  ids.q = -1;
-  ids.nxt = pf_id_load(a, row, l, nblk, status);  // chunk 0, entered by the first load
-  PfMeta m0{1.f, 1.f, 0}, m1{1.f, 1.f, 0};
-  if (npairs > 0) {
-    pf_load<KV, D>(sa, a, ids, row, 0, nblk, nkeys, kvh, status);
-    pf_store<KV, D>(sa, lds, status);
-    m0 = pf_meta<KV, D>(sa, a.scale_log2);
-  }
-  if (npairs > 1) {
-    pf_load<KV, D>(sb, a, ids, row, 2, nblk, nkeys, kvh, status);
-    pf_store<KV, D>(sb, lds + C::BUF, status);
-    m1 = pf_meta<KV, D>(sb, a.scale_log2);
-  }
-  __syncthreads();
-  for (int j2 = 0; j2 < npairs; j2 += 2) {
-    // past the end the last pair is loaded again (unused): the same loads on every step
-    const int ja = j2 + 2 < npairs ? j2 + 2 : npairs - 1, jb = j2 + 3 < npairs ? j2 + 3 : npairs - 1;
-    pf_load<KV, D>(sa, a, ids, row, 2 * ja, nblk, nkeys, kvh, status);
-    pf_load<KV, D>(sb, a, ids, row, 2 * jb, nblk, nkeys, kvh, status);
-    if (j2 < wpairs) {
-      f32x4 s0[kPfNT], s1[kPfNT];
-      pf_scores<KV, D>(lds + (j2 & 3) * C::BUF, qb, s0, s1);
-      finish(j2, s0, s1, m0);
-    }
-    if (j2 + 1 < wpairs) {
-      f32x4 s0[kPfNT], s1[kPfNT];
-      pf_scores<KV, D>(lds + ((j2 + 1) & 3) * C::BUF, qb, s0, s1);
-      finish(j2 + 1, s0, s1, m1);
-    }
-    if (j2 + 2 < npairs) {
-      pf_store<KV, D>(sa, lds + ((j2 + 2) & 3) * C::BUF, status);
+    f32x4 acc[C::MT][kPfNT];
+#pragma unroll
+    for (int m = 0; m < C::MT; ++m)
+#pragma unroll
+      for (int n = 0; n < kPfNT; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    PfRow rows[kPfNT];
+#pragma unroll
+    for (int n = 0; n < kPfNT; ++n) rows[n] = PfRow{kNegInf, 0.f, f32x4{0.f, 0.f, 0.f, 0.f}};
+
+    // pair j2's weights and P . V, on the masked path where some column of the
+    // wave does not see every key of the pair, or a key is past the tile
+    auto finish = [&](int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const PfMeta& m) {
+      const int key0 = 32 * j2;
+      const uint8_t* buf = lds + (j2 & 3) * C::BUF;
+      int see[kPfNT];
+      if (key0 + 31 <= pos_lo && m.live >= 32) {
+#pragma unroll
+        for (int n = 0; n < kPfNT; ++n) see[n] = 32;
+        pf_softmax_pv<KV, D, false>(s0, s1, buf, m.c0, m.c1, see, 32, acc, rows);
+      } else {
+#pragma unroll
+        for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < m.live ? vis[n] - key0 : m.live;
+        pf_softmax_pv<KV, D, true>(s0, s1, buf, m.c0, m.c1, see, m.live, acc, rows);
+      }
+    };
+
+    // Two pairs per barrier: step j computes pairs j and j + 1 from LDS buffers
+    // j % 4 and (j + 1) % 4 while pairs j + 2 and j + 3 are loaded into two
+    // register sets and staged into the other two buffers. The loads are
+    // unconditional (past the end the last pair again, never stored), so no
+    // loaded register is merged across paths: a copy of one would wait for its
+    // load at once. (Running the two waves of a SIMD half a pair apart, so one's
+    // softmax would overlap the other's matrix work, measured slower.)
+    PfStage<KV, D> sa, sb;
+    PfIds ids;
+    ids.q = -1;
+    ids.id = 0;
+    ids.nxt = pf_id_load(row, l, nblk);  // chunk 0
+    pf_ids_advance(ids, row, 0, nblk);
+    PfMeta m0{1.f, 1.f, 0}, m1{1.f, 1.f, 0};
+    if (npairs > 0) {
+      pf_load<KV, D>(sa, a, ids, 0, nblk, nkeys, kvh, status);
+      pf_store<KV, D>(sa, lds, status);
       m0 = pf_meta<KV, D>(sa, a.scale_log2);
     }
-    if (j2 + 3 < npairs) {
-      pf_store<KV, D>(sb, lds + ((j2 + 3) & 3) * C::BUF, status);
+    if (npairs > 1) {
+      pf_load<KV, D>(sb, a, ids, 2, nblk, nkeys, kvh, status);
+      pf_store<KV, D>(sb, lds + C::BUF, status);
       m1 = pf_meta<KV, D>(sb, a.scale_log2);
     }
+    if (threadIdx.x == 0) {  // the next unit: 8 * index + queue, or -1 once every queue is drained
+      int code = -1, m = tick + first_claims;
+      if (m < qsize) code = 8 * m + q;
+      for (int s = 1; s < nq && code < 0; ++s) {
+        const int q2 = (q + s) % nq;
+        m = atomicAdd(a.hdr + kHdrPfQueue + q2, 1) + first_claims;
+        if (m < qsize) code = 8 * m + q2;
+      }
+      s_next[k & 1] = code;
+    }
     __syncthreads();
+    for (int j2 = 0; j2 < npairs; j2 += 2) {
+      // past the end the last pair is loaded again (unused): the same loads on every step
+      const int ja = j2 + 2 < npairs ? j2 + 2 : npairs - 1, jb = j2 + 3 < npairs ? j2 + 3 : npairs - 1;
+      // blocks 2ja .. 2jb + 1 lie in one chunk of 64 (2ja is a multiple of 4, or jb = ja)
+      pf_ids_advance(ids, row, ja >> 5, nblk);
+      pf_load<KV, D>(sa, a, ids, 2 * ja, nblk, nkeys, kvh, status);
+      pf_load<KV, D>(sb, a, ids, 2 * jb, nblk, nkeys, kvh, status);
+      if (j2 < wpairs) {
+        f32x4 s0[kPfNT], s1[kPfNT];
+        pf_scores<KV, D>(lds + (j2 & 3) * C::BUF, qb, s0, s1);
+        finish(j2, s0, s1, m0);
+      }
+      if (j2 + 1 < wpairs) {
+        f32x4 s0[kPfNT], s1[kPfNT];
+        pf_scores<KV, D>(lds + ((j2 + 1) & 3) * C::BUF, qb, s0, s1);
+        finish(j2 + 1, s0, s1, m1);
+      }
+      if (j2 + 2 < npairs) {
+        pf_store<KV, D>(sa, lds + ((j2 + 2) & 3) * C::BUF, status);
+        m0 = pf_meta<KV, D>(sa, a.scale_log2);
+      }
+      if (j2 + 3 < npairs) {
+        pf_store<KV, D>(sb, lds + ((j2 + 3) & 3) * C::BUF, status);
+        m1 = pf_meta<KV, D>(sb, a.scale_log2);
+      }
+      __syncthreads();
+    }
+    if (wave_on) {
+#pragma unroll
+      for (int n = 0; n < kPfNT; ++n) {
+        const float lt = rows[n].l[0];
+        if (tokq[n] < 0) continue;
+        const float inv = lt > 0.f ? 1.f / lt : 0.f;
+        if (a.out_bf16) {
+          uint16_t* o = static_cast<uint16_t*>(a.out) + (int64_t)tokq[n] * D;
+#pragma unroll
+          for (int m = 0; m < C::MT; ++m)
+            *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) =
+                u32x2{pk_bf16(acc[m][n][0] * inv, acc[m][n][1] * inv), pk_bf16(acc[m][n][2] * inv, acc[m][n][3] * inv)};
+        } else {
+          float* o = static_cast<float*>(a.out) + (int64_t)tokq[n] * D;
+#pragma unroll
+          for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m][n] * inv;
+        }
+      }
+    }
+    const int code = s_next[k & 1];
+    if (code < 0) break;
+    un = code >> 3;
+    uq = code & 7;
   }
   if (status) atomicOr(a.hdr + kHdrStatus, status);  // error paths only
-  if (!wave_on) return;
-
-#pragma unroll
-  for (int n = 0; n < kPfNT; ++n) {
-    const float lt = rows[n].l[0];
-    if (tokq[n] < 0) continue;
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    if (a.out_bf16) {
-      uint16_t* o = static_cast<uint16_t*>(a.out) + (int64_t)tokq[n] * D;
-#pragma unroll
-      for (int m = 0; m < C::MT; ++m)
-        *reinterpret_cast<u32x2*>(o + 16 * m + 4 * c) =
-            u32x2{pk_bf16(acc[m][n][0] * inv, acc[m][n][1] * inv), pk_bf16(acc[m][n][2] * inv, acc[m][n][3] * inv)};
-    } else {
-      float* o = static_cast<float*>(a.out) + (int64_t)tokq[n] * D;
-#pragma unroll
-      for (int m = 0; m < C::MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m + 4 * c) = acc[m][n] * inv;
-    }
-  }
 }
 
 template <KvType KV>
@@ -671,7 +706,22 @@ hipError_t launch_prefill(const PrefillArgs& a, KvType kv, hipStream_t s) {
                                  0, s);
   if (e != hipSuccess) return e;
   void* fn = kv == KvType::FP8 ? prefill_for_d<KvType::FP8>(a.D) : prefill_for_d<KvType::BF16>(a.D);
-  const int64_t wgs = (int64_t)a.items_max * a.Hkv;
+  // the persistent grid: resident workgroups per CU times the CUs, a multiple
+  // of 8 (the queues' start assumes it), no more than the units need
+  static std::atomic<int> per_cu_memo[4];  // per kernel, queried once
+  const int slot = (kv == KvType::FP8 ? 2 : 0) + (a.D == 128 ? 1 : 0);
+  int per_cu = per_cu_memo[slot].load(std::memory_order_relaxed);
+  if (per_cu == 0) {
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kPfThreads, 0);
+    if (e != hipSuccess) return e;
+    per_cu = per_cu > 0 ? per_cu : 1;
+    per_cu_memo[slot].store(per_cu, std::memory_order_relaxed);
+  }
+  const int64_t units = (int64_t)a.items_max * a.Hkv;
+  int64_t wgs = (int64_t)per_cu * a.cus;
+  const int64_t need = (units + 7) / 8 * 8;
+  wgs = wgs < need ? wgs : need;
+  wgs = wgs / 8 * 8 > 8 ? wgs / 8 * 8 : 8;
   return hipLaunchKernel(fn, dim3((unsigned)wgs), dim3(kPfThreads), params, 0, s);
 }
 
