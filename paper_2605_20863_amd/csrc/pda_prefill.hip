@@ -400,49 +400,68 @@ struct PfRow {
   f32x4 l;    // sum of the fp16 weights (every row of a ones . P^T product)
 };
 
-// Scores of one pair for this wave's columns: S^T[32 keys x 32 columns] =
-// K . Q^T from LDS; s0 holds keys 4c..4c+3 of the first block, s1 of the
-// second, for column r of each N-tile.
+// A pair's LDS operands in registers: K pieces (d-step j: k[j][0] rows r of
+// block 0, k[j][1] rows 16 + r of block 1) and V^T tiles (v[m]: dim rows 16m + r,
+// keys 8c .. 8c + 7 of the pair in the P^T order).
 template <KvType KV, int D>
-__device__ __forceinline__ void pf_scores(const uint8_t* buf, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
-                                          f32x4 (&s0)[kPfNT], f32x4 (&s1)[kPfNT]) {
+struct PfOps {
+  bf16x8 k[PfCfg<KV, D>::KSTEPS][2];
+  u32x4 v[PfCfg<KV, D>::MT];
+};
+
+// K piece i (d-step i / 2, block i % 2) and V tile m of the pair in buf.
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_kread(const uint8_t* buf, PfOps<KV, D>& o, int i) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
+  const int j = i >> 1, t = i & 1;
+  o.k[j][t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + (16 * t + r) * C::KROW + 64 * j + 16 * c));
+}
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_vread(const uint8_t* buf, PfOps<KV, D>& o, int m) {
+  using C = PfCfg<KV, D>;
+  const int l = lane_id();
+  const int r = l & 15, c = l >> 4;
+  o.v[m] = *reinterpret_cast<const u32x4*>(buf + C::KBUF + (16 * m + r) * C::VROW + 16 * c);
+}
+
+// S^T[32 keys x 32 columns] = K . Q^T of a pair whose K pieces are in o.k. s0
+// holds keys 4c..4c+3 of the first block, s1 of the second, for column r of
+// each N-tile.
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_scores(const PfOps<KV, D>& o, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
+                                          f32x4 (&s0)[kPfNT], f32x4 (&s1)[kPfNT]) {
+  using C = PfCfg<KV, D>;
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) s0[n] = s1[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < C::KSTEPS; ++j) {
-    const bf16x8 k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + r * C::KROW + 64 * j + 16 * c));
-    const bf16x8 k1 =
-        __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + (16 + r) * C::KROW + 64 * j + 16 * c));
 #pragma unroll
     for (int n = 0; n < kPfNT; ++n) {
-      s0[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qb[n][j], s0[n], 0, 0, 0);
-      s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qb[n][j], s1[n], 0, 0, 0);
+      s0[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(o.k[j][0], qb[n][j], s0[n], 0, 0, 0);
+      s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(o.k[j][1], qb[n][j], s1[n], 0, 0, 0);
     }
   }
 }
 
-// Softmax weights of one pair from its scores, and O^T += V^T . P^T. MASKED:
-// per-column key limits see[n] (keys of the pair the column sees) and the
-// pair's live keys (V rows at or past `live` are zeroed). c0 / c1: softmax
-// scale (log2 units) times the blocks' K scales, > 0.
+// Softmax weights of one pair from its scores. MASKED: per-column key limits
+// see[n] (keys of the pair the column sees). c0 / c1: softmax scale (log2
+// units) times the blocks' K scales, > 0.
 //
 // The weights are exp2(logit - m) with a lazily updated running max m: only
 // when a logit exceeds m by more than kSlack (so weights stay below 2^8 and fit
 // fp16) is m raised and the accumulators rescaled. Each lane first checks its
 // own 8 logits; the cross-lane max over the column's 4 lanes runs only when a
-// lane of the wave crosses the threshold.
+// lane of the wave crosses the threshold. The row sums come from a product of
+// the fp16 weights with a ones operand.
 template <KvType KV, int D, bool MASKED>
-__device__ __forceinline__ void pf_softmax_pv(const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const uint8_t* buf,
-                                              float c0, float c1, const int (&see)[kPfNT], int live,
-                                              f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], PfRow (&row)[kPfNT]) {
+__device__ __forceinline__ void pf_softmax(const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], float c0, float c1,
+                                           const int (&see)[kPfNT], f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT],
+                                           PfRow (&row)[kPfNT], f16x8 (&ph)[kPfNT]) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
-  const int r = l & 15, c = l >> 4;
-  const uint8_t* vb = buf + C::KBUF;
-  f16x8 ph[kPfNT];
+  const int c = l >> 4;
   const f16x8 ones = {1, 1, 1, 1, 1, 1, 1, 1};
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) {
@@ -482,6 +501,26 @@ __device__ __forceinline__ void pf_softmax_pv(const f32x4 (&s0)[kPfNT], const f3
     ph[n] = __builtin_bit_cast(f16x8, w);
     row[n].l = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, ph[n], row[n].l, 0, 0, 0);
   }
+}
+
+// O^T += V^T . P^T, the V tiles read from vbuf. MASKED: V rows at or past
+// `live` keys are zeroed (bitwise, so NaN poison in unused slots never reaches
+// the product). KNEXT: the next pair's K pieces are read from kbuf between the
+// MFMAs, so the LDS serves them while the matrix core works (a wave issues in
+// order: reads placed after the MFMAs would start only when the last one
+// issues). Reading V tiles between the score MFMAs as well would keep them
+// live through the softmax, which needs 32 more registers than two waves per
+// SIMD have.
+template <KvType KV, int D, bool MASKED, bool KNEXT>
+__device__ __forceinline__ void pf_pv(PfOps<KV, D>& o, const f16x8 (&ph)[kPfNT], int live,
+                                      f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], const uint8_t* vbuf,
+                                      const uint8_t* kbuf) {
+  using C = PfCfg<KV, D>;
+  static_assert(C::MT == 2 * C::KSTEPS, "one K piece per V tile");
+#pragma unroll
+  for (int m = 0; m < C::MT; ++m) pf_vread<KV, D>(vbuf, o, m);
+  const int l = lane_id();
+  const int c = l >> 4;
   uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
   if constexpr (MASKED) {
 #pragma unroll
@@ -492,11 +531,16 @@ __device__ __forceinline__ void pf_softmax_pv(const f32x4 (&s0)[kPfNT], const f3
   }
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
-    u32x4 w = *reinterpret_cast<const u32x4*>(vb + (16 * m + r) * C::VROW + 16 * c);
+    u32x4 w = o.v[m];
     if constexpr (MASKED) w = u32x4{w.x & mk[0], w.y & mk[1], w.z & mk[2], w.w & mk[3]};
     const f16x8 va = __builtin_bit_cast(f16x8, w);
 #pragma unroll
     for (int n = 0; n < kPfNT; ++n) acc[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, ph[n], acc[m][n], 0, 0, 0);
+    if constexpr (KNEXT) {
+      __builtin_amdgcn_sched_barrier(0);
+      pf_kread<KV, D>(kbuf, o, m);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 }
 
@@ -584,20 +628,26 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int n = 0; n < kPfNT; ++n) rows[n] = PfRow{kNegInf, 0.f, f32x4{0.f, 0.f, 0.f, 0.f}};
 
-    // pair j2's weights and P . V, on the masked path where some column of the
-    // wave does not see every key of the pair, or a key is past the tile
-    auto finish = [&](int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const PfMeta& m) {
+    // pair j2's weights and P . V from its scores and V tiles, on the masked
+    // path where some column of the wave does not see every key of the pair, or
+    // a key is past the tile; KNEXT: the next pair's K pieces are read from kbuf
+    // during the P . V
+    auto finish = [&](auto knext, int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const PfMeta& m,
+                      PfOps<KV, D>& o, const uint8_t* vbuf, const uint8_t* kbuf) {
+      constexpr bool KNEXT = decltype(knext)::value;
       const int key0 = 32 * j2;
-      const uint8_t* buf = lds + (j2 & 3) * C::BUF;
       int see[kPfNT];
+      f16x8 ph[kPfNT];
       if (key0 + 31 <= pos_lo && m.live >= 32) {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = 32;
-        pf_softmax_pv<KV, D, false>(s0, s1, buf, m.c0, m.c1, see, 32, acc, rows);
+        pf_softmax<KV, D, false>(s0, s1, m.c0, m.c1, see, acc, rows, ph);
+        pf_pv<KV, D, false, KNEXT>(o, ph, 32, acc, vbuf, kbuf);
       } else {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < m.live ? vis[n] - key0 : m.live;
-        pf_softmax_pv<KV, D, true>(s0, s1, buf, m.c0, m.c1, see, m.live, acc, rows);
+        pf_softmax<KV, D, true>(s0, s1, m.c0, m.c1, see, acc, rows, ph);
+        pf_pv<KV, D, true, KNEXT>(o, ph, m.live, acc, vbuf, kbuf);
       }
     };
 
@@ -644,14 +694,20 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       pf_load<KV, D>(sa, a, ids, 2 * ja, nblk, nkeys, kvh, status);
       pf_load<KV, D>(sb, a, ids, 2 * jb, nblk, nkeys, kvh, status);
       if (j2 < wpairs) {
+        // pair j2 + 1's K pieces are read during pair j2's P . V (even when
+        // this wave skips pair j2 + 1: the buffer is in bounds)
+        const uint8_t* ba = lds + (j2 & 3) * C::BUF;
+        const uint8_t* bb = lds + ((j2 + 1) & 3) * C::BUF;
+        PfOps<KV, D> o;
+#pragma unroll
+        for (int i = 0; i < C::MT; ++i) pf_kread<KV, D>(ba, o, i);
         f32x4 s0[kPfNT], s1[kPfNT];
-        pf_scores<KV, D>(lds + (j2 & 3) * C::BUF, qb, s0, s1);
-        finish(j2, s0, s1, m0);
-      }
-      if (j2 + 1 < wpairs) {
-        f32x4 s0[kPfNT], s1[kPfNT];
-        pf_scores<KV, D>(lds + ((j2 + 1) & 3) * C::BUF, qb, s0, s1);
-        finish(j2 + 1, s0, s1, m1);
+        pf_scores<KV, D>(o, qb, s0, s1);
+        finish(std::true_type{}, j2, s0, s1, m0, o, ba, bb);
+        if (j2 + 1 < wpairs) {
+          pf_scores<KV, D>(o, qb, s0, s1);
+          finish(std::false_type{}, j2 + 1, s0, s1, m1, o, bb, bb);
+        }
       }
       if (j2 + 2 < npairs) {
         pf_store<KV, D>(sa, lds + ((j2 + 2) & 3) * C::BUF, status);
