@@ -153,6 +153,32 @@ def test_graph_prefill(lib):
     assert lib.read_device_status() == 0
 
 
+def test_graph_prefill_more_units_than_workgroups(lib):
+    """Enough tiles that the persistent grid claims most units from its queue
+    counters: the plan kernel must reset them on every replay (a stale counter
+    would skip units, which the oracle check of the first replay, made after an
+    eager call on the same stream, would show)."""
+    w = W.WORKLOADS["logprob_gqa7b_bf16"].replace(name="graph_logprob_many", num_seqs=24,
+                                                  lengths=("lognormal", 600, 0.5, 64, 1500))
+    pin = W.generate_prefill(w, DEV)
+    c = pin.cache
+    units = sum((int(n) + 35) // 36 for n in pin.counts) * w.num_kv_heads
+    assert units > 4 * torch.cuda.get_device_properties(DEV).multi_processor_count, units
+    out_g = torch.empty(pin.q.shape, dtype=torch.bfloat16, device=DEV)
+    out_e = torch.empty_like(out_g)
+
+    def call(out):
+        lib.paged_prefill_attention(pin.q, pin.q_offsets, c.k_cache, c.v_cache, c.block_table, c.seq_lens, None,
+                                    out, c.softmax_scale, max_seq_len=c.layout.max_seq_len)
+
+    def check(out):
+        ref = U.oracle_prefill_whole(pin, "graph prefill, many units")
+        U.assert_close(U.out_to_f64(out), ref, "bf16", "graph prefill, many units", bf16_out_rounding=True)
+
+    replay_and_compare(call, out_g, out_e, lambda r: pin.q.copy_(fresh_q(pin.q, 500 + r)), check)
+    assert lib.read_device_status() == 0
+
+
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
 def test_graph_append_decode_loop(lib, kv):
     """A serving loop as one graph: append each sequence's new key and value
