@@ -665,15 +665,15 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     ids.nxt = pf_id_load(row, l, nblk);  // chunk 0
     pf_ids_advance(ids, row, 0, nblk);
     PfMeta m0{1.f, 1.f, 0}, m1{1.f, 1.f, 0};
-    if (npairs > 0) {
+    if (npairs > 0) {  // both pairs' loads before either store: one round trip
       pf_load<KV, D>(sa, a, ids, 0, nblk, nkeys, kvh, status);
+      pf_load<KV, D>(sb, a, ids, npairs > 1 ? 2 : 0, nblk, nkeys, kvh, status);
       pf_store<KV, D>(sa, lds, status);
       m0 = pf_meta<KV, D>(sa, a.scale_log2);
-    }
-    if (npairs > 1) {
-      pf_load<KV, D>(sb, a, ids, 2, nblk, nkeys, kvh, status);
-      pf_store<KV, D>(sb, lds + C::BUF, status);
-      m1 = pf_meta<KV, D>(sb, a.scale_log2);
+      if (npairs > 1) {
+        pf_store<KV, D>(sb, lds + C::BUF, status);
+        m1 = pf_meta<KV, D>(sb, a.scale_log2);
+      }
     }
     if (threadIdx.x == 0) {  // the next unit: 8 * index + queue, or -1 once every queue is drained
       int code = -1, m = tick + first_claims;
