@@ -30,15 +30,17 @@
 //   (32 keys, a pair) at a time, two pairs per barrier. The workgroup loads the
 //   next two pairs' K and V tiles while it computes the current two, decodes
 //   them (fp8 codes to bf16 K; V to fp16, fp8 as code times the block's V
-//   scale) and writes them to the other two of four LDS buffers. K rows are padded so 16 rows hit distinct banks; V rows are
-//   stored with the two blocks' tokens interleaved in the order the P^T
-//   operand holds them, so each lane reads its 8 keys at once.
+//   scale) and writes them to the other two of four LDS buffers. K rows are
+//   padded so 16 rows hit distinct banks; V rows are stored with the two
+//   blocks' tokens interleaved in the order the P^T operand holds them, so each
+//   lane reads its 8 keys at once.
 // * Per wave and pair: S^T[32 keys x 32 columns] = K . Q^T on
 //   v_mfma_f32_16x16x32_bf16, online softmax on the accumulators (lazy
 //   rescale), weights packed to fp16 and O^T += V^T . P^T on
 //   v_mfma_f32_16x16x32_f16; the row sums come from a product with a ones
 //   operand, so they add exactly the fp16 weights the product uses. The K scale
-//   of an fp8 block goes on its logits.
+//   of an fp8 block goes on its logits. The second pair of a step has its K
+//   operands read from LDS between the first pair's P . V MFMAs.
 // * Causal masking selects per column (a key is seen iff it is at or before the
 //   column's position); V rows of keys past the tile's last position are zeroed,
 //   so NaN poison in unused slots never reaches the products. Only pairs that
