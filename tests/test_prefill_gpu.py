@@ -77,6 +77,31 @@ def test_prefill_matches_oracle(lib, kv, d, hq, hkv):
     check(lib, pin, f"{kv} D{d} G{hq // hkv}")
 
 
+# (Hq, Hkv, D): the attention grid's unit queues, gcd(Hkv, 8) of them, each
+# holding Hkv / gcd(Hkv, 8) KV heads: 8 queues of one head, 8 of two, 2 of
+# three, one of five. The lengths give more units than the grid has
+# workgroups, so most units are claimed from the counters, and queues drain
+# at different times, so workgroups take units from other queues.
+QUEUE_SHAPES = [(16, 8, 64), (16, 16, 64), (18, 6, 128), (15, 5, 64)]
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+@pytest.mark.parametrize("hq,hkv,d", QUEUE_SHAPES)
+def test_prefill_queues_more_units_than_workgroups(lib, kv, hq, hkv, d):
+    lens = [1300, 41, 2100, 700, 1650, 5, 999]
+    counts = [1300, 41, 1500, 700, 1650, 5, 640]
+    pin = W.generate_prefill(wl(hq, hkv, d, kv), DEV, seq_lens=lens, q_counts=counts)
+    tq = 256 // (hq // hkv)
+    units = sum((n + tq - 1) // tq for n in counts) * hkv
+    cus = torch.cuda.get_device_properties(DEV).multi_processor_count
+    print(f"[prefill queues] kv={kv} Hq={hq} Hkv={hkv} D={d} units={units} CUs={cus}", flush=True)
+    assert units > cus, (units, cus)
+    out = run(lib, pin, torch.float32)
+    ref = U.oracle_prefill_whole(pin, f"queues Hq{hq} Hkv{hkv}")
+    U.assert_close(U.out_to_f64(out), ref, kv, f"queues Hq{hq} Hkv{hkv} {kv}")
+    assert lib.read_device_status() == 0
+
+
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
 def test_prefill_bf16_output(lib, kv):
     pin = W.generate_prefill(wl(28, 4, 128, kv), DEV, seq_lens=[40, 300, 129], q_counts=[40, 300, 2])
