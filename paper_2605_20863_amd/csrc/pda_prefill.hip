@@ -40,7 +40,8 @@
 //   v_mfma_f32_16x16x32_f16; the row sums come from a product with a ones
 //   operand, so they add exactly the fp16 weights the product uses. The K scale
 //   of an fp8 block goes on its logits. The second pair of a step has its K
-//   operands read from LDS between the first pair's P . V MFMAs.
+//   operands read from LDS between the first pair's P . V MFMAs and its V
+//   operands between its own score MFMAs.
 // * Causal masking selects per column (a key is seen iff it is at or before the
 //   column's position); V rows of keys past the tile's last position are zeroed,
 //   so NaN poison in unused slots never reaches the products. Only pairs that
@@ -402,13 +403,14 @@ struct PfRow {
   f32x4 l;    // sum of the fp16 weights (every row of a ones . P^T product)
 };
 
-// A pair's LDS operands in registers: K pieces (d-step j: k[j][0] rows r of
-// block 0, k[j][1] rows 16 + r of block 1) and V^T tiles (v[m]: dim rows 16m + r,
-// keys 8c .. 8c + 7 of the pair in the P^T order).
+// A pair's LDS operands in registers, one slot per K piece or V tile: slot i
+// holds K piece i (d-step i / 2; rows r of block 0 for even i, rows 16 + r of
+// block 1 for odd i), then V^T tile i (dim rows 16i + r, keys 8c .. 8c + 7 of
+// the pair in the P^T order). A pair's tiles replace its pieces, and the next
+// pair's pieces replace the tiles.
 template <KvType KV, int D>
 struct PfOps {
-  bf16x8 k[PfCfg<KV, D>::KSTEPS][2];
-  u32x4 v[PfCfg<KV, D>::MT];
+  u32x4 x[PfCfg<KV, D>::MT];
 };
 
 // K piece i (d-step i / 2, block i % 2) and V tile m of the pair in buf.
@@ -418,31 +420,41 @@ __device__ __forceinline__ void pf_kread(const uint8_t* buf, PfOps<KV, D>& o, in
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
   const int j = i >> 1, t = i & 1;
-  o.k[j][t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + (16 * t + r) * C::KROW + 64 * j + 16 * c));
+  o.x[i] = *reinterpret_cast<const u32x4*>(buf + (16 * t + r) * C::KROW + 64 * j + 16 * c);
 }
 template <KvType KV, int D>
 __device__ __forceinline__ void pf_vread(const uint8_t* buf, PfOps<KV, D>& o, int m) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
-  o.v[m] = *reinterpret_cast<const u32x4*>(buf + C::KBUF + (16 * m + r) * C::VROW + 16 * c);
+  o.x[m] = *reinterpret_cast<const u32x4*>(buf + C::KBUF + (16 * m + r) * C::VROW + 16 * c);
 }
 
-// S^T[32 keys x 32 columns] = K . Q^T of a pair whose K pieces are in o.k. s0
+// S^T[32 keys x 32 columns] = K . Q^T of a pair whose K pieces are in o. s0
 // holds keys 4c..4c+3 of the first block, s1 of the second, for column r of
-// each N-tile.
-template <KvType KV, int D>
-__device__ __forceinline__ void pf_scores(const PfOps<KV, D>& o, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
-                                          f32x4 (&s0)[kPfNT], f32x4 (&s1)[kPfNT]) {
+// each N-tile. VNEXT: the pair's V tiles are read from vbuf between the MFMAs,
+// each into the slots of the d-step just used, so the LDS serves them while
+// the matrix core works (a wave issues in order: reads placed after the MFMAs
+// would start only when the last one issues).
+template <KvType KV, int D, bool VNEXT>
+__device__ __forceinline__ void pf_scores(PfOps<KV, D>& o, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
+                                          f32x4 (&s0)[kPfNT], f32x4 (&s1)[kPfNT], const uint8_t* vbuf) {
   using C = PfCfg<KV, D>;
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) s0[n] = s1[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < C::KSTEPS; ++j) {
+    const bf16x8 k0 = __builtin_bit_cast(bf16x8, o.x[2 * j]), k1 = __builtin_bit_cast(bf16x8, o.x[2 * j + 1]);
 #pragma unroll
     for (int n = 0; n < kPfNT; ++n) {
-      s0[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(o.k[j][0], qb[n][j], s0[n], 0, 0, 0);
-      s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(o.k[j][1], qb[n][j], s1[n], 0, 0, 0);
+      s0[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qb[n][j], s0[n], 0, 0, 0);
+      s1[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qb[n][j], s1[n], 0, 0, 0);
+    }
+    if constexpr (VNEXT) {
+      __builtin_amdgcn_sched_barrier(0);
+      pf_vread<KV, D>(vbuf, o, 2 * j);
+      pf_vread<KV, D>(vbuf, o, 2 * j + 1);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 }
@@ -505,22 +517,21 @@ __device__ __forceinline__ void pf_softmax(const f32x4 (&s0)[kPfNT], const f32x4
   }
 }
 
-// O^T += V^T . P^T, the V tiles read from vbuf. MASKED: V rows at or past
-// `live` keys are zeroed (bitwise, so NaN poison in unused slots never reaches
-// the product). KNEXT: the next pair's K pieces are read from kbuf between the
-// MFMAs, so the LDS serves them while the matrix core works (a wave issues in
-// order: reads placed after the MFMAs would start only when the last one
-// issues). Reading V tiles between the score MFMAs as well would keep them
-// live through the softmax, which needs 32 more registers than two waves per
-// SIMD have.
-template <KvType KV, int D, bool MASKED, bool KNEXT>
+// O^T += V^T . P^T with the V tiles read from vbuf first (VREAD) or already in
+// o. MASKED: V rows at or past `live` keys are zeroed (bitwise, so NaN poison
+// in unused slots never reaches the product). KNEXT: the next pair's K pieces
+// are read from kbuf between the MFMAs, each into the slot of the tile just
+// used.
+template <KvType KV, int D, bool MASKED, bool KNEXT, bool VREAD>
 __device__ __forceinline__ void pf_pv(PfOps<KV, D>& o, const f16x8 (&ph)[kPfNT], int live,
                                       f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], const uint8_t* vbuf,
                                       const uint8_t* kbuf) {
   using C = PfCfg<KV, D>;
   static_assert(C::MT == 2 * C::KSTEPS, "one K piece per V tile");
+  if constexpr (VREAD) {
 #pragma unroll
-  for (int m = 0; m < C::MT; ++m) pf_vread<KV, D>(vbuf, o, m);
+    for (int m = 0; m < C::MT; ++m) pf_vread<KV, D>(vbuf, o, m);
+  }
   const int l = lane_id();
   const int c = l >> 4;
   uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
@@ -533,7 +544,7 @@ __device__ __forceinline__ void pf_pv(PfOps<KV, D>& o, const f16x8 (&ph)[kPfNT],
   }
 #pragma unroll
   for (int m = 0; m < C::MT; ++m) {
-    u32x4 w = o.v[m];
+    u32x4 w = o.x[m];
     if constexpr (MASKED) w = u32x4{w.x & mk[0], w.y & mk[1], w.z & mk[2], w.w & mk[3]};
     const f16x8 va = __builtin_bit_cast(f16x8, w);
 #pragma unroll
@@ -644,18 +655,19 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = 32;
         pf_softmax<KV, D, false>(s0, s1, m.c0, m.c1, see, acc, rows, ph);
-        pf_pv<KV, D, false, KNEXT>(o, ph, 32, acc, vbuf, kbuf);
+        pf_pv<KV, D, false, KNEXT, KNEXT>(o, ph, 32, acc, vbuf, kbuf);
       } else {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < m.live ? vis[n] - key0 : m.live;
         pf_softmax<KV, D, true>(s0, s1, m.c0, m.c1, see, acc, rows, ph);
-        pf_pv<KV, D, true, KNEXT>(o, ph, m.live, acc, vbuf, kbuf);
+        pf_pv<KV, D, true, KNEXT, KNEXT>(o, ph, m.live, acc, vbuf, kbuf);
       }
     };
 
     // Two pairs per barrier: step j computes pairs j and j + 1 from LDS buffers
     // j % 4 and (j + 1) % 4 while pairs j + 2 and j + 3 are loaded into two
-    // register sets and staged into the other two buffers. The loads are
+    // register sets and staged (between pairs j and j + 1) into the other two
+    // buffers. The loads are
     // unconditional (past the end the last pair again, never stored), so no
     // loaded register is merged across paths: a copy of one would wait for its
     // load at once. (Running the two waves of a SIMD half a pair apart, so one's
@@ -695,22 +707,23 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       pf_ids_advance(ids, row, ja >> 5, nblk);
       pf_load<KV, D>(sa, a, ids, 2 * ja, nblk, nkeys, kvh, status);
       pf_load<KV, D>(sb, a, ids, 2 * jb, nblk, nkeys, kvh, status);
+      PfOps<KV, D> o;
       if (j2 < wpairs) {
         // pair j2 + 1's K pieces are read during pair j2's P . V (even when
         // this wave skips pair j2 + 1: the buffer is in bounds)
         const uint8_t* ba = lds + (j2 & 3) * C::BUF;
         const uint8_t* bb = lds + ((j2 + 1) & 3) * C::BUF;
-        PfOps<KV, D> o;
 #pragma unroll
         for (int i = 0; i < C::MT; ++i) pf_kread<KV, D>(ba, o, i);
         f32x4 s0[kPfNT], s1[kPfNT];
-        pf_scores<KV, D>(o, qb, s0, s1);
+        pf_scores<KV, D, false>(o, qb, s0, s1, ba);
         finish(std::true_type{}, j2, s0, s1, m0, o, ba, bb);
-        if (j2 + 1 < wpairs) {
-          pf_scores<KV, D>(o, qb, s0, s1);
-          finish(std::false_type{}, j2 + 1, s0, s1, m1, o, bb, bb);
-        }
       }
+      // the next pairs are staged between this step's two: with their registers
+      // free, pair j2 + 1's V tiles fit beside its softmax and are read during
+      // its score MFMAs (pair j2's V tiles are read after its softmax, whose
+      // registers the staged loads still hold)
+      const PfMeta m1cur = m1;
       if (j2 + 2 < npairs) {
         pf_store<KV, D>(sa, lds + ((j2 + 2) & 3) * C::BUF, status);
         m0 = pf_meta<KV, D>(sa, a.scale_log2);
@@ -718,6 +731,12 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       if (j2 + 3 < npairs) {
         pf_store<KV, D>(sb, lds + ((j2 + 3) & 3) * C::BUF, status);
         m1 = pf_meta<KV, D>(sb, a.scale_log2);
+      }
+      if (j2 + 1 < wpairs) {
+        const uint8_t* bb = lds + ((j2 + 1) & 3) * C::BUF;
+        f32x4 s0[kPfNT], s1[kPfNT];
+        pf_scores<KV, D, true>(o, qb, s0, s1, bb);
+        finish(std::false_type{}, j2 + 1, s0, s1, m1cur, o, bb, bb);
       }
       __syncthreads();
     }
