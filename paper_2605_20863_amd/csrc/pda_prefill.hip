@@ -39,9 +39,10 @@
 //   rescale), weights packed to fp16 and O^T += V^T . P^T on
 //   v_mfma_f32_16x16x32_f16; the row sums come from a product with a ones
 //   operand, so they add exactly the fp16 weights the product uses. The K scale
-//   of an fp8 block goes on its logits. The second pair of a step has its K
-//   operands read from LDS between the first pair's P . V MFMAs and its V
-//   operands between its own score MFMAs.
+//   of an fp8 block goes on its logits. LDS operand reads sit beside matrix
+//   work: the second pair of a step has its K operands read between the first
+//   pair's P . V MFMAs and its V operands between its own score MFMAs; half of
+//   the first pair's V operands are read during its softmax.
 // * Causal masking selects per column (a key is seen iff it is at or before the
 //   column's position); V rows of keys past the tile's last position are zeroed,
 //   so NaN poison in unused slots never reaches the products. Only pairs that
@@ -468,11 +469,14 @@ __device__ __forceinline__ void pf_scores(PfOps<KV, D>& o, const bf16x8 (&qb)[kP
 // fp16) is m raised and the accumulators rescaled. Each lane first checks its
 // own 8 logits; the cross-lane max over the column's 4 lanes runs only when a
 // lane of the wave crosses the threshold. The row sums come from a product of
-// the fp16 weights with a ones operand.
-template <KvType KV, int D, bool MASKED>
+// the fp16 weights with a ones operand. VMID: the first half of the pair's V
+// tiles are read from vbuf once N-tile 0 is done, into registers its scores
+// held, so those reads overlap N-tile 1's softmax.
+template <KvType KV, int D, bool MASKED, bool VMID>
 __device__ __forceinline__ void pf_softmax(const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], float c0, float c1,
                                            const int (&see)[kPfNT], f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT],
-                                           PfRow (&row)[kPfNT], f16x8 (&ph)[kPfNT]) {
+                                           PfRow (&row)[kPfNT], f16x8 (&ph)[kPfNT], PfOps<KV, D>& o,
+                                           const uint8_t* vbuf) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int c = l >> 4;
@@ -514,24 +518,30 @@ __device__ __forceinline__ void pf_softmax(const f32x4 (&s0)[kPfNT], const f32x4
     for (int i = 0; i < 4; ++i) w[i] = pk_f16(p[2 * i], p[2 * i + 1]);
     ph[n] = __builtin_bit_cast(f16x8, w);
     row[n].l = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones, ph[n], row[n].l, 0, 0, 0);
+    if constexpr (VMID) {
+      if (n == 0) {  // the first half of the V tiles, in the registers N-tile 0's scores held
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int m = 0; m < C::MT / 2; ++m) pf_vread<KV, D>(vbuf, o, m);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
   }
 }
 
-// O^T += V^T . P^T with the V tiles read from vbuf first (VREAD) or already in
-// o. MASKED: V rows at or past `live` keys are zeroed (bitwise, so NaN poison
+// O^T += V^T . P^T, V tiles VFROM .. MT - 1 read from vbuf first (the others
+// are in o already). MASKED: V rows at or past `live` keys are zeroed (bitwise, so NaN poison
 // in unused slots never reaches the product). KNEXT: the next pair's K pieces
 // are read from kbuf between the MFMAs, each into the slot of the tile just
 // used.
-template <KvType KV, int D, bool MASKED, bool KNEXT, bool VREAD>
+template <KvType KV, int D, bool MASKED, bool KNEXT, int VFROM>
 __device__ __forceinline__ void pf_pv(PfOps<KV, D>& o, const f16x8 (&ph)[kPfNT], int live,
                                       f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], const uint8_t* vbuf,
                                       const uint8_t* kbuf) {
   using C = PfCfg<KV, D>;
   static_assert(C::MT == 2 * C::KSTEPS, "one K piece per V tile");
-  if constexpr (VREAD) {
 #pragma unroll
-    for (int m = 0; m < C::MT; ++m) pf_vread<KV, D>(vbuf, o, m);
-  }
+  for (int m = VFROM; m < C::MT; ++m) pf_vread<KV, D>(vbuf, o, m);
   const int l = lane_id();
   const int c = l >> 4;
   uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
@@ -654,13 +664,13 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       if (key0 + 31 <= pos_lo && m.live >= 32) {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = 32;
-        pf_softmax<KV, D, false>(s0, s1, m.c0, m.c1, see, acc, rows, ph);
-        pf_pv<KV, D, false, KNEXT, KNEXT>(o, ph, 32, acc, vbuf, kbuf);
+        pf_softmax<KV, D, false, KNEXT>(s0, s1, m.c0, m.c1, see, acc, rows, ph, o, vbuf);
+        pf_pv<KV, D, false, KNEXT, KNEXT ? C::MT / 2 : C::MT>(o, ph, 32, acc, vbuf, kbuf);
       } else {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < m.live ? vis[n] - key0 : m.live;
-        pf_softmax<KV, D, true>(s0, s1, m.c0, m.c1, see, acc, rows, ph);
-        pf_pv<KV, D, true, KNEXT, KNEXT>(o, ph, m.live, acc, vbuf, kbuf);
+        pf_softmax<KV, D, true, KNEXT>(s0, s1, m.c0, m.c1, see, acc, rows, ph, o, vbuf);
+        pf_pv<KV, D, true, KNEXT, KNEXT ? C::MT / 2 : C::MT>(o, ph, m.live, acc, vbuf, kbuf);
       }
     };
 
