@@ -620,7 +620,10 @@ int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, co
   const int TQ = pda::kPfColumns / G;
   // every sequence's tiles: sum of ceil(n_b / TQ) <= (T + B (TQ - 1)) / TQ
   const int64_t items_max = ((int64_t)pr->num_tokens + (int64_t)pr->num_seqs * (TQ - 1)) / TQ;
-  if (items_max * pr->num_kv_heads > INT32_MAX) return fail(PDA_EINVAL, "too many work items for one grid");
+  // the attention grid names a claimed unit (item, KV head) as 8 * index + queue in an int32
+  if (items_max * pr->num_kv_heads > INT32_MAX / 8)
+    return fail(PDA_EINVAL, "too many work units (%lld tiles x %d KV heads) for the unit queues", (long long)items_max,
+                pr->num_kv_heads);
   if (pr->num_seqs == 0 || pr->num_tokens == 0) return PDA_OK;
   if (!q || !q_offsets || !k_cache || !v_cache || !block_table || !seq_lens || !out)
     return fail(PDA_EINVAL, "a required pointer (q, q_offsets, k_cache, v_cache, block_table, seq_lens, out) is NULL");

@@ -349,6 +349,9 @@ def test_prefill_argument_checks():
     assert call(pprob(out_dtype=L.FP8_E4M3)) == L.EINVAL
     assert call(pprob(), scale=math.inf) == L.EINVAL
     assert call(pprob(num_tokens=2 ** 30, num_q_heads=8)) == L.EINVAL   # T * Hq overflows int32
+    # ~17M one-token tiles x 16 KV heads: more units than 8 * unit + queue can name in an int32
+    assert call(pprob(num_seqs=17_000_000, num_tokens=1, num_q_heads=16, num_kv_heads=16)) == L.EINVAL
+    assert "work units" in L.last_error()
     for i in range(8):
         ptrs = list(ok_ptrs)
         ptrs[i] = None
