@@ -378,9 +378,10 @@ typedef struct pda_prefill_problem {
  *
  * Errors: all checks run on the host before any HIP call: PDA_EINVAL for bad
  * sizes, dtypes, NULL pointers or misaligned ones (q, the caches and out need
- * 16 bytes, the int32 and f32 arrays 4); PDA_EUNSUPPORTED for head_dim not in
- * {64, 128}, block_size != 16, G > 16, or an f32 cache. Uses the stream's
- * workspace (16 bytes per work item of 256 / G query tokens).
+ * 16 bytes, the int32 and f32 arrays 4), or more than INT32_MAX / 8 work units
+ * (tiles of 256 / G query tokens times KV heads); PDA_EUNSUPPORTED for
+ * head_dim not in {64, 128}, block_size != 16, G > 16, or an f32 cache. Uses
+ * the stream's workspace (16 bytes per work item of 256 / G query tokens).
  */
 int pda_paged_prefill_attention(const void* q,
                                 const int32_t* q_offsets,
