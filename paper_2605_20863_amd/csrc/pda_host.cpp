@@ -11,6 +11,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <initializer_list>
 #include <map>
@@ -574,6 +575,17 @@ int append_run(const void* k_new, const void* v_new, void* k_cache, void* v_cach
   return PDA_OK;
 }
 
+// Largest prefill image in bytes: PDA_PREFILL_IMAGE_MAX_MB (MiB, read on each
+// call; 0 always stages through registers), 8 GiB by default.
+int64_t prefill_image_cap() {
+  const char* v = std::getenv("PDA_PREFILL_IMAGE_MAX_MB");
+  if (!v || !*v) return 8ll << 30;
+  char* end = nullptr;
+  const long long mb = std::strtoll(v, &end, 10);
+  if (end == v || mb < 0) return 8ll << 30;
+  return mb > (INT64_MAX >> 20) ? INT64_MAX : (int64_t)mb << 20;
+}
+
 int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, const void* v_cache,
                 const int32_t* block_table, const int32_t* seq_lens, const float* kv_scales, void* out,
                 float softmax_scale, const pda_prefill_problem* pr, hipStream_t stream) {
@@ -645,7 +657,25 @@ int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, co
   Workspace* ws = workspace_for(dev, stream);
   std::lock_guard<std::mutex> lk(ws->mu);
   const int64_t items_off = align_up(pda::kHdrWords * 4);
-  if ((rc = ensure_workspace(ws, items_off + items_max * 16, stream)) != PDA_OK) return rc;
+  const int64_t plain_bytes = items_off + items_max * 16;
+  // The image (V in fp16; for an fp8 cache K in bf16 too) follows the work
+  // list when it fits the cap; a capture that cannot grow the workspace, or a
+  // failed allocation, takes the staging kernel, whose results are the same.
+  const int64_t img_half = pr->num_blocks * pr->num_kv_heads * (int64_t)pda::kBlockSize * pr->head_dim * 2;
+  const int64_t img_bytes = kd == PDA_DTYPE_FP8_E4M3 ? 2 * img_half : img_half;
+  const int64_t img_off = align_up(plain_bytes);
+  bool use_img = img_bytes <= prefill_image_cap();
+  if (use_img && capturing(stream) && ws->bytes < img_off + img_bytes) use_img = false;
+  if (use_img) {
+    rc = ensure_workspace(ws, img_off + img_bytes, stream);
+    if (rc == PDA_ENOMEM) {
+      use_img = false;
+      g_error.clear();
+    } else if (rc != PDA_OK) {
+      return rc;
+    }
+  }
+  if (!use_img && (rc = ensure_workspace(ws, plain_bytes, stream)) != PDA_OK) return rc;
   char* base = static_cast<char*>(ws->ptr);
 
   pda::PrefillArgs a;
@@ -678,6 +708,8 @@ int prefill_run(const void* q, const int32_t* q_offsets, const void* k_cache, co
   a.nq = std::gcd(a.Hkv, 8);
   a.hdr = reinterpret_cast<int32_t*>(base);
   a.items = reinterpret_cast<int4*>(base + items_off);
+  a.v_img = use_img ? base + img_off : nullptr;
+  a.k_img = use_img && kd == PDA_DTYPE_FP8_E4M3 ? base + img_off + img_half : nullptr;
   const pda::KvType kv = kd == PDA_DTYPE_BF16 ? pda::KvType::BF16 : pda::KvType::FP8;
   if ((e = pda::launch_prefill(a, kv, stream)) != hipSuccess) return fail_hip(e, "prefill kernel launch");
   return PDA_OK;

@@ -139,6 +139,12 @@ struct PrefillArgs {
   int32_t nq;           // unit queues: gcd(Hkv, 8)
   int32_t* hdr;         // workspace header (status, item count, queue counters)
   int4* items;          // [items_max] {sequence, first q row, tokens, first position}
+  // Image of the cache's tiles in the products' operand types, indexed like the
+  // cache (block * Hkv + KV head, 16 * D two-byte elements per tile): V in fp16
+  // (v_img), and for an fp8 cache K in bf16 (k_img). v_img null: the attention
+  // kernel stages the tiles through registers instead.
+  void* k_img;
+  void* v_img;
 };
 
 hipError_t launch_prefill(const PrefillArgs& a, KvType kv, hipStream_t s);

@@ -10,10 +10,13 @@
 // of a tile, so K and V go through LDS once per workgroup and the products run
 // on the matrix cores.
 //
-// * Plan kernel (one workgroup): per sequence, its tiles of 256 / G query
+// * Prep kernel. Workgroup 0 plans: per sequence, its tiles of 256 / G query
 //   tokens; sequences sorted by length, longest first (counting sort on the
 //   length), and a work list of (sequence, tile) items, each sequence's last
-//   (heaviest) tile first.
+//   (heaviest) tile first. The other workgroups (image path) write the image:
+//   every tile of a block that a sequence with queries reads, converted to the
+//   operand types of the products (V to fp16, fp8 as code times the block's V
+//   scale; for fp8 caches K codes to bf16), indexed like the cache.
 // * Attention kernel: a persistent grid, one workgroup (8 waves, 2 per SIMD)
 //   per CU, that takes (item, KV head) units from queues, so a CU goes from one
 //   unit to the next without a workgroup launch between them (which cost ~4 us
@@ -27,13 +30,16 @@
 //   A unit's query columns are (token, head) pairs, 256 / G tokens times the G
 //   query heads of the KV head; each wave owns 32 columns (2 MFMA N-tiles).
 // * The KV prefix up to the tile's last position is walked two 16-token blocks
-//   (32 keys, a pair) at a time, two pairs per barrier. The workgroup loads the
-//   next two pairs' K and V tiles while it computes the current two, decodes
-//   them (fp8 codes to bf16 K; V to fp16, fp8 as code times the block's V
-//   scale) and writes them to the other two of four LDS buffers. K rows are
-//   padded so 16 rows hit distinct banks; V rows are stored with the two
-//   blocks' tokens interleaved in the order the P^T operand holds them, so each
-//   lane reads its 8 keys at once.
+//   (32 keys, a pair) at a time, two pairs per barrier, from four LDS buffers:
+//   while a step computes two pairs, the next two pairs' tiles travel to the
+//   other two buffers. On the image path they go straight from memory to LDS
+//   (global_load_lds, two 16-byte pieces per lane and pair, no registers and
+//   no conversion instructions); on the staging path (an image larger than the
+//   host allows) each thread loads its pieces into registers, converts them and
+//   writes them to LDS between the step's two pairs.
+// * Key order: lane group c (lanes 16c .. 16c + 15) holds keys 8c .. 8c + 7 of
+//   a pair in its score and P^T registers, 8 consecutive tokens of one block,
+//   so a 16-byte V operand is one 16-byte piece of a cached dim row.
 // * Per wave and pair: S^T[32 keys x 32 columns] = K . Q^T on
 //   v_mfma_f32_16x16x32_bf16, online softmax on the accumulators (lazy
 //   rescale), weights packed to fp16 and O^T += V^T . P^T on
@@ -146,7 +152,7 @@ __device__ PfSeq pf_seq(const PrefillArgs& a, int b, int& status, bool& bad) {
 // Offsets that are not non-decreasing within [0, T] list no item at all (status
 // bit 8): with them the sequences could overlap and overrun the list. Otherwise
 // the tiles add up to at most (T + B (TQ - 1)) / TQ = items_max.
-__global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PrefillArgs a) {
+__device__ void pf_plan(const PrefillArgs& a) {
   __shared__ int cursor[kPfBuckets];
   __shared__ int wave_sum[kPlanThreads / 64];
   const int tid = (int)threadIdx.x;
@@ -206,114 +212,39 @@ __global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PrefillArgs 
   if (status) atomicOr(a.hdr + kHdrStatus, status);
 }
 
-// ------------------------------------------------------------- attention
+// ------------------------------------------------------- layout and image
 
-// LDS layout of one pair (two 16-token blocks of one KV head), the same for
-// bf16 and fp8 caches (fp8 tiles are decoded while they are staged, once per
-// workgroup rather than once per wave):
-//   K  [32 keys][D] bf16 (fp8: the codes, exact in bf16), rows padded by 16 B
-//   V  [D][32 keys] fp16 (fp8: code * V scale), per dim row the segments
-//      c = 0..3 hold [block 0 tokens 4c..4c+3][block 1 tokens 4c..4c+3],
-//      the order in which a lane's P^T operand holds its 8 keys
+// LDS layout of one pair (two 16-token blocks of one KV head), the same on both
+// paths:
+//   K [32 keys][D] bf16 (fp8: the codes, exact in bf16); the 16-byte chunk h
+//     of key row k sits at chunk h ^ kswz(k), so the 16 rows that one K operand
+//     read touches fall on distinct banks
+//   V [2 blocks][D dims][16 tokens] fp16 (fp8: code * V scale); the 8-token
+//     half h of dim row d sits at half h ^ ((d >> 3) & 1)
+// Image tiles keep the cache's own layout (K [16 tokens][D] bf16, V [D][16
+// tokens] fp16), so a direct load copies 16-byte pieces of a tile.
 template <KvType KV, int D>
 struct PfCfg {
   static constexpr int GSZ = KV == KvType::FP8 ? 1 : 2;  // bytes per cached element
   static constexpr int KSTEPS = D / 32;                 // 16x16x32 k-steps over head_dim
   static constexpr int MT = D / 16;                     // 16-row tiles of O^T
-  static constexpr int GROW = D * GSZ;                  // bytes of a cached K token row
-  static constexpr int GVROW = 16 * GSZ;                // bytes of a cached V dim row (16 tokens)
-  static constexpr int TILEB = 16 * GROW;               // bytes of one cached (block, KV head) tile
+  static constexpr int GTILE = 16 * D * GSZ;            // bytes of one cached (block, KV head) tile
+  static constexpr int TILEB = 16 * D * 2;              // bytes of one image tile (and of a bf16 cache tile)
+  static constexpr int KROW = 2 * D;                    // bytes of an LDS K row
+  static constexpr int KBUF = 32 * KROW;
+  static constexpr int VBLK = 32 * D;                   // bytes of one block's V part in LDS
+  static constexpr int BUF = KBUF + 2 * VBLK;
+  static constexpr int NI = D / 64;                     // direct loads per wave and pair
   // staging unit: 8 elements (16 bytes of bf16, 8 bytes of fp8), so fp8 pairs keep every thread busy
   static constexpr int UB = 8 * GSZ;
-  static constexpr int UNITS = 2 * TILEB / UB;          // units of a pair's K (or V) tiles
+  static constexpr int UNITS = 2 * GTILE / UB;          // units of a pair's K (or V) tiles
   static constexpr int UPT = (UNITS + kPfThreads - 1) / kPfThreads;
-  static constexpr int KROW = 2 * D + 16;               // LDS K row stride: 16 rows on distinct banks
-  static constexpr int VROW = 64 + 16;                  // LDS V row stride (32 fp16 keys + pad)
-  static constexpr int KBUF = 32 * KROW;
-  static constexpr int BUF = KBUF + D * VROW;
 };
 
-// One pair on its way to LDS: each thread's 16-byte units of the cached K and
-// V tiles, and the pair's workgroup-uniform block flags, scales and live keys.
-template <KvType KV, int D>
-struct PfStage {
-  using Unit = typename std::conditional<KV == KvType::FP8, u32x2, u32x4>::type;
-  Unit k[PfCfg<KV, D>::UPT], v[PfCfg<KV, D>::UPT];
-  int ok0, ok1;   // block holds keys of the tile and its id is in range
-  int live;       // keys of the pair that exist (from the pair's first key)
-  float ks[2], vs[2];
-};
-
-// The tile's physical block ids, 64 at a time: lane i holds the id of block
-// 64q + i of chunk q (and, for fp8 caches, that block's K and V scales), read
-// with one vector load per chunk, the next chunk's ids one chunk ahead, so a
-// pair's ids come from v_readlane instead of a scalar load per block.
-struct PfIds {
-  int q;          // current chunk
-  int id, nxt;    // table entries of chunks q and q + 1, unchecked (lanes past the tile repeat its last block)
-};
-
-// Unconditional, and checked only where a pair reads it (pf_load): a check
-// here would wait for the load at once and the next chunk would not be
-// prefetched. The table row has max_blocks >= 1 entries and nblk <= max_blocks.
-__device__ __forceinline__ int pf_id_load(const int32_t* row, int j, int nblk) {
-  const int last = nblk > 0 ? nblk - 1 : 0;
-  return row[j < last ? j : last];
-}
-
-// Moves the ids to chunk q (q is ids.q or ids.q + 1) and loads chunk q + 1.
-// Unconditional: no loaded register is merged across paths (a copy of one
-// waits for its load), and the select reads a load issued a step earlier.
-__device__ __forceinline__ void pf_ids_advance(PfIds& ids, const int32_t* row, int q, int nblk) {
-  ids.id = q != ids.q ? ids.nxt : ids.id;
-  ids.q = q;
-  ids.nxt = pf_id_load(row, 64 * (q + 1) + lane_id(), nblk);
-}
-
-template <KvType KV, int D>
-__device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, const PfIds& ids, int j0, int nblk,
-                                        int nkeys, int kvh, int& status) {
-  using C = PfCfg<KV, D>;
-  int64_t tile[2];
-  int ok[2];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int p = __builtin_amdgcn_readlane(ids.id, (j0 + s) & 63);
-    const bool inside = j0 + s < nblk;  // the block holds keys of the tile
-    ok[s] = inside && (uint64_t)(uint32_t)p < (uint64_t)a.num_blocks;
-    if (inside && !ok[s]) status |= kStatusBadBlock;
-    tile[s] = (int64_t)(ok[s] ? p : 0) * a.Hkv + kvh;
-    st.ks[s] = 1.f;
-    st.vs[s] = 1.f;
-    if constexpr (KV == KvType::FP8) {  // raw: a block with no id takes scale 1 where they are used
-      st.ks[s] = a.kv_scales[tile[s]];
-      st.vs[s] = a.kv_scales[a.num_blocks * a.Hkv + tile[s]];
-    }
-  }
-  st.ok0 = ok[0];
-  st.ok1 = ok[1];
-  int live = nkeys - 16 * j0;
-  if (!ok[1]) live = live < 16 ? live : 16;
-  if (!ok[0]) live = 0;
-  st.live = live;
-  const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
-  const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
-  using Unit = typename PfStage<KV, D>::Unit;
-  static_assert((C::TILEB / C::UB) % 64 == 0, "a wave's units lie in one block");
-#pragma unroll
-  for (int u = 0; u < C::UPT; ++u) {
-    const int unit = (int)threadIdx.x + kPfThreads * u;
-    const int blk = uni(unit / (C::TILEB / C::UB));  // the same for the whole wave
-    const int off = (unit - blk * (C::TILEB / C::UB)) * C::UB;
-    const int64_t base = (blk & 1 ? tile[1] : tile[0]) * C::TILEB;  // uniform
-    // Unconditional: a block with no id reads tile 0 of its KV head and a unit
-    // past the pair's tiles reads inside them (never stored), so every path
-    // issues the same loads and the store that consumes them waits for its own
-    // pair's loads only. The keys of a block with no id are masked (scores to
-    // -inf, V rows zeroed bitwise) on every path that could read them.
-    st.k[u] = *reinterpret_cast<const Unit*>(kc + base + off);
-    st.v[u] = *reinterpret_cast<const Unit*>(vc + base + off);
-  }
+template <int D>
+__device__ __forceinline__ int pf_kswz(int k) {
+  if constexpr (D == 128) return (k & 3) | ((k >> 3) << 2);
+  else return ((k >> 1) & 1) | ((k >> 3) << 1);
 }
 
 constexpr float kHalfMax = 65504.f;  // largest finite fp16
@@ -339,63 +270,354 @@ __device__ __forceinline__ void v_pack(const float (&f)[N], uint32_t (&out)[N / 
   }
 }
 
+// 8 bf16 (one 16-byte piece) -> 8 fp16; k0: key index of the first, live: keys that exist
+__device__ __forceinline__ u32x4 bf16x8_to_half(u32x4 x, int k0, int live, int& ovf) {
+  float f[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __builtin_bit_cast(float, x[i] << 16);
+    f[2 * i + 1] = __builtin_bit_cast(float, x[i] & 0xFFFF0000u);
+  }
+  uint32_t h[4];
+  v_pack<8>(f, h, k0, live, ovf);
+  return u32x4{h[0], h[1], h[2], h[3]};
+}
+
+// 8 E4M3 codes times the block's V scale -> 8 fp16, one rounding from fp32
+__device__ __forceinline__ u32x4 fp8x8_to_half(u32x2 x, float vs, int k0, int live, int& ovf) {
+  float f[8];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float2 x01 = fp8x2_to_f32x2<false>(x[i], vs), x23 = fp8x2_to_f32x2<true>(x[i], vs);
+    f[4 * i] = x01.x;
+    f[4 * i + 1] = x01.y;
+    f[4 * i + 2] = x23.x;
+    f[4 * i + 3] = x23.y;
+  }
+  uint32_t h[4];
+  if (vs * 448.f <= kHalfMax) {  // no code can leave the fp16 range
+#pragma unroll
+    for (int i = 0; i < 4; ++i) h[i] = pk_f16(f[2 * i], f[2 * i + 1]);
+  } else {
+    v_pack<8>(f, h, k0, live, ovf);
+  }
+  return u32x4{h[0], h[1], h[2], h[3]};
+}
+
+// 8 E4M3 codes -> 8 bf16 (exact, unscaled: the K scale goes on the logits)
+__device__ __forceinline__ u32x4 fp8x8_to_bf16(u32x2 x) {
+  const u32x2 a0 = fp8x4_to_bf16x4(x.x), a1 = fp8x4_to_bf16x4(x.y);
+  return u32x4{a0.x, a0.y, a1.x, a1.y};
+}
+
+constexpr int kImgBlocks = 16;  // table entries per image workgroup
+constexpr int kImgBatch = 4;    // pieces a thread loads before it converts and stores them
+
+// Image workgroup g: table entries kImgBlocks * (g % cps) + 0 .. kImgBlocks - 1
+// of sequence g / cps. Every tile (all KV heads) of a block that a sequence
+// with queries reads, keys 0 .. L_b - 1, is converted to the image, indexed
+// like the cache (block * Hkv + KV head); blocks shared by several sequences
+// are written by each with the same bytes. Entries outside [0, num_blocks) are
+// skipped (the attention kernel flags them). A live V value beyond the fp16
+// range saturates and sets status bit 16.
 template <KvType KV, int D>
-__device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, uint8_t* buf, int& status) {
+__device__ void pf_image(const PrefillArgs& a, int g) {
+  using C = PfCfg<KV, D>;
+  const int cps = (a.max_blocks + kImgBlocks - 1) / kImgBlocks;
+  const int b = g / cps;
+  const int j0 = (g - b * cps) * kImgBlocks;
+  const int o0 = a.q_offsets[b], o1 = a.q_offsets[b + 1];
+  if (o0 < 0 || o1 > a.T || o1 <= o0) return;  // no queries, or offsets the plan rejects
+  int L = a.seq_lens[b];
+  L = L < 0 ? 0 : (L > a.len_cap ? a.len_cap : L);
+  const int nblk = (L + 15) / 16;
+  const int nb = nblk - j0 < kImgBlocks ? nblk - j0 : kImgBlocks;
+  if (nb <= 0) return;
+  constexpr int UT = 2 * D;  // 8-element pieces of a tile
+  const int vpieces = a.Hkv * UT;
+  const int per_blk = KV == KvType::FP8 ? 2 * vpieces : vpieces;  // fp8: V pieces, then K pieces
+  const int total = nb * per_blk;
+  const int32_t* row = a.block_table + (int64_t)b * a.max_blocks;
+  const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
+  const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
+  uint8_t* ki = static_cast<uint8_t*>(a.k_img);
+  uint8_t* vi = static_cast<uint8_t*>(a.v_img);
+  using Unit = typename std::conditional<KV == KvType::FP8, u32x2, u32x4>::type;
+  int ovf = 0;
+  for (int u0 = (int)threadIdx.x; u0 < total; u0 += kImgBatch * kPlanThreads) {
+    Unit x[kImgBatch];
+    int64_t tile[kImgBatch];
+    int e[kImgBatch], live[kImgBatch], kind[kImgBatch];  // kind: 0 none, 1 V, 2 K
+    float vs[kImgBatch];
+#pragma unroll
+    for (int i = 0; i < kImgBatch; ++i) {
+      const int u = u0 + i * kPlanThreads;
+      kind[i] = 0;
+      if (u >= total) continue;
+      const int jj = u / per_blk;
+      int rest = u - jj * per_blk;
+      const int p = row[j0 + jj];
+      if ((uint64_t)(uint32_t)p >= (uint64_t)a.num_blocks) continue;
+      const bool is_k = rest >= vpieces;
+      if (is_k) rest -= vpieces;
+      const int h = rest / UT;
+      e[i] = rest - h * UT;
+      tile[i] = (int64_t)p * a.Hkv + h;
+      live[i] = L - 16 * (j0 + jj);
+      kind[i] = is_k ? 2 : 1;
+      x[i] = *reinterpret_cast<const Unit*>((is_k ? kc : vc) + tile[i] * C::GTILE + e[i] * C::UB);
+      vs[i] = 1.f;
+      if constexpr (KV == KvType::FP8) {
+        if (!is_k) vs[i] = a.kv_scales[a.num_blocks * a.Hkv + tile[i]];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kImgBatch; ++i) {
+      if (kind[i] == 0) continue;
+      // piece e of a V tile: dim row e / 2, tokens 8 (e % 2) .. + 7 of the block
+      const int k0 = 8 * (e[i] & 1);
+      uint8_t* dst = (kind[i] == 2 ? ki : vi) + tile[i] * C::TILEB + e[i] * 16;
+      u32x4 y;
+      if constexpr (KV == KvType::FP8) {
+        y = kind[i] == 2 ? fp8x8_to_bf16(x[i]) : fp8x8_to_half(x[i], vs[i], k0, live[i], ovf);
+      } else {
+        y = bf16x8_to_half(x[i], k0, live[i], ovf);
+      }
+      *reinterpret_cast<u32x4*>(dst) = y;
+    }
+  }
+  if (ovf) atomicOr(a.hdr + kHdrStatus, kStatusHalfRange);
+}
+
+__global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PrefillArgs a) { pf_plan(a); }
+
+// The plan (workgroup 0) and the image (the others) in one launch.
+template <KvType KV, int D>
+__global__ __launch_bounds__(kPlanThreads) void prefill_prep_kernel(PrefillArgs a) {
+  if (blockIdx.x == 0) {
+    pf_plan(a);
+    return;
+  }
+  pf_image<KV, D>(a, (int)blockIdx.x - 1);
+}
+
+// ------------------------------------------------------------- attention
+
+// The tile's physical block ids, 64 at a time: lane i holds the id of block
+// 64q + i of chunk q, read with one vector load per chunk, the next chunk's
+// ids one chunk ahead, so a pair's ids come from v_readlane instead of a
+// scalar load per block.
+struct PfIds {
+  int q;          // current chunk
+  int id, nxt;    // table entries of chunks q and q + 1, unchecked (lanes past the tile repeat its last block)
+};
+
+// Unconditional, and checked only where a pair reads it (pf_pair): a check
+// here would wait for the load at once and the next chunk would not be
+// prefetched. The table row has max_blocks >= 1 entries and nblk <= max_blocks.
+__device__ __forceinline__ int pf_id_load(const int32_t* row, int j, int nblk) {
+  const int last = nblk > 0 ? nblk - 1 : 0;
+  return row[j < last ? j : last];
+}
+
+// Moves the ids to chunk q (q is ids.q or ids.q + 1) and loads chunk q + 1.
+// Unconditional: no loaded register is merged across paths (a copy of one
+// waits for its load), and the select reads a load issued a step earlier.
+__device__ __forceinline__ void pf_ids_advance(PfIds& ids, const int32_t* row, int q, int nblk) {
+  ids.id = q != ids.q ? ids.nxt : ids.id;
+  ids.q = q;
+  ids.nxt = pf_id_load(row, 64 * (q + 1) + lane_id(), nblk);
+}
+
+__device__ __forceinline__ int64_t uni64(int64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// One pair's blocks, workgroup-uniform: tiles (block * Hkv + KV head; a block
+// with no id names tile 0 of its KV head, whose keys are masked), flags,
+// fp8 scales as loaded (used only after the next wait) and live keys. Named
+// fields, not two-element arrays: a select between array elements can become
+// an indexed access, which puts the array in scratch memory.
+struct PfPair {
+  int64_t t0, t1;
+  int ok0, ok1;   // block holds keys of the tile and its id is in range
+  float ks0, ks1, vs0, vs1;
+  int live;       // keys of the pair that exist (from the pair's first key)
+};
+
+template <KvType KV, bool IMG>
+__device__ __forceinline__ PfPair pf_pair(const PrefillArgs& a, const PfIds& ids, int j0, int nblk, int nkeys,
+                                          int kvh, int& status) {
+  int64_t tile[2];
+  int ok[2];
+  float ks[2] = {1.f, 1.f}, vs[2] = {1.f, 1.f};
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int p = __builtin_amdgcn_readlane(ids.id, (j0 + s) & 63);
+    const bool inside = j0 + s < nblk;  // the block holds keys of the tile
+    ok[s] = inside && (uint64_t)(uint32_t)p < (uint64_t)a.num_blocks;
+    if (inside && !ok[s]) status |= kStatusBadBlock;
+    tile[s] = uni64((int64_t)(ok[s] ? p : 0) * a.Hkv + kvh);
+    if constexpr (KV == KvType::FP8) {  // raw: a block with no id takes scale 1 where they are used
+      ks[s] = a.kv_scales[tile[s]];
+      if constexpr (!IMG) vs[s] = a.kv_scales[a.num_blocks * a.Hkv + tile[s]];
+    }
+  }
+  int live = nkeys - 16 * j0;
+  if (!ok[1]) live = live < 16 ? live : 16;
+  if (!ok[0]) live = 0;
+  return PfPair{tile[0], tile[1], ok[0], ok[1], ks[0], ks[1], vs[0], vs[1], live};
+}
+
+// V scale of block s of the pair (1 for a block with no id; staging path)
+__device__ __forceinline__ float pf_vs(const PfPair& pp, int s) {
+  return s ? (pp.ok1 ? pp.vs1 : 1.f) : (pp.ok0 ? pp.vs0 : 1.f);
+}
+
+// Per-pair values a wave needs once the pair's tiles are in LDS.
+struct PfMeta {
+  float c0, c1;  // softmax scale (log2 units) times the blocks' K scales, > 0
+  int live;      // keys of the pair that exist
+};
+
+__device__ __forceinline__ PfMeta pf_meta(const PfPair& pp, float scale_log2) {
+  // c > 0: a zero or tiny scale leaves every weight at 1 either way
+  const float k0 = pp.ok0 ? pp.ks0 : 1.f, k1 = pp.ok1 ? pp.ks1 : 1.f;
+  return PfMeta{fmaxf(scale_log2 * k0, 1e-30f), fmaxf(scale_log2 * k1, 1e-30f), pp.live};
+}
+
+// ---- image path: direct loads
+
+// A wave's part of a pair's direct loads: per load, K or V, which of the two
+// blocks, this lane's byte offset in that block's tile, and the LDS offset in
+// the pair's buffer of the load's first lane (lane i writes 16 bytes at + 16 i).
+template <int D>
+struct PfLane {
+  int is_v[D / 64], blk[D / 64], dst[D / 64];
+  uint32_t off[D / 64];
+};
+
+// D = 128: wave w loads K rows 4w .. 4w + 3 (block w / 4) and V dim rows
+// 32 (w % 4) .. + 31 of block w / 4. D = 64: waves 0-3 load K rows 8w .. 8w + 7,
+// waves 4-7 V dim rows 32 (w % 2) .. + 31 of block (w - 4) / 2.
+template <int D>
+__device__ __forceinline__ PfLane<D> pf_lane(int w, int l) {
+  PfLane<D> pl;
+  const int kbuf = 32 * 2 * D;
+  if constexpr (D == 128) {
+    const int row = 4 * w + (l >> 4);
+    pl.is_v[0] = 0;
+    pl.blk[0] = w >> 2;
+    pl.dst[0] = 1024 * w;
+    pl.off[0] = (uint32_t)((row & 15) * 256 + 16 * ((l & 15) ^ pf_kswz<D>(row)));
+    const int d = 32 * (w & 3) + (l >> 1);
+    pl.is_v[1] = 1;
+    pl.blk[1] = w >> 2;
+    pl.dst[1] = kbuf + 1024 * w;
+    pl.off[1] = (uint32_t)(d * 32 + 16 * ((l & 1) ^ ((d >> 3) & 1)));
+  } else {
+    if (w < 4) {
+      const int row = 8 * w + (l >> 3);
+      pl.is_v[0] = 0;
+      pl.blk[0] = w >> 1;
+      pl.dst[0] = 1024 * w;
+      pl.off[0] = (uint32_t)((row & 15) * 128 + 16 * ((l & 7) ^ pf_kswz<D>(row)));
+    } else {
+      const int v = w - 4, d = 32 * (v & 1) + (l >> 1);
+      pl.is_v[0] = 1;
+      pl.blk[0] = v >> 1;
+      pl.dst[0] = kbuf + 1024 * v;
+      pl.off[0] = (uint32_t)(d * 32 + 16 * ((l & 1) ^ ((d >> 3) & 1)));
+    }
+  }
+  return pl;
+}
+
+// One 16-byte piece per lane from base + off to LDS address lds + 16 * lane
+// (global_load_lds_dwordx4; M0 holds the LDS address). base and lds are
+// wave-uniform and made scalar here, as the instruction needs. The compiler
+// does not see this load: completion is awaited with pf_dma_wait before the
+// barrier that publishes the buffer. (Through the compiler's own builtin every
+// LDS read in the kernel would wait for all LDS traffic, lgkmcnt(0).)
+__device__ __forceinline__ void pf_dma16(const uint8_t* base_v, uint32_t off, uint32_t lds_v) {
+  const uint8_t* base = reinterpret_cast<const uint8_t*>(uni64(reinterpret_cast<int64_t>(base_v)));
+  const uint32_t lds = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_v);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+__device__ __forceinline__ void pf_dma_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_dma(const uint8_t* kimg, const uint8_t* vimg, int64_t t0, int64_t t1,
+                                       const PfLane<D>& pl, uint32_t buf) {
+  using C = PfCfg<KV, D>;
+#pragma unroll
+  for (int e = 0; e < C::NI; ++e) {
+    const uint8_t* base = (pl.is_v[e] ? vimg : kimg) + (pl.blk[e] ? t1 : t0) * C::TILEB;
+    pf_dma16(base, pl.off[e], buf + pl.dst[e]);
+  }
+}
+
+// ---- staging path: registers
+
+// One pair on its way to LDS: each thread's pieces of the cached K and V tiles.
+template <KvType KV, int D>
+struct PfStage {
+  using Unit = typename std::conditional<KV == KvType::FP8, u32x2, u32x4>::type;
+  Unit k[PfCfg<KV, D>::UPT], v[PfCfg<KV, D>::UPT];
+};
+
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_load(PfStage<KV, D>& st, const PrefillArgs& a, int64_t t0, int64_t t1) {
+  using C = PfCfg<KV, D>;
+  const uint8_t* kc = static_cast<const uint8_t*>(a.k_cache);
+  const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
+  using Unit = typename PfStage<KV, D>::Unit;
+  static_assert((C::GTILE / C::UB) % 64 == 0, "a wave's units lie in one block");
+#pragma unroll
+  for (int u = 0; u < C::UPT; ++u) {
+    const int unit = (int)threadIdx.x + kPfThreads * u;
+    const int blk = uni(unit / (C::GTILE / C::UB));  // the same for the whole wave
+    const int off = (unit - blk * (C::GTILE / C::UB)) * C::UB;
+    const int64_t base = (blk & 1 ? t1 : t0) * C::GTILE;  // uniform
+    // Unconditional: a unit past the pair's tiles reads inside them (never
+    // stored), so every path issues the same loads and the store that consumes
+    // them waits for its own pair's loads only.
+    st.k[u] = *reinterpret_cast<const Unit*>(kc + base + off);
+    st.v[u] = *reinterpret_cast<const Unit*>(vc + base + off);
+  }
+}
+
+template <KvType KV, int D>
+__device__ __forceinline__ void pf_store(const PfStage<KV, D>& st, float vs0, float vs1, int live, uint8_t* buf,
+                                         int& status) {
   using C = PfCfg<KV, D>;
   int ovf = 0;
 #pragma unroll
   for (int u = 0; u < C::UPT; ++u) {
     const int unit = (int)threadIdx.x + kPfThreads * u;
     if (unit >= C::UNITS) break;
-    const int blk = unit / (C::TILEB / C::UB);
-    const int off = (unit - blk * (C::TILEB / C::UB)) * C::UB;
-    const int krow = off / C::GROW, e0 = (off - krow * C::GROW) / C::GSZ;  // token row, first element
-    uint8_t* kdst = buf + (blk * 16 + krow) * C::KROW + 2 * e0;
-    const int d = off / C::GVROW, t0 = (off - d * C::GVROW) / C::GSZ;     // dim row, first token
-    uint8_t* vrow = buf + C::KBUF + d * C::VROW + 8 * blk;               // segment c at + 16 c
-    const int k0 = 16 * blk + t0;                                         // pair-relative key of t0
+    const int blk = unit / (C::GTILE / C::UB);
+    const int off = (unit - blk * (C::GTILE / C::UB)) * C::UB;
+    const int krow = off / (D * C::GSZ), kh = (off - krow * D * C::GSZ) / (8 * C::GSZ);  // token row, chunk
+    const int k = 16 * blk + krow;
+    uint8_t* kdst = buf + k * C::KROW + 16 * (kh ^ pf_kswz<D>(k));
+    const int d = off / (16 * C::GSZ), t0 = (off - d * 16 * C::GSZ) / C::GSZ;  // dim row, first token (0 or 8)
+    uint8_t* vdst = buf + C::KBUF + blk * C::VBLK + d * 32 + 16 * ((t0 >> 3) ^ ((d >> 3) & 1));
+    const int k0 = 16 * blk + t0;  // pair-relative key of token t0
     if constexpr (KV == KvType::BF16) {
       *reinterpret_cast<u32x4*>(kdst) = st.k[u];
-      float f[8];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f[2 * i] = __builtin_bit_cast(float, st.v[u][i] << 16);
-        f[2 * i + 1] = __builtin_bit_cast(float, st.v[u][i] & 0xFFFF0000u);
-      }
-      uint32_t h[4];
-      v_pack<8>(f, h, k0, st.live, ovf);
-      const int c = t0 / 4;  // 0 or 2
-      *reinterpret_cast<u32x2*>(vrow + 16 * c) = u32x2{h[0], h[1]};
-      *reinterpret_cast<u32x2*>(vrow + 16 * (c + 1)) = u32x2{h[2], h[3]};
+      *reinterpret_cast<u32x4*>(vdst) = bf16x8_to_half(st.v[u], k0, live, ovf);
     } else {
-      // K: 8 codes -> 8 bf16 (exact, unscaled: the K scale goes on the logits)
-      const u32x2 a0 = fp8x4_to_bf16x4(st.k[u].x), a1 = fp8x4_to_bf16x4(st.k[u].y);
-      *reinterpret_cast<u32x4*>(kdst) = u32x4{a0.x, a0.y, a1.x, a1.y};
-      // V: tokens t0 .. t0 + 7 of dim row d, code * scale in fp32, one rounding to fp16
-      const float vs = (blk & 1) ? (st.ok1 ? st.vs[1] : 1.f) : (st.ok0 ? st.vs[0] : 1.f);
-      float f[8];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const float2 x01 = fp8x2_to_f32x2<false>(st.v[u][i], vs), x23 = fp8x2_to_f32x2<true>(st.v[u][i], vs);
-        f[4 * i] = x01.x;
-        f[4 * i + 1] = x01.y;
-        f[4 * i + 2] = x23.x;
-        f[4 * i + 3] = x23.y;
-      }
-      uint32_t h[4];
-      if (vs * 448.f <= kHalfMax) {  // no code can leave the fp16 range
-#pragma unroll
-        for (int i = 0; i < 4; ++i) h[i] = pk_f16(f[2 * i], f[2 * i + 1]);
-      } else {
-        v_pack<8>(f, h, k0, st.live, ovf);
-      }
-      const int c = t0 / 4;  // 0 or 2
-      *reinterpret_cast<u32x2*>(vrow + 16 * c) = u32x2{h[0], h[1]};
-      *reinterpret_cast<u32x2*>(vrow + 16 * (c + 1)) = u32x2{h[2], h[3]};
+      *reinterpret_cast<u32x4*>(kdst) = fp8x8_to_bf16(st.k[u]);
+      *reinterpret_cast<u32x4*>(vdst) = fp8x8_to_half(st.v[u], blk & 1 ? vs1 : vs0, k0, live, ovf);
     }
   }
   if (ovf) status |= kStatusHalfRange;
 }
+
+// ---- per wave and pair
 
 // Running softmax state of one 16-column N-tile (per lane: column r).
 struct PfRow {
@@ -405,37 +627,42 @@ struct PfRow {
 };
 
 // A pair's LDS operands in registers, one slot per K piece or V tile: slot i
-// holds K piece i (d-step i / 2; rows r of block 0 for even i, rows 16 + r of
-// block 1 for odd i), then V^T tile i (dim rows 16i + r, keys 8c .. 8c + 7 of
-// the pair in the P^T order). A pair's tiles replace its pieces, and the next
-// pair's pieces replace the tiles.
+// holds K piece i (d-step i / 2, t = i % 2), then V^T tile i (dim rows
+// 16i + r). A pair's tiles replace its pieces, and the next pair's pieces
+// replace the tiles.
 template <KvType KV, int D>
 struct PfOps {
   u32x4 x[PfCfg<KV, D>::MT];
 };
 
-// K piece i (d-step i / 2, block i % 2) and V tile m of the pair in buf.
+// K piece i: lane (r, c) reads key row 8 (r / 4) + 4t + r % 4, d-step i / 2,
+// so row 4c + e of the piece's scores is key 8c + 4t + e.
 template <KvType KV, int D>
 __device__ __forceinline__ void pf_kread(const uint8_t* buf, PfOps<KV, D>& o, int i) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
   const int j = i >> 1, t = i & 1;
-  o.x[i] = *reinterpret_cast<const u32x4*>(buf + (16 * t + r) * C::KROW + 64 * j + 16 * c);
+  const int k = 8 * (r >> 2) + 4 * t + (r & 3);
+  o.x[i] = *reinterpret_cast<const u32x4*>(buf + k * C::KROW + 16 * ((4 * j + c) ^ pf_kswz<D>(k)));
 }
+// V tile m: lane (r, c) reads dim row 16m + r, keys 8c .. 8c + 7 (block c / 2,
+// half c % 2), the P^T operand order.
 template <KvType KV, int D>
 __device__ __forceinline__ void pf_vread(const uint8_t* buf, PfOps<KV, D>& o, int m) {
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
-  o.x[m] = *reinterpret_cast<const u32x4*>(buf + C::KBUF + (16 * m + r) * C::VROW + 16 * c);
+  const int d = 16 * m + r;
+  o.x[m] = *reinterpret_cast<const u32x4*>(buf + C::KBUF + (c >> 1) * C::VBLK + d * 32 +
+                                           16 * ((c & 1) ^ ((d >> 3) & 1)));
 }
 
-// S^T[32 keys x 32 columns] = K . Q^T of a pair whose K pieces are in o. s0
-// holds keys 4c..4c+3 of the first block, s1 of the second, for column r of
-// each N-tile. VNEXT: the pair's V tiles are read from vbuf between the MFMAs,
-// each into the slots of the d-step just used, so the LDS serves them while
-// the matrix core works (a wave issues in order: reads placed after the MFMAs
+// S^T[32 keys x 32 columns] = K . Q^T of a pair whose K pieces are in o: s0
+// holds keys 8c .. 8c + 3, s1 keys 8c + 4 .. 8c + 7 for column r of each
+// N-tile. VNEXT: the pair's V tiles are read from vbuf between the MFMAs, each
+// into the slots of the d-step just used, so the LDS serves them while the
+// matrix core works (a wave issues in order: reads placed after the MFMAs
 // would start only when the last one issues).
 template <KvType KV, int D, bool VNEXT>
 __device__ __forceinline__ void pf_scores(PfOps<KV, D>& o, const bf16x8 (&qb)[kPfNT][PfCfg<KV, D>::KSTEPS],
@@ -462,7 +689,7 @@ __device__ __forceinline__ void pf_scores(PfOps<KV, D>& o, const bf16x8 (&qb)[kP
 
 // Softmax weights of one pair from its scores. MASKED: per-column key limits
 // see[n] (keys of the pair the column sees). c0 / c1: softmax scale (log2
-// units) times the blocks' K scales, > 0.
+// units) times the blocks' K scales, > 0; a lane's 8 keys lie in block c / 2.
 //
 // The weights are exp2(logit - m) with a lazily updated running max m: only
 // when a logit exceeds m by more than kSlack (so weights stay below 2^8 and fit
@@ -480,25 +707,23 @@ __device__ __forceinline__ void pf_softmax(const f32x4 (&s0)[kPfNT], const f32x4
   using C = PfCfg<KV, D>;
   const int l = lane_id();
   const int c = l >> 4;
+  const float cs = c < 2 ? c0 : c1;
   const f16x8 ones = {1, 1, 1, 1, 1, 1, 1, 1};
 #pragma unroll
   for (int n = 0; n < kPfNT; ++n) {
-    float y[8];  // raw scores of keys 4c+i (block 0) and 16+4c+i (block 1)
+    float y[8];  // raw scores of keys 8c + i
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       y[i] = s0[n][i];
       y[4 + i] = s1[n][i];
-      if constexpr (MASKED) {
-        y[i] = 4 * c + i < see[n] ? y[i] : kNegInf;
-        y[4 + i] = 16 + 4 * c + i < see[n] ? y[4 + i] : kNegInf;
-      }
     }
-    float lm;  // this lane's largest scaled logit
-    if constexpr (KV == KvType::FP8) {
-      lm = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])) * c0, fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7])) * c1);
-    } else {
-      lm = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]))) * c0;
+    if constexpr (MASKED) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) y[i] = 8 * c + i < see[n] ? y[i] : kNegInf;
     }
+    // this lane's largest scaled logit
+    const float lm =
+        fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7]))) * cs;
     if (__any(lm > row[n].m + kSlack)) {
       float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
@@ -512,7 +737,7 @@ __device__ __forceinline__ void pf_softmax(const f32x4 (&s0)[kPfNT], const f32x4
     }
     float p[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(y[i], i < 4 ? c0 : c1, row[n].nm));
+    for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(y[i], cs, row[n].nm));
     u32x4 w;
 #pragma unroll
     for (int i = 0; i < 4; ++i) w[i] = pk_f16(p[2 * i], p[2 * i + 1]);
@@ -530,10 +755,10 @@ __device__ __forceinline__ void pf_softmax(const f32x4 (&s0)[kPfNT], const f32x4
 }
 
 // O^T += V^T . P^T, V tiles VFROM .. MT - 1 read from vbuf first (the others
-// are in o already). MASKED: V rows at or past `live` keys are zeroed (bitwise, so NaN poison
-// in unused slots never reaches the product). KNEXT: the next pair's K pieces
-// are read from kbuf between the MFMAs, each into the slot of the tile just
-// used.
+// are in o already). MASKED: V rows at or past `live` keys are zeroed (bitwise,
+// so NaN poison in unused slots never reaches the product). KNEXT: the next
+// pair's K pieces are read from kbuf between the MFMAs, each into the slot of
+// the tile just used.
 template <KvType KV, int D, bool MASKED, bool KNEXT, int VFROM>
 __device__ __forceinline__ void pf_pv(PfOps<KV, D>& o, const f16x8 (&ph)[kPfNT], int live,
                                       f32x4 (&acc)[PfCfg<KV, D>::MT][kPfNT], const uint8_t* vbuf,
@@ -547,8 +772,8 @@ __device__ __forceinline__ void pf_pv(PfOps<KV, D>& o, const f16x8 (&ph)[kPfNT],
   uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};
   if constexpr (MASKED) {
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {  // word h: keys 16 * (h / 2) + 4c + 2 * (h % 2) + {0, 1}
-      const int k = 16 * (h >> 1) + 4 * c + 2 * (h & 1);
+    for (int h = 0; h < 4; ++h) {  // word h: keys 8c + 2h, 8c + 2h + 1
+      const int k = 8 * c + 2 * h;
       mk[h] = (k < live ? 0xFFFFu : 0u) | (k + 1 < live ? 0xFFFF0000u : 0u);
     }
   }
@@ -567,20 +792,7 @@ __device__ __forceinline__ void pf_pv(PfOps<KV, D>& o, const f16x8 (&ph)[kPfNT],
   }
 }
 
-// Per-pair values a wave needs after the pair's tiles are in LDS.
-struct PfMeta {
-  float c0, c1;  // softmax scale (log2 units) times the blocks' K scales, > 0
-  int live;      // keys of the pair that exist
-};
-
-template <KvType KV, int D>
-__device__ __forceinline__ PfMeta pf_meta(const PfStage<KV, D>& st, float scale_log2) {
-  // c > 0: a zero or tiny scale leaves every weight at 1 either way
-  const float k0 = st.ok0 ? st.ks[0] : 1.f, k1 = st.ok1 ? st.ks[1] : 1.f;
-  return PfMeta{fmaxf(scale_log2 * k0, 1e-30f), fmaxf(scale_log2 * k1, 1e-30f), st.live};
-}
-
-template <KvType KV, int D>
+template <KvType KV, int D, bool IMG>
 __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   using C = PfCfg<KV, D>;
   __shared__ __attribute__((aligned(16))) uint8_t lds[4 * C::BUF];
@@ -588,13 +800,18 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const int l = lane_id();
   const int r = l & 15, c = l >> 4;
   const int w = uni((int)(threadIdx.x >> 6));  // wave-uniform: keeps per-wave values scalar
+  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)lds;
+  const uint8_t* kimg = static_cast<const uint8_t*>(KV == KvType::FP8 ? a.k_img : a.k_cache);
+  const uint8_t* vimg = static_cast<const uint8_t*>(a.v_img);
+  PfLane<D> pl;
+  if constexpr (IMG) pl = pf_lane<D>(w, l);
   // Unit n of queue x is item n / hq for KV head x + nq (n % hq). The grid
   // (a multiple of 8 workgroups) starts on the first gridDim / nq units of each
   // queue; each further unit is claimed with a ticket from the queue's counter
-  // in the workspace header (zeroed by the plan kernel). Unit k's claim is
-  // issued as unit k starts and published in s_next[k & 1] at its first
-  // barrier; every thread reads it after its last, so a slot is rewritten only
-  // after all threads read it (two units later).
+  // in the workspace header (zeroed by the plan). Unit k's claim is issued as
+  // unit k starts and published in s_next[k & 1] at its first barrier; every
+  // thread reads it after its last, so a slot is rewritten only after all
+  // threads read it (two units later).
   const int nq = a.nq, hq = a.Hkv / nq;
   const int qsize = uni(a.hdr[kHdrItems]) * hq;  // units per queue
   const int first_claims = (int)gridDim.x / nq;
@@ -675,29 +892,35 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     };
 
     // Two pairs per barrier: step j computes pairs j and j + 1 from LDS buffers
-    // j % 4 and (j + 1) % 4 while pairs j + 2 and j + 3 are loaded into two
-    // register sets and staged (between pairs j and j + 1) into the other two
-    // buffers. The loads are
-    // unconditional (past the end the last pair again, never stored), so no
-    // loaded register is merged across paths: a copy of one would wait for its
-    // load at once. (Running the two waves of a SIMD half a pair apart, so one's
-    // softmax would overlap the other's matrix work, measured slower.)
-    PfStage<KV, D> sa, sb;
+    // j % 4 and (j + 1) % 4 while pairs j + 2 and j + 3 travel to the other two:
+    // direct loads issued at the step's start (image path), or loads into two
+    // register sets that are converted and stored between the step's two pairs
+    // (staging path: with their registers free, pair j + 1's V tiles fit beside
+    // its softmax). The id and staging loads are unconditional (past the end
+    // the last pair again, never stored), so no loaded register is merged
+    // across paths: a copy of one would wait for its load at once.
     PfIds ids;
     ids.q = -1;
     ids.id = 0;
     ids.nxt = pf_id_load(row, l, nblk);  // chunk 0
     pf_ids_advance(ids, row, 0, nblk);
     PfMeta m0{1.f, 1.f, 0}, m1{1.f, 1.f, 0};
-    if (npairs > 0) {  // both pairs' loads before either store: one round trip
-      pf_load<KV, D>(sa, a, ids, 0, nblk, nkeys, kvh, status);
-      pf_load<KV, D>(sb, a, ids, npairs > 1 ? 2 : 0, nblk, nkeys, kvh, status);
-      pf_store<KV, D>(sa, lds, status);
-      m0 = pf_meta<KV, D>(sa, a.scale_log2);
-      if (npairs > 1) {
-        pf_store<KV, D>(sb, lds + C::BUF, status);
-        m1 = pf_meta<KV, D>(sb, a.scale_log2);
+    {
+      const PfPair pa = pf_pair<KV, IMG>(a, ids, 0, nblk, nkeys, kvh, status);
+      const PfPair pb = pf_pair<KV, IMG>(a, ids, npairs > 1 ? 2 : 0, nblk, nkeys, kvh, status);
+      if constexpr (IMG) {
+        if (npairs > 0) pf_dma<KV, D>(kimg, vimg, pa.t0, pa.t1, pl, lds0);
+        if (npairs > 1) pf_dma<KV, D>(kimg, vimg, pb.t0, pb.t1, pl, lds0 + C::BUF);
+        pf_dma_wait();
+      } else if (npairs > 0) {  // both pairs' loads before either store: one round trip
+        PfStage<KV, D> sa, sb;
+        pf_load<KV, D>(sa, a, pa.t0, pa.t1);
+        pf_load<KV, D>(sb, a, pb.t0, pb.t1);
+        pf_store<KV, D>(sa, pf_vs(pa, 0), pf_vs(pa, 1), pa.live, lds, status);
+        if (npairs > 1) pf_store<KV, D>(sb, pf_vs(pb, 0), pf_vs(pb, 1), pb.live, lds + C::BUF, status);
       }
+      m0 = pf_meta(pa, a.scale_log2);
+      m1 = pf_meta(pb, a.scale_log2);
     }
     if (threadIdx.x == 0) {  // the next unit: 8 * index + queue, or -1 once every queue is drained
       int code = -1, m = tick + first_claims;
@@ -711,12 +934,19 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     }
     __syncthreads();
     for (int j2 = 0; j2 < npairs; j2 += 2) {
-      // past the end the last pair is loaded again (unused): the same loads on every step
-      const int ja = j2 + 2 < npairs ? j2 + 2 : npairs - 1, jb = j2 + 3 < npairs ? j2 + 3 : npairs - 1;
       // blocks 2ja .. 2jb + 1 lie in one chunk of 64 (2ja is a multiple of 4, or jb = ja)
+      const int ja = j2 + 2 < npairs ? j2 + 2 : npairs - 1, jb = j2 + 3 < npairs ? j2 + 3 : npairs - 1;
       pf_ids_advance(ids, row, ja >> 5, nblk);
-      pf_load<KV, D>(sa, a, ids, 2 * ja, nblk, nkeys, kvh, status);
-      pf_load<KV, D>(sb, a, ids, 2 * jb, nblk, nkeys, kvh, status);
+      const PfPair pa = pf_pair<KV, IMG>(a, ids, 2 * ja, nblk, nkeys, kvh, status);
+      const PfPair pb = pf_pair<KV, IMG>(a, ids, 2 * jb, nblk, nkeys, kvh, status);
+      PfStage<KV, D> sa, sb;
+      if constexpr (IMG) {
+        if (j2 + 2 < npairs) pf_dma<KV, D>(kimg, vimg, pa.t0, pa.t1, pl, lds0 + ((j2 + 2) & 3) * C::BUF);
+        if (j2 + 3 < npairs) pf_dma<KV, D>(kimg, vimg, pb.t0, pb.t1, pl, lds0 + ((j2 + 3) & 3) * C::BUF);
+      } else {
+        pf_load<KV, D>(sa, a, pa.t0, pa.t1);
+        pf_load<KV, D>(sb, a, pb.t0, pb.t1);
+      }
       PfOps<KV, D> o;
       if (j2 < wpairs) {
         // pair j2 + 1's K pieces are read during pair j2's P . V (even when
@@ -729,24 +959,25 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
         pf_scores<KV, D, false>(o, qb, s0, s1, ba);
         finish(std::true_type{}, j2, s0, s1, m0, o, ba, bb);
       }
-      // the next pairs are staged between this step's two: with their registers
-      // free, pair j2 + 1's V tiles fit beside its softmax and are read during
-      // its score MFMAs (pair j2's V tiles are read after its softmax, whose
-      // registers the staged loads still hold)
       const PfMeta m1cur = m1;
-      if (j2 + 2 < npairs) {
-        pf_store<KV, D>(sa, lds + ((j2 + 2) & 3) * C::BUF, status);
-        m0 = pf_meta<KV, D>(sa, a.scale_log2);
-      }
-      if (j2 + 3 < npairs) {
-        pf_store<KV, D>(sb, lds + ((j2 + 3) & 3) * C::BUF, status);
-        m1 = pf_meta<KV, D>(sb, a.scale_log2);
+      if constexpr (!IMG) {
+        if (j2 + 2 < npairs)
+          pf_store<KV, D>(sa, pf_vs(pa, 0), pf_vs(pa, 1), pa.live, lds + ((j2 + 2) & 3) * C::BUF, status);
+        if (j2 + 3 < npairs)
+          pf_store<KV, D>(sb, pf_vs(pb, 0), pf_vs(pb, 1), pb.live, lds + ((j2 + 3) & 3) * C::BUF, status);
+        m0 = pf_meta(pa, a.scale_log2);
+        m1 = pf_meta(pb, a.scale_log2);
       }
       if (j2 + 1 < wpairs) {
         const uint8_t* bb = lds + ((j2 + 1) & 3) * C::BUF;
         f32x4 s0[kPfNT], s1[kPfNT];
         pf_scores<KV, D, true>(o, qb, s0, s1, bb);
         finish(std::false_type{}, j2 + 1, s0, s1, m1cur, o, bb, bb);
+      }
+      if constexpr (IMG) {
+        pf_dma_wait();  // the next step's tiles are in LDS (and the fp8 scales in registers)
+        m0 = pf_meta(pa, a.scale_log2);
+        m1 = pf_meta(pb, a.scale_log2);
       }
       __syncthreads();
     }
@@ -777,10 +1008,21 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   if (status) atomicOr(a.hdr + kHdrStatus, status);  // error paths only
 }
 
+template <KvType KV, int D>
+void* prefill_fn(bool img) {
+  return img ? reinterpret_cast<void*>(&prefill_kernel<KV, D, true>)
+             : reinterpret_cast<void*>(&prefill_kernel<KV, D, false>);
+}
+
 template <KvType KV>
-void* prefill_for_d(int D) {
-  return D == 64 ? reinterpret_cast<void*>(&prefill_kernel<KV, 64>)
-                 : reinterpret_cast<void*>(&prefill_kernel<KV, 128>);
+void* prefill_for_d(int D, bool img) {
+  return D == 64 ? prefill_fn<KV, 64>(img) : prefill_fn<KV, 128>(img);
+}
+
+template <KvType KV>
+void* prep_for_d(int D) {
+  return D == 64 ? reinterpret_cast<void*>(&prefill_prep_kernel<KV, 64>)
+                 : reinterpret_cast<void*>(&prefill_prep_kernel<KV, 128>);
 }
 
 }  // namespace
@@ -789,14 +1031,21 @@ hipError_t launch_prefill(const PrefillArgs& a, KvType kv, hipStream_t s) {
   if (a.B == 0 || a.items_max == 0) return hipSuccess;
   PrefillArgs args = a;
   void* params[] = {&args};
-  hipError_t e = hipLaunchKernel(reinterpret_cast<void*>(&prefill_plan_kernel), dim3(1), dim3(kPlanThreads), params,
-                                 0, s);
+  const bool img = a.v_img != nullptr;
+  hipError_t e;
+  if (img) {  // the plan and the image in one launch
+    const int64_t cps = (a.max_blocks + kImgBlocks - 1) / kImgBlocks;
+    void* prep = kv == KvType::FP8 ? prep_for_d<KvType::FP8>(a.D) : prep_for_d<KvType::BF16>(a.D);
+    e = hipLaunchKernel(prep, dim3((unsigned)(1 + a.B * cps)), dim3(kPlanThreads), params, 0, s);
+  } else {
+    e = hipLaunchKernel(reinterpret_cast<void*>(&prefill_plan_kernel), dim3(1), dim3(kPlanThreads), params, 0, s);
+  }
   if (e != hipSuccess) return e;
-  void* fn = kv == KvType::FP8 ? prefill_for_d<KvType::FP8>(a.D) : prefill_for_d<KvType::BF16>(a.D);
+  void* fn = kv == KvType::FP8 ? prefill_for_d<KvType::FP8>(a.D, img) : prefill_for_d<KvType::BF16>(a.D, img);
   // the persistent grid: resident workgroups per CU times the CUs, a multiple
   // of 8 (the queues' start assumes it), no more than the units need
-  static std::atomic<int> per_cu_memo[4];  // per kernel, queried once
-  const int slot = (kv == KvType::FP8 ? 2 : 0) + (a.D == 128 ? 1 : 0);
+  static std::atomic<int> per_cu_memo[8];  // per kernel, queried once
+  const int slot = (kv == KvType::FP8 ? 4 : 0) + (a.D == 128 ? 2 : 0) + (img ? 1 : 0);
   int per_cu = per_cu_memo[slot].load(std::memory_order_relaxed);
   if (per_cu == 0) {
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kPfThreads, 0);

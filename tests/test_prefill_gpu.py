@@ -25,6 +25,19 @@ def lib():
     return _lib
 
 
+@pytest.fixture(params=["image", "staging"])
+def path(request, monkeypatch):
+    """The attention kernel's two ways of bringing K and V tiles to LDS: direct
+    loads from the converted image (the default whenever the image fits), or
+    registers and conversion in the kernel (PDA_PREFILL_IMAGE_MAX_MB = 0, as
+    for an image larger than the cap)."""
+    if request.param == "staging":
+        monkeypatch.setenv("PDA_PREFILL_IMAGE_MAX_MB", "0")
+    else:
+        monkeypatch.delenv("PDA_PREFILL_IMAGE_MAX_MB", raising=False)
+    return request.param
+
+
 def wl(hq, hkv, d, kv, cfg=40):
     return W.Workload(f"prefill_{hq}_{hkv}_{d}_{kv}", 1, hq, hkv, d, "bf16", kv, ("uniform", 1, 1), cfg_id=cfg,
                       prefill_frac=1.0)
@@ -67,7 +80,7 @@ GROUPS = [(4, 4), (4, 2), (6, 2), (8, 2), (14, 2), (8, 1), (16, 1)]
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("hq,hkv", GROUPS)
-def test_prefill_matches_oracle(lib, kv, d, hq, hkv):
+def test_prefill_matches_oracle(lib, path, kv, d, hq, hkv):
     """Full prefills (n = L) of ragged sequences spanning several tiles, and
     chunked prefills (n < L) of the same caches."""
     lens = [1, 15, 16, 17, 33, 100, 257, 700]
@@ -103,12 +116,29 @@ def test_prefill_queues_more_units_than_workgroups(lib, kv, hq, hkv, d):
 
 
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+@pytest.mark.parametrize("hq,hkv,d", [(28, 4, 128), (8, 2, 64), (16, 1, 128), (15, 5, 64)])
+def test_prefill_paths_agree_bitwise(lib, monkeypatch, kv, hq, hkv, d):
+    """The image and staging paths convert V (and fp8 K) with the same
+    functions and run the same products in the same order: their outputs
+    agree bit for bit, and the image path matches the oracle."""
+    pin = W.generate_prefill(wl(hq, hkv, d, kv), DEV, seq_lens=[40, 700, 129, 5, 300],
+                             q_counts=[40, 700, 2, 5, 17])
+    monkeypatch.delenv("PDA_PREFILL_IMAGE_MAX_MB", raising=False)
+    img = run(lib, pin, torch.float32)
+    monkeypatch.setenv("PDA_PREFILL_IMAGE_MAX_MB", "0")
+    stg = run(lib, pin, torch.float32)
+    assert torch.equal(img.view(torch.int32), stg.view(torch.int32))
+    U.assert_close(U.out_to_f64(img), reference(pin), kv, f"paths Hq{hq} Hkv{hkv} D{d} {kv}")
+    assert lib.read_device_status() == 0
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
 def test_prefill_bf16_output(lib, kv):
     pin = W.generate_prefill(wl(28, 4, 128, kv), DEV, seq_lens=[40, 300, 129], q_counts=[40, 300, 2])
     check(lib, pin, f"bf16 out {kv}", out_dtype=torch.bfloat16)
 
 
-def test_prefill_edge_counts(lib):
+def test_prefill_edge_counts(lib, path):
     """Empty sequences, queries beyond the cache (n > L: positions below 0 give
     zeros), an empty cache with queries, single tokens, and a sequence long
     enough for many tiles."""
@@ -122,7 +152,7 @@ def test_prefill_edge_counts(lib):
     assert not got[off[2]:off[3]].any()           # sequence 2 has no cached token
 
 
-def test_prefill_many_tiny_sequences(lib):
+def test_prefill_many_tiny_sequences(lib, path):
     """More sequences than the plan kernel has threads: 2500 sequences of 0 to
     3 queries each."""
     rng = np.random.default_rng(7)
@@ -153,7 +183,7 @@ def test_prefill_untouched_rows_and_determinism(lib):
     U.assert_close(outs[0][3:3 + T].double().numpy(), reference(pin), "bf16", "offset rows")
 
 
-def test_prefill_status_bits(lib):
+def test_prefill_status_bits(lib, path):
     pin = W.generate_prefill(wl(8, 2, 128, "bf16"), DEV, seq_lens=[40, 70], q_counts=[40, 70])
     c = pin.cache
     out = torch.full(pin.q.shape, 7.0, dtype=torch.float32, device=DEV)
@@ -201,7 +231,7 @@ def test_prefill_softmax_scales(lib, scale):
     assert lib.read_device_status() == 0
 
 
-def test_prefill_value_range_flag(lib):
+def test_prefill_value_range_flag(lib, path):
     """P . V runs in fp16: a live V value beyond +-65504 saturates and sets
     status bit 16; values in range, and poison in dead slots, do not."""
     pin = W.generate_prefill(wl(8, 2, 128, "bf16"), DEV, seq_lens=[40, 70], q_counts=[40, 70])
