@@ -47,8 +47,9 @@
 //   operand, so they add exactly the fp16 weights the product uses. The K scale
 //   of an fp8 block goes on its logits. LDS operand reads sit beside matrix
 //   work: the second pair of a step has its K operands read between the first
-//   pair's P . V MFMAs and its V operands between its own score MFMAs; half of
-//   the first pair's V operands are read during its softmax.
+//   pair's P . V MFMAs, and every pair its V operands between its own score
+//   MFMAs (on the staging path, where the staged registers are still live
+//   then, the first pair reads half of them during its softmax instead).
 // * Causal masking selects per column (a key is seen iff it is at or before the
 //   column's position); V rows of keys past the tile's last position are zeroed,
 //   so NaN poison in unused slots never reaches the products. Only pairs that
@@ -871,23 +872,26 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     // pair j2's weights and P . V from its scores and V tiles, on the masked
     // path where some column of the wave does not see every key of the pair, or
     // a key is past the tile; KNEXT: the next pair's K pieces are read from kbuf
-    // during the P . V
-    auto finish = [&](auto knext, int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT], const PfMeta& m,
-                      PfOps<KV, D>& o, const uint8_t* vbuf, const uint8_t* kbuf) {
+    // during the P . V; VMID: half of the V tiles are read during the softmax
+    // and half before the P . V (otherwise all were read during the scores)
+    auto finish = [&](auto knext, auto vmid, int j2, const f32x4 (&s0)[kPfNT], const f32x4 (&s1)[kPfNT],
+                      const PfMeta& m, PfOps<KV, D>& o, const uint8_t* vbuf, const uint8_t* kbuf) {
       constexpr bool KNEXT = decltype(knext)::value;
+      constexpr bool VMID = decltype(vmid)::value;
+      constexpr int VFROM = VMID ? C::MT / 2 : C::MT;
       const int key0 = 32 * j2;
       int see[kPfNT];
       f16x8 ph[kPfNT];
       if (key0 + 31 <= pos_lo && m.live >= 32) {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = 32;
-        pf_softmax<KV, D, false, KNEXT>(s0, s1, m.c0, m.c1, see, acc, rows, ph, o, vbuf);
-        pf_pv<KV, D, false, KNEXT, KNEXT ? C::MT / 2 : C::MT>(o, ph, 32, acc, vbuf, kbuf);
+        pf_softmax<KV, D, false, VMID>(s0, s1, m.c0, m.c1, see, acc, rows, ph, o, vbuf);
+        pf_pv<KV, D, false, KNEXT, VFROM>(o, ph, 32, acc, vbuf, kbuf);
       } else {
 #pragma unroll
         for (int n = 0; n < kPfNT; ++n) see[n] = vis[n] - key0 < m.live ? vis[n] - key0 : m.live;
-        pf_softmax<KV, D, true, KNEXT>(s0, s1, m.c0, m.c1, see, acc, rows, ph, o, vbuf);
-        pf_pv<KV, D, true, KNEXT, KNEXT ? C::MT / 2 : C::MT>(o, ph, m.live, acc, vbuf, kbuf);
+        pf_softmax<KV, D, true, VMID>(s0, s1, m.c0, m.c1, see, acc, rows, ph, o, vbuf);
+        pf_pv<KV, D, true, KNEXT, VFROM>(o, ph, m.live, acc, vbuf, kbuf);
       }
     };
 
@@ -956,8 +960,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
         for (int i = 0; i < C::MT; ++i) pf_kread<KV, D>(ba, o, i);
         f32x4 s0[kPfNT], s1[kPfNT];
-        pf_scores<KV, D, false>(o, qb, s0, s1, ba);
-        finish(std::true_type{}, j2, s0, s1, m0, o, ba, bb);
+        pf_scores<KV, D, IMG>(o, qb, s0, s1, ba);
+        finish(std::true_type{}, std::integral_constant<bool, !IMG>{}, j2, s0, s1, m0, o, ba, bb);
       }
       const PfMeta m1cur = m1;
       if constexpr (!IMG) {
@@ -972,7 +976,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
         const uint8_t* bb = lds + ((j2 + 1) & 3) * C::BUF;
         f32x4 s0[kPfNT], s1[kPfNT];
         pf_scores<KV, D, true>(o, qb, s0, s1, bb);
-        finish(std::false_type{}, j2 + 1, s0, s1, m1cur, o, bb, bb);
+        finish(std::false_type{}, std::false_type{}, j2 + 1, s0, s1, m1cur, o, bb, bb);
       }
       if constexpr (IMG) {
         pf_dma_wait();  // the next step's tiles are in LDS (and the fp8 scales in registers)
