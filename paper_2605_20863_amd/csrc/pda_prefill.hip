@@ -454,11 +454,14 @@ __device__ __forceinline__ PfPair pf_pair(const PrefillArgs& a, const PfIds& ids
   int64_t tile[2];
   int ok[2];
   float ks[2] = {1.f, 1.f}, vs[2] = {1.f, 1.f};
+  // ids are int32: p is a block iff 0 <= p < num_blocks, one unsigned 32-bit
+  // compare against min(num_blocks, 2^31) (scalar: there is no 64-bit scalar <)
+  const uint32_t nbu = a.num_blocks < (1ll << 31) ? (uint32_t)a.num_blocks : 0x80000000u;
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int p = __builtin_amdgcn_readlane(ids.id, (j0 + s) & 63);
     const bool inside = j0 + s < nblk;  // the block holds keys of the tile
-    ok[s] = inside && (uint64_t)(uint32_t)p < (uint64_t)a.num_blocks;
+    ok[s] = inside && (uint32_t)p < nbu;
     if (inside && !ok[s]) status |= kStatusBadBlock;
     tile[s] = uni64((int64_t)(ok[s] ? p : 0) * a.Hkv + kvh);
     if constexpr (KV == KvType::FP8) {  // raw: a block with no id takes scale 1 where they are used
@@ -821,7 +824,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   int un = (int)(blockIdx.x >> 3) * (8 / nq) + xq / nq, uq = q;  // current unit: index, queue
   int status = 0;
   for (int k = 0; un < qsize; ++k) {
-    const int item = un / hq, kvh = uq + nq * (un - item * hq);
+    const int item = un / hq, kvh = uni(uq + nq * (un - item * hq));
     int tick = 0;
     if (threadIdx.x == 0) tick = atomicAdd(a.hdr + kHdrPfQueue + q, 1);
     const int4 it = a.items[item];
@@ -854,8 +857,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     const int pos_hi = first + tok_hi;
 
     const int nkeys = first + nt > 0 ? first + nt : 0;  // keys up to the tile's last position
-    const int npairs = (nkeys + 31) / 32;
-    const int nblk = (nkeys + 15) / 16;
+    const int npairs = uni((nkeys + 31) / 32);
+    const int nblk = uni((nkeys + 15) / 16);
     // pairs this wave computes: those with a key at or before its last position
     const int wpairs = !wave_on || pos_hi < 0 ? 0 : (pos_hi / 32 + 1 < npairs ? pos_hi / 32 + 1 : npairs);
     const int32_t* row = a.block_table + (int64_t)b * a.max_blocks;
