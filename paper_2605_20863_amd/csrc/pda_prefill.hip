@@ -334,7 +334,10 @@ __device__ void pf_image(const PrefillArgs& a, int g) {
   const int nblk = (L + 15) / 16;
   const int nb = nblk - j0 < kImgBlocks ? nblk - j0 : kImgBlocks;
   if (nb <= 0) return;
-  constexpr int UT = 2 * D;  // 8-element pieces of a tile
+  // a piece is 16 bytes of the cache: 8 bf16 values, or 16 fp8 codes (for V a
+  // whole dim row of the block, for K 16 dims of one token)
+  constexpr int EPP = KV == KvType::FP8 ? 16 : 8;  // elements per piece
+  constexpr int UT = 16 * D / EPP;                 // pieces of a tile
   const int vpieces = a.Hkv * UT;
   const int per_blk = KV == KvType::FP8 ? 2 * vpieces : vpieces;  // fp8: V pieces, then K pieces
   const int total = nb * per_blk;
@@ -343,10 +346,9 @@ __device__ void pf_image(const PrefillArgs& a, int g) {
   const uint8_t* vc = static_cast<const uint8_t*>(a.v_cache);
   uint8_t* ki = static_cast<uint8_t*>(a.k_img);
   uint8_t* vi = static_cast<uint8_t*>(a.v_img);
-  using Unit = typename std::conditional<KV == KvType::FP8, u32x2, u32x4>::type;
   int ovf = 0;
   for (int u0 = (int)threadIdx.x; u0 < total; u0 += kImgBatch * kPlanThreads) {
-    Unit x[kImgBatch];
+    u32x4 x[kImgBatch];
     int64_t tile[kImgBatch];
     int e[kImgBatch], live[kImgBatch], kind[kImgBatch];  // kind: 0 none, 1 V, 2 K
     float vs[kImgBatch];
@@ -366,7 +368,7 @@ __device__ void pf_image(const PrefillArgs& a, int g) {
       tile[i] = (int64_t)p * a.Hkv + h;
       live[i] = L - 16 * (j0 + jj);
       kind[i] = is_k ? 2 : 1;
-      x[i] = *reinterpret_cast<const Unit*>((is_k ? kc : vc) + tile[i] * C::GTILE + e[i] * C::UB);
+      x[i] = *reinterpret_cast<const u32x4*>((is_k ? kc : vc) + tile[i] * C::GTILE + e[i] * 16);
       vs[i] = 1.f;
       if constexpr (KV == KvType::FP8) {
         if (!is_k) vs[i] = a.kv_scales[a.num_blocks * a.Hkv + tile[i]];
@@ -375,16 +377,19 @@ __device__ void pf_image(const PrefillArgs& a, int g) {
 #pragma unroll
     for (int i = 0; i < kImgBatch; ++i) {
       if (kind[i] == 0) continue;
-      // piece e of a V tile: dim row e / 2, tokens 8 (e % 2) .. + 7 of the block
-      const int k0 = 8 * (e[i] & 1);
-      uint8_t* dst = (kind[i] == 2 ? ki : vi) + tile[i] * C::TILEB + e[i] * 16;
-      u32x4 y;
+      uint8_t* dst = (kind[i] == 2 ? ki : vi) + tile[i] * C::TILEB + e[i] * (2 * EPP);
       if constexpr (KV == KvType::FP8) {
-        y = kind[i] == 2 ? fp8x8_to_bf16(x[i]) : fp8x8_to_half(x[i], vs[i], k0, live[i], ovf);
-      } else {
-        y = bf16x8_to_half(x[i], k0, live[i], ovf);
+        const u32x2 lo{x[i].x, x[i].y}, hi{x[i].z, x[i].w};
+        if (kind[i] == 2) {  // K: 16 dims of one token
+          *reinterpret_cast<u32x4*>(dst) = fp8x8_to_bf16(lo);
+          *reinterpret_cast<u32x4*>(dst + 16) = fp8x8_to_bf16(hi);
+        } else {             // V: dim row e, tokens 0 .. 15
+          *reinterpret_cast<u32x4*>(dst) = fp8x8_to_half(lo, vs[i], 0, live[i], ovf);
+          *reinterpret_cast<u32x4*>(dst + 16) = fp8x8_to_half(hi, vs[i], 8, live[i], ovf);
+        }
+      } else {  // V piece e: dim row e / 2, tokens 8 (e % 2) .. + 7
+        *reinterpret_cast<u32x4*>(dst) = bf16x8_to_half(x[i], 8 * (e[i] & 1), live[i], ovf);
       }
-      *reinterpret_cast<u32x4*>(dst) = y;
     }
   }
   if (ovf) atomicOr(a.hdr + kHdrStatus, kStatusHalfRange);
@@ -853,15 +858,15 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     const int tok_hi_raw = (kPfWaveCols * w + kPfWaveCols - 1) / a.G;
     const int tok_hi = tok_hi_raw < nt - 1 ? tok_hi_raw : nt - 1;
     const bool wave_on = tok_lo < nt;
-    const int pos_lo = first + tok_lo;  // this wave's first and last query positions
-    const int pos_hi = first + tok_hi;
+    const int pos_lo = uni(first + tok_lo);  // this wave's first and last query positions
+    const int pos_hi = uni(first + tok_hi);
 
     const int nkeys = first + nt > 0 ? first + nt : 0;  // keys up to the tile's last position
     const int npairs = uni((nkeys + 31) / 32);
     const int nblk = uni((nkeys + 15) / 16);
     // pairs this wave computes: those with a key at or before its last position
-    const int wpairs = !wave_on || pos_hi < 0 ? 0 : (pos_hi / 32 + 1 < npairs ? pos_hi / 32 + 1 : npairs);
-    const int32_t* row = a.block_table + (int64_t)b * a.max_blocks;
+    const int wpairs = uni(!wave_on || pos_hi < 0 ? 0 : (pos_hi / 32 + 1 < npairs ? pos_hi / 32 + 1 : npairs));
+    const int32_t* row = a.block_table + uni64((int64_t)b * a.max_blocks);
 
     f32x4 acc[C::MT][kPfNT];
 #pragma unroll
