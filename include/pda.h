@@ -372,6 +372,17 @@ typedef struct pda_prefill_problem {
  * the P . V product as fp16 (11 significant bits; bf16 V converts exactly),
  * accumulated in fp32. A live V value beyond +-65504 saturates (status bit 16).
  *
+ * Image: each call first converts every cache tile that its sequences read
+ * into the stream's workspace, in the products' operand types (V to fp16, and
+ * for an fp8 cache K codes to bf16), indexed like the cache; the attention
+ * kernel then copies tiles from that image straight into LDS. The image takes
+ * num_blocks * num_kv_heads * 16 * head_dim * 2 bytes (twice that for an fp8
+ * cache). When that exceeds the environment variable PDA_PREFILL_IMAGE_MAX_MB
+ * (MiB, read on every call; default 8192), when a stream being captured into a
+ * HIP graph has too small a workspace for it, or when its allocation fails, the
+ * kernel converts each tile in registers instead. Both ways give bit-identical
+ * outputs.
+ *
  * Device-checked: lengths are clamped as in decode (status bit 1), block-table
  * entries outside [0, num_blocks) are skipped (bit 2), and offsets that are not
  * non-decreasing within [0, T] make the call write nothing (bit 8).
@@ -381,7 +392,8 @@ typedef struct pda_prefill_problem {
  * 16 bytes, the int32 and f32 arrays 4), or more than INT32_MAX / 8 work units
  * (tiles of 256 / G query tokens times KV heads); PDA_EUNSUPPORTED for
  * head_dim not in {64, 128}, block_size != 16, G > 16, or an f32 cache. Uses
- * the stream's workspace (16 bytes per work item of 256 / G query tokens).
+ * the stream's workspace: 16 bytes per work item of 256 / G query tokens, plus
+ * the image described above.
  */
 int pda_paged_prefill_attention(const void* q,
                                 const int32_t* q_offsets,
