@@ -429,8 +429,8 @@ def paged_prefill_attention(q, q_offsets, k_cache, v_cache, block_table, seq_len
     q_offsets[b] .. q_offsets[b + 1] - 1 (int32 [B + 1]) are the last tokens of
     sequence b, whose cache holds seq_lens[b] tokens; cache layouts as for
     paged_decode_attention. The call converts the cache tiles it reads into an
-    image in the stream's workspace (V as fp16, an fp8 cache's K as bf16; as
-    large as the cache's V tensor, twice that for fp8) unless that exceeds
+    image in the stream's workspace (V as fp16, an fp8 cache's K as bf16;
+    NB * Hkv * 16 * D * 2 bytes, twice that for fp8) unless that exceeds
     PDA_PREFILL_IMAGE_MAX_MB (default 8192), in which case the kernel converts
     tiles in registers; the results are the same bit for bit.
     """
