@@ -180,6 +180,48 @@ def test_graph_prefill_more_units_than_workgroups(lib):
 
 
 @pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_graph_prefill_capture_falls_back_to_staging(lib, monkeypatch, kv):
+    """A stream whose workspace was sized by a staging-path call (image cap 0)
+    is captured with the image allowed again: a capture cannot grow the
+    workspace for the image, so the recorded call converts tiles in registers.
+    Every replay matches an eager image-path call on another stream bit for
+    bit, and the first matches the oracle."""
+    w = W.WORKLOADS["logprob_gqa7b_bf16"].replace(name=f"graph_prefill_staging_{kv}", num_seqs=6, kv_dtype=kv,
+                                                  lengths=("lognormal", 300, 0.5, 16, 700))
+    pin = W.generate_prefill(w, DEV)
+    c = pin.cache
+    out_g = torch.empty(pin.q.shape, dtype=torch.float32, device=DEV)
+    out_e = torch.empty_like(out_g)
+
+    def call(out):
+        lib.paged_prefill_attention(pin.q, pin.q_offsets, c.k_cache, c.v_cache, c.block_table, c.seq_lens,
+                                    c.kv_scales, out, c.softmax_scale, max_seq_len=c.layout.max_seq_len)
+
+    s = torch.cuda.Stream(DEV)
+    monkeypatch.setenv("PDA_PREFILL_IMAGE_MAX_MB", "0")
+    with torch.cuda.stream(s):
+        call(out_g)  # sizes this stream's workspace for the staging path only
+    s.synchronize()
+    monkeypatch.delenv("PDA_PREFILL_IMAGE_MAX_MB")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        call(out_g)
+    for r in range(REPLAYS):
+        with torch.cuda.stream(s):
+            pin.q.copy_(fresh_q(pin.q, 700 + r))
+            g.replay()
+        s.synchronize()
+        call(out_e)  # the current stream: its own workspace, room for the image
+        torch.cuda.synchronize()
+        print(f"[graph] replay {r}", flush=True)
+        assert torch.equal(bits(out_g), bits(out_e)), f"replay {r} differs from the eager image-path call"
+        if r == 0:
+            ref = U.oracle_prefill_whole(pin, f"graph prefill staging {kv}")
+            U.assert_close(U.out_to_f64(out_g), ref, kv, f"graph prefill staging {kv}")
+    assert lib.read_device_status() == 0
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
 def test_graph_append_decode_loop(lib, kv):
     """A serving loop as one graph: append each sequence's new key and value
     at its position, then attend with the new length. Positions and lengths
