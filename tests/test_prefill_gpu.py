@@ -250,6 +250,31 @@ def test_prefill_value_range_flag(lib, path):
     assert torch.isfinite(out).all()
 
 
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_prefill_shared_blocks(lib, path, kv):
+    """Sequences that share their leading physical blocks, as the rollouts of
+    one GRPO group share their prompt's: on the image path several workgroups
+    convert the same tiles (writing the same bytes). Against the oracle with
+    the same shared table."""
+    pin = W.generate_prefill(wl(28, 4, 128, kv), DEV, seq_lens=[300, 170, 260, 49, 333, 95],
+                             q_counts=[300, 170, 200, 49, 12, 95])
+    c = pin.cache
+    table = c.layout.block_table.copy()
+    shared = 3  # every sequence's first 48 tokens live in sequence 0's first three blocks
+    table[1:, :shared] = table[0, :shared]
+    tdev = torch.from_numpy(table).to(DEV)
+    out = torch.full(pin.q.shape, float("nan"), dtype=torch.float32, device=DEV)
+    lib.paged_prefill_attention(pin.q, pin.q_offsets, c.k_cache, c.v_cache, tdev, c.seq_lens, c.kv_scales, out,
+                                c.softmax_scale, max_seq_len=c.layout.max_seq_len)
+    torch.cuda.synchronize()
+    ref = oracle.paged_prefill_attention(
+        q=U.raw(pin.q), q_offsets=pin.offsets, k_cache=U.raw(c.k_cache), v_cache=U.raw(c.v_cache),
+        block_table=table, seq_lens=c.layout.seq_lens, softmax_scale=c.softmax_scale, q_dtype="bf16",
+        kv_dtype=kv, kv_scales=U.raw(c.kv_scales) if c.kv_scales is not None else None)
+    U.assert_close(U.out_to_f64(out), ref, kv, f"shared blocks {kv} ({path})")
+    assert lib.read_device_status() == 0
+
+
 def test_prefill_after_appends(lib):
     """A cache written token by token by the append kernel, then read by the
     prefill (the log-prob forward after rollout), against the oracle."""
